@@ -1,0 +1,40 @@
+/*
+ * vla_ops.h -- operator-level entry points of the VLA prefix library.
+ *
+ * The kernels that vla_prefix.h's block calls are built from, exposed one by
+ * one on caller-owned DEVICE pointers so each can be checked and timed alone.
+ * All are enqueued on `stream` (a hipStream_t as void*, NULL = the null
+ * stream) and return after launch; shapes are validated first and a rejected
+ * call launches nothing (VLA_ERR_INVALID_ARG / VLA_ERR_UNSUPPORTED).
+ * bf16 = bfloat16 bit patterns.  Row-major, innermost index last.
+ */
+#ifndef VLA_OPS_H
+#define VLA_OPS_H
+
+#include "vla_prefix.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* C[M][N] (fp32) = A[M][K] (bf16) * W[N][K]^T (bf16): the projection of every
+ * block's linear layers (bf16 MFMA, fp32 accumulation).  K % 64 == 0. */
+vla_status vla_op_gemm_bf16(const void *A, const void *W, float *C, int M, int N, int K, void *stream);
+
+/* Scaled dot-product attention of the blocks: o[B][L][H*dh] (bf16) =
+ * softmax(q k^T / sqrt(dh), causal mask if `causal`) v per (b, head), query
+ * head h reading KV head h / (H / Hkv).  q[B][H][L][dh], k[B][Hkv][L][dh],
+ * vt[B][Hkv][dh][ldvt] = V transposed (ldvt >= L, ldvt % 8 == 0), all bf16.
+ * dh in {64, 128}. */
+vla_status vla_op_attention_bf16(const void *q, const void *k, const void *vt, int ldvt, void *o, int B, int H,
+                                 int Hkv, int L, int dh, int causal, void *stream);
+
+/* y[M][d] (bf16) = RMSNorm(x[M][d] fp32; gain g[d] fp32, eps) -- or
+ * LayerNorm with shift b[d] when b != NULL.  d % 4 == 0, d <= 8192. */
+vla_status vla_op_norm_bf16(const float *x, const float *g, const float *b, float eps, void *y, int M, int d,
+                            void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* VLA_OPS_H */

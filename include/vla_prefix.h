@@ -1,0 +1,180 @@
+/*
+ * vla_prefix.h -- C ABI of the MI355X (gfx950) GPU-resident prefix of
+ * block-layer partitioned vision-language-action inference.
+ *
+ * What it computes (the paper's Sec. IV-B, Eq. (5)): for a partition point k
+ * (a count of whole transformer blocks), the boundary hidden state
+ *     h^(k) = B_k( ... B_1( E(x) ) )
+ * of one frame, together with the KV cache those k decoder blocks wrote, and
+ * hands both to pinned host memory: the cross-device transfer T(.) of Eq. (6),
+ * whose size for the hidden state is S_hid = B * L * D * b bytes (Eq. (11)).
+ * The visual encoder's transformer blocks (the ViT on the GPU, Sec. IV-A) are
+ * a second stack run by vla_run_encoder.  Frame identities survive the handoff
+ * (Sec. IV-C, producer-consumer pipeline), so a consumer can pair every
+ * boundary with its input frame while the GPU already works on the next one.
+ *
+ * Conventions for every call:
+ *  - Every function returns vla_status; nothing throws or aborts across the
+ *    ABI.  On failure the context keeps a message (vla_last_error) until the
+ *    next call on it succeeds.
+ *  - Validation happens before any launch: a rejected call enqueues nothing.
+ *  - Tensors are row-major, innermost index last.  bf16 means IEEE bfloat16
+ *    bit patterns (uint16_t); f32 means IEEE binary32.
+ *  - "host or device" pointers are classified with hipPointerGetAttributes.
+ *  - A context belongs to one device and is not thread-safe: serialise calls
+ *    on one context externally.
+ *  - Streams are hipStream_t values passed as void*.  NULL asks the library
+ *    to create its own non-blocking streams (default priority).
+ */
+#ifndef VLA_PREFIX_H
+#define VLA_PREFIX_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct vla_ctx vla_ctx;
+
+typedef enum {
+  VLA_OK = 0,
+  VLA_ERR_INVALID_ARG = -1, /* NULL pointer, bad enum, k_begin > k_end, ... */
+  VLA_ERR_SHAPE = -2,       /* sizes exceed the context's limits or a buffer is too small */
+  VLA_ERR_NOT_LOADED = -3,  /* a block in the requested range has no weights */
+  VLA_ERR_NOT_PINNED = -4,  /* an output host buffer is not page-locked (hipHostMalloc) */
+  VLA_ERR_OOM = -5,         /* the caller's device arena is smaller than vla_query_sizes asked */
+  VLA_ERR_TIMEOUT = -6,     /* vla_wait_boundary gave up; the work is still in flight */
+  VLA_ERR_HIP = -7,         /* a HIP runtime call failed; vla_last_error has its text */
+  VLA_ERR_UNSUPPORTED = -8, /* a shape the kernels do not implement (see vla_stack_cfg) */
+  VLA_ERR_UNKNOWN_FRAME = -9 /* no in-flight or finished frame has this id */
+} vla_status;
+
+typedef enum { VLA_BF16 = 0, VLA_F32 = 1 } vla_dtype;
+typedef enum { VLA_STACK_LLM = 0, VLA_STACK_ENC = 1 } vla_stack;
+
+/*
+ * Shape of one stack of transformer blocks held on the GPU.
+ *  n_blocks   blocks resident on the GPU (the largest partition point the
+ *             context can run; GPU memory grows with it, Table V's trade-off).
+ *  max_tokens largest tokens per sequence L; max_batch largest batch B
+ *             (images for the encoder).  Workspace is sized for B*L rows.
+ *  LLM stacks: RMSNorm, RoPE (rotate-half, angles from rope_base), causal
+ *             attention with grouped KV heads, SwiGLU MLP, no biases.
+ *  Encoder stacks: LayerNorm (with shift), bidirectional attention, GELU
+ *             (erf) MLP, biases on every projection.
+ *  dtype      VLA_BF16: bf16 weights and activations, fp32 accumulation,
+ *             fp32 residual stream and reductions.  VLA_F32: the fp32 debug
+ *             path, no reduced precision anywhere.
+ * bf16 stacks need head_dim in {64, 128} and d_model, n_heads*head_dim,
+ * d_ff multiples of 64; fp32 stacks need head_dim <= 128 and even.
+ */
+typedef struct {
+  int n_blocks, d_model, n_heads, n_kv_heads, head_dim, d_ff;
+  int max_tokens, max_batch;
+  int norm_is_layernorm, mlp_is_gelu, causal, use_rope, has_bias;
+  float norm_eps, rope_base;
+  vla_dtype dtype;
+} vla_stack_cfg;
+
+/*
+ * Host weights of one block, nn.Linear convention W[out][in], element type
+ * = the stack's dtype (norm gains/shifts and biases too).  Shapes, with
+ * d = d_model, hd = n_heads*head_dim, kvd = n_kv_heads*head_dim, F = d_ff:
+ *   w_q[hd][d] w_k[kvd][d] w_v[kvd][d] w_o[d][hd]   norm1_g[d] norm2_g[d]
+ *   LLM:     w_gate[F][d] w_up[F][d] w_down[d][F]
+ *   encoder: w_fc1[F][d] b_fc1[F] w_fc2[d][F] b_fc2[d] b_qkv[hd+2kvd] b_o[d]
+ *            norm1_b[d] norm2_b[d]
+ * Fields a stack does not use must be NULL.  The library copies (and
+ * re-lays-out) everything into its arena; the caller may free them on return.
+ */
+typedef struct {
+  const void *w_q, *w_k, *w_v, *w_o, *b_qkv, *b_o;
+  const void *w_gate, *w_up, *w_down;
+  const void *w_fc1, *b_fc1, *w_fc2, *b_fc2;
+  const void *norm1_g, *norm1_b, *norm2_g, *norm2_b;
+} vla_block_weights;
+
+/*
+ * Caller-owned, caller-allocated PINNED host memory receiving one frame's
+ * handoff.  hidden: [B][L][d] in out_dtype (bf16 requires a bf16 stack).
+ * kv: [k_end-k_begin][2][B][n_kv_heads][L][head_dim] in the stack's dtype,
+ * K after RoPE, V as projected; may be NULL (kv_bytes 0) to skip the KV copy.
+ * frame_id is written by the library.  The buffers must stay untouched until
+ * vla_wait_boundary(frame_id) returns VLA_OK.
+ */
+typedef struct {
+  void *hidden;
+  size_t hidden_bytes;
+  void *kv;
+  size_t kv_bytes;
+  vla_dtype out_dtype;
+  uint64_t frame_id;
+} vla_boundary;
+
+/* Device arena bytes a context needs for these stacks (enc may be NULL), and
+ * the hidden / KV handoff sizes of a run of k blocks at batch B, length L. */
+vla_status vla_query_sizes(const vla_stack_cfg *llm, const vla_stack_cfg *enc, int B, int L, int k,
+                           size_t *arena_bytes, size_t *hidden_bytes, size_t *kv_bytes);
+
+/* Create a context on `device` over a caller-owned device arena of
+ * arena_bytes (>= vla_query_sizes' answer; the library never calls hipMalloc
+ * after this point).  llm may be NULL for an encoder-only context and vice
+ * versa.  compute_stream runs the blocks; copy_stream runs the handoff. */
+vla_status vla_create(const vla_stack_cfg *llm, const vla_stack_cfg *enc, int device, void *dev_arena,
+                      size_t arena_bytes, void *compute_stream, void *copy_stream, vla_ctx **out);
+
+/* Copy block `block` (0-based, < n_blocks) of stack `which` from host memory
+ * into the arena.  Synchronous.  Re-loading a block replaces it. */
+vla_status vla_load_block_weights(vla_ctx *ctx, vla_stack which, int block, const vla_block_weights *w);
+
+/* Encoder: all n_blocks encoder blocks over patches[n_img][L_img][d_enc]
+ * (host or device, stack dtype), each image attended independently; result
+ * to out_dev[n_img][L_img][d_enc] (device, stack dtype).  Enqueued on the
+ * compute stream; returns after launch. */
+vla_status vla_run_encoder(vla_ctx *ctx, uint64_t frame_id, const void *patches, int n_img, int L_img,
+                           void *out_dev);
+
+/* Prefix: decoder blocks [0, k) over tokens[B][L][d] (host or device, stack
+ * dtype) as one causal prefill; the boundary h^(k) and the KV cache of the k
+ * blocks are copied to `out` on the copy stream, each layer's KV as soon as
+ * that layer has written it.  k = 0 hands back the input (Eq. (5) with no
+ * blocks).  Enqueued; returns after launch.  Equivalent to
+ * vla_run_blocks(ctx, frame_id, tokens, B, L, 0, k, out). */
+vla_status vla_run_prefix(vla_ctx *ctx, uint64_t frame_id, const void *tokens, int B, int L, int k,
+                          vla_boundary *out);
+
+/* Decoder blocks [k_begin, k_end) over an intermediate state h^(k_begin)
+ * given as `tokens` (positions still start at 0): one stage of the block
+ * pipeline of Eq. (6).  KV in `out` covers the blocks run. */
+vla_status vla_run_blocks(vla_ctx *ctx, uint64_t frame_id, const void *tokens, int B, int L, int k_begin,
+                          int k_end, vla_boundary *out);
+
+/* Block the host until frame_id's handoff is complete (its host buffers are
+ * then readable), or timeout_ms elapses (< 0: wait forever). */
+vla_status vla_wait_boundary(vla_ctx *ctx, uint64_t frame_id, int timeout_ms);
+
+/* Stage times of a completed frame (Eq. (8)-(9)): t_gpu_ms from the start of
+ * the frame's prefix to its last block on the compute stream (T_G); t_xfer_ms
+ * of the boundary hidden-state copy alone (T_X); t_total_ms from the prefix
+ * start until every copy of the frame, KV included, finished.  Any output
+ * pointer may be NULL. */
+vla_status vla_frame_times(vla_ctx *ctx, uint64_t frame_id, float *t_gpu_ms, float *t_xfer_ms,
+                           float *t_total_ms);
+
+/* Bytes of the arena in use after the loads so far (weights + workspace). */
+vla_status vla_arena_used(const vla_ctx *ctx, size_t *bytes);
+
+const char *vla_status_string(vla_status s);
+/* Message of the last failure on ctx (ctx NULL: of the last failed
+ * vla_create / vla_query_sizes on this thread). */
+const char *vla_last_error(const vla_ctx *ctx);
+/* Wait for all enqueued work, then release the context (not the arena or
+ * caller streams). */
+void vla_destroy(vla_ctx *ctx);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* VLA_PREFIX_H */

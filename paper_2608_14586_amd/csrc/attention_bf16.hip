@@ -1,0 +1,256 @@
+// Flash-style attention for gfx950 (bf16 MFMA, fp32 online softmax).
+//
+// One workgroup = 4 waves = 128 queries of one (batch, head); each wave owns
+// 32 queries.  Keys advance in tiles of 64 staged in LDS (double buffered):
+// K as [key][dh] and V transposed as [dh][key], so every MFMA operand is a
+// contiguous LDS read.
+//
+// The scores are formed transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16
+// (A = K tile from LDS, B = the wave's Q held in registers).  In the 32x32
+// accumulator layout each lane then holds 16 keys of ONE query, so a query's
+// running max/sum needs a single cross-half exchange (lane ^ 32) instead of a
+// 32-lane reduction, and the probabilities already sit where the PV product
+// O^T = V^T P^T wants its B operand: a lane's 8 bf16 values for keys
+// {8i + 4h + j : i in {2s, 2s+1}, j < 4} feed k-step s directly, and the A
+// fragment (V^T) is read from LDS in the same key order.  The softmax runs in
+// base 2 with log2(e)/sqrt(dh) folded into one scale.
+//
+// Causal tiles are masked per element only on the diagonal; a wave skips the
+// MFMAs of key tiles entirely beyond its last query.  Query blocks are issued
+// heaviest first.
+
+#include <math.h>
+
+#include "kernels.h"
+
+namespace vla {
+namespace {
+
+constexpr int BQ = 128, BKV = 64, PADK = 8, PADV = 8;
+
+template <int DH, bool CAUSAL>
+__global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
+                                                        const bf16_t* __restrict__ vt, int ldvt,
+                                                        bf16_t* __restrict__ o, int B, int H, int Hkv, int L,
+                                                        float scale_log2) {
+  constexpr int LDK = DH + PADK, LDV = BKV + PADV;
+  constexpr int KCH = BKV * DH / 8 / 256;  // 16-byte chunks per thread, K tile
+  constexpr int VCH = DH * BKV / 8 / 256;  // V^T tile
+  constexpr int ND = DH / 32;
+  __shared__ __attribute__((aligned(16))) bf16_t sK[2][BKV * LDK];
+  __shared__ __attribute__((aligned(16))) bf16_t sV[2][DH * LDV];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int half = lane >> 5, li = lane & 31;
+  const int nqb = (L + BQ - 1) / BQ;
+  const int id = blockIdx.x;
+  const int rest = id % (H * B);
+  const int qb_r = id / (H * B);
+  const int qb = CAUSAL ? (nqb - 1 - qb_r) : qb_r;
+  const int h = rest % H, b = rest / H;
+  const int hk = h / (H / Hkv);
+  const int q0 = qb * BQ;
+  const int qw0 = q0 + wave * 32;
+  const int qi = qw0 + li;  // this lane's query
+
+  const bf16_t* qh = q + ((size_t)b * H + h) * L * DH;
+  const bf16_t* kh = k + ((size_t)b * Hkv + hk) * L * DH;
+  const bf16_t* vh = vt + ((size_t)b * Hkv + hk) * DH * (size_t)ldvt;
+
+  // Q fragments (B operand of S^T): query qi, dims ks*16 + half*8 .. +8
+  bf16x8 fq[DH / 16];
+#pragma unroll
+  for (int ks = 0; ks < DH / 16; ++ks) {
+    if (qi < L)
+      fq[ks] = *(const bf16x8*)(qh + (size_t)qi * DH + ks * 16 + half * 8);
+    else
+      fq[ks] = bf16x8{0, 0, 0, 0, 0, 0, 0, 0};
+  }
+
+  const int kend = CAUSAL ? min(L, q0 + BQ) : L;
+  const int ntiles = (kend + BKV - 1) / BKV;
+
+  u32x4 rk[KCH], rv[VCH];
+  auto gload = [&](int kb) {
+#pragma unroll
+    for (int c = 0; c < KCH; ++c) {
+      int idx = tid + c * 256;
+      int row = idx / (DH / 8), cc = idx % (DH / 8);
+      int key = kb + row;
+      rk[c] = key < L ? *(const u32x4*)(kh + (size_t)key * DH + cc * 8) : u32x4{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int c = 0; c < VCH; ++c) {
+      int idx = tid + c * 256;
+      int d = idx / (BKV / 8), cc = idx % (BKV / 8);
+      int key = kb + cc * 8;
+      const bf16_t* src = vh + (size_t)d * ldvt + key;
+      if (key + 8 <= L) {
+        rv[c] = *(const u32x4*)src;
+      } else {
+        uint32_t w[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          uint32_t lo = (key + 2 * e < L) ? src[2 * e] : 0u;
+          uint32_t hi = (key + 2 * e + 1 < L) ? src[2 * e + 1] : 0u;
+          w[e] = lo | (hi << 16);
+        }
+        rv[c] = u32x4{w[0], w[1], w[2], w[3]};
+      }
+    }
+  };
+  auto lstore = [&](int buf) {
+#pragma unroll
+    for (int c = 0; c < KCH; ++c) {
+      int idx = tid + c * 256;
+      int row = idx / (DH / 8), cc = idx % (DH / 8);
+      *(u32x4*)(&sK[buf][row * LDK + cc * 8]) = rk[c];
+    }
+#pragma unroll
+    for (int c = 0; c < VCH; ++c) {
+      int idx = tid + c * 256;
+      int d = idx / (BKV / 8), cc = idx % (BKV / 8);
+      *(u32x4*)(&sV[buf][d * LDV + cc * 8]) = rv[c];
+    }
+  };
+
+  f32x16 acc_o[ND];
+#pragma unroll
+  for (int t = 0; t < ND; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc_o[t][r] = 0.f;
+  float m_run = -INFINITY, l_part = 0.f;
+
+  gload(0);
+  lstore(0);
+  __syncthreads();
+
+  for (int it = 0; it < ntiles; ++it) {
+    const int buf = it & 1;
+    const int kb = it * BKV;
+    if (it + 1 < ntiles) gload(kb + BKV);
+    const bool active = !CAUSAL || kb <= qw0 + 31;
+    if (active && qw0 < L) {
+      // S^T for two 32-key tiles
+      f32x16 s[2];
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[t][r] = 0.f;
+        const bf16_t* kbase = &sK[buf][(t * 32 + li) * LDK + half * 8];
+#pragma unroll
+        for (int ks = 0; ks < DH / 16; ++ks) {
+          bf16x8 fk = *(const bf16x8*)(kbase + ks * 16);
+          s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fk, fq[ks], s[t], 0, 0, 0);
+        }
+      }
+      // mask, scale, tile max
+      const bool need_mask = (kb + BKV > L) || (CAUSAL && kb + BKV - 1 > qw0);
+      float mt = -INFINITY;
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          float x = s[t][r] * scale_log2;
+          if (need_mask) {
+            int key = kb + t * 32 + (r >> 2) * 8 + half * 4 + (r & 3);
+            bool ok = key < L && (!CAUSAL || key <= qi);
+            x = ok ? x : -INFINITY;
+          }
+          s[t][r] = x;
+          mt = fmaxf(mt, x);
+        }
+      mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+      const float m_new = fmaxf(m_run, mt);
+      const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+      const float alpha = exp2f(m_run - m_use);
+      float psum = 0.f;
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          float p = exp2f(s[t][r] - m_use);
+          s[t][r] = p;
+          psum += p;
+        }
+      l_part = l_part * alpha + psum;
+      m_run = m_new;
+#pragma unroll
+      for (int t = 0; t < ND; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc_o[t][r] *= alpha;
+      // O^T += V^T P^T over 4 k-steps of 16 keys
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int ih = 0; ih < 2; ++ih) {
+          bf16x8 fp;
+          {
+            union {
+              uint32_t u[4];
+              bf16x8 v;
+            } cv;
+            cv.u[0] = pack_bf2(s[t][(2 * ih) * 4 + 0], s[t][(2 * ih) * 4 + 1]);
+            cv.u[1] = pack_bf2(s[t][(2 * ih) * 4 + 2], s[t][(2 * ih) * 4 + 3]);
+            cv.u[2] = pack_bf2(s[t][(2 * ih + 1) * 4 + 0], s[t][(2 * ih + 1) * 4 + 1]);
+            cv.u[3] = pack_bf2(s[t][(2 * ih + 1) * 4 + 2], s[t][(2 * ih + 1) * 4 + 3]);
+            fp = cv.v;
+          }
+          const int key0 = t * 32 + (2 * ih) * 8 + half * 4;
+#pragma unroll
+          for (int dt = 0; dt < ND; ++dt) {
+            const bf16_t* vrow = &sV[buf][(dt * 32 + li) * LDV];
+            union {
+              u32x2 w[2];
+              bf16x8 v;
+            } cvv;
+            cvv.w[0] = *(const u32x2*)(vrow + key0);
+            cvv.w[1] = *(const u32x2*)(vrow + key0 + 8);
+            acc_o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cvv.v, fp, acc_o[dt], 0, 0, 0);
+          }
+        }
+    }
+    if (it + 1 < ntiles) lstore(buf ^ 1);
+    __syncthreads();
+  }
+
+  const float l_tot = l_part + __shfl_xor(l_part, 32, 64);
+  if (qi < L) {
+    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    bf16_t* orow = o + ((size_t)b * L + qi) * (size_t)(H * DH) + h * DH;
+#pragma unroll
+    for (int dt = 0; dt < ND; ++dt)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        int d = dt * 32 + g * 8 + half * 4;
+        u32x2 w = {pack_bf2(acc_o[dt][g * 4 + 0] * inv, acc_o[dt][g * 4 + 1] * inv),
+                   pack_bf2(acc_o[dt][g * 4 + 2] * inv, acc_o[dt][g * 4 + 3] * inv)};
+        *(u32x2*)(orow + d) = w;
+      }
+  }
+}
+
+template <int DH, bool CAUSAL>
+hipError_t launch_attn(const bf16_t* q, const bf16_t* k, const bf16_t* vt, int ldvt, bf16_t* o, int B, int H, int Hkv,
+                       int L, hipStream_t s) {
+  const int nqb = (L + BQ - 1) / BQ;
+  const float scale_log2 = 1.4426950408889634f / sqrtf((float)DH);
+  hipLaunchKernelGGL((attn_bf16_kernel<DH, CAUSAL>), dim3(nqb * H * B), dim3(256), 0, s, q, k, vt, ldvt, o, B, H, Hkv,
+                     L, scale_log2);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t attention_bf16(const bf16_t* q, const bf16_t* k, const bf16_t* vt, int ldvt, bf16_t* o, int B, int H,
+                          int Hkv, int L, int dh, bool causal, hipStream_t s) {
+  if (B <= 0 || L <= 0 || H <= 0) return hipSuccess;
+  if (Hkv <= 0 || H % Hkv != 0 || ldvt < L || ldvt % 8 != 0) return hipErrorInvalidValue;
+  if (dh == 128) return causal ? launch_attn<128, true>(q, k, vt, ldvt, o, B, H, Hkv, L, s)
+                               : launch_attn<128, false>(q, k, vt, ldvt, o, B, H, Hkv, L, s);
+  if (dh == 64) return causal ? launch_attn<64, true>(q, k, vt, ldvt, o, B, H, Hkv, L, s)
+                              : launch_attn<64, false>(q, k, vt, ldvt, o, B, H, Hkv, L, s);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace vla

@@ -1,0 +1,83 @@
+// Host-side launch wrappers of the gfx950 kernels (internal to the library).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "common.h"
+
+namespace vla {
+
+// ---------------------------------------------------------------- bf16 GEMMs
+// Every GEMM computes acc[M][N] = A[M][K] * W[N][K]^T (bf16 in, fp32
+// accumulate) and hands acc to an epilogue.  K % 64 == 0, lda/ldw % 8 == 0.
+
+// C (fp32) = acc
+hipError_t gemm_bf16_store_f32(const bf16_t* A, int lda, const bf16_t* W, int ldw, float* C, int ldc, int M,
+                               int N, int K, hipStream_t s);
+// C (bf16) = acc + bias (bias may be NULL)
+hipError_t gemm_bf16_store_bf16(const bf16_t* A, int lda, const bf16_t* W, int ldw, bf16_t* C, int ldc,
+                                const float* bias, int M, int N, int K, hipStream_t s);
+// H (fp32 residual) += acc + bias (bias may be NULL)
+hipError_t gemm_bf16_residual(const bf16_t* A, int lda, const bf16_t* W, int ldw, float* H, int ldh,
+                              const float* bias, int M, int N, int K, hipStream_t s);
+// out (bf16) [M][N/2] = silu(gate) * up, W rows interleaved in groups of 32
+// (32 gate rows, then the 32 up rows of the same features); N % 64 == 0.
+hipError_t gemm_bf16_swiglu(const bf16_t* A, int lda, const bf16_t* W, int ldw, bf16_t* out, int ldo, int M,
+                            int N, int K, hipStream_t s);
+// out (bf16) = gelu_erf(acc + bias)
+hipError_t gemm_bf16_gelu(const bf16_t* A, int lda, const bf16_t* W, int ldw, bf16_t* out, int ldo,
+                          const float* bias, int M, int N, int K, hipStream_t s);
+
+// Fused QKV projection epilogue.  Packed weight rows: [q heads | k heads |
+// v heads], each head's head_dim rows in 64-row groups that hold 32 rows of
+// the first rotary half followed by their 32 partner rows of the second half
+// (dims c*32..c*32+31 then dh/2+c*32..), so a wave owns every rotary pair.
+struct QkvArgs {
+  const float* bias;    // packed order, NULL if none
+  const float* rope_cos;  // [max_tokens][dh/2], NULL: no rotary embedding
+  const float* rope_sin;
+  bf16_t* q;   // [B][H][L][dh]
+  bf16_t* k;   // [B][Hkv][L][dh]
+  bf16_t* v;   // [B][Hkv][L][dh]
+  bf16_t* vt;  // [B][Hkv][dh][ldvt] (V transposed, for the attention's PV product)
+  int ldvt;
+  int L, H, Hkv, dh;
+};
+hipError_t gemm_bf16_qkv(const bf16_t* A, int lda, const bf16_t* W, int ldw, const QkvArgs& qa, int M, int N,
+                         int K, hipStream_t s);
+
+// ---------------------------------------------------------- bf16 attention
+// o[B][L][H*dh] = softmax(q k^T / sqrt(dh) [+ causal mask]) v per (b, head);
+// query head h reads KV head h / (H / Hkv).  q [B][H][L][dh], k [B][Hkv][L][dh],
+// vt [B][Hkv][dh][ldvt].  dh in {64, 128}.
+hipError_t attention_bf16(const bf16_t* q, const bf16_t* k, const bf16_t* vt, int ldvt, bf16_t* o, int B, int H,
+                          int Hkv, int L, int dh, bool causal, hipStream_t s);
+
+// ----------------------------------------------------- norms and elementwise
+// y[M][d] = norm(x[M][d]) (fp32 in); RMSNorm when beta == NULL and !layernorm.
+hipError_t rmsnorm_bf16(const float* x, const float* g, float eps, bf16_t* y, int M, int d, hipStream_t s);
+hipError_t layernorm_bf16(const float* x, const float* g, const float* b, float eps, bf16_t* y, int M, int d,
+                          hipStream_t s);
+hipError_t rmsnorm_f32(const float* x, const float* g, float eps, float* y, int M, int d, hipStream_t s);
+hipError_t layernorm_f32(const float* x, const float* g, const float* b, float eps, float* y, int M, int d,
+                         hipStream_t s);
+hipError_t bf16_to_f32(const bf16_t* x, float* y, size_t n, hipStream_t s);
+hipError_t f32_to_bf16(const float* x, bf16_t* y, size_t n, hipStream_t s);
+
+// ------------------------------------------------------------- fp32 debug path
+// C[M][N] (op) A[M][K] * W[N][K]^T in fp32 FMA; mode 0: C = acc + bias,
+// mode 1: C += acc + bias.
+hipError_t gemm_f32(const float* A, int lda, const float* W, int ldw, float* C, int ldc, const float* bias,
+                    int mode, int M, int N, int K, hipStream_t s);
+// qkv[M][(H+2Hkv)*dh] natural order -> q/k/v/vt (fp32) with rotary on q, k.
+hipError_t qkv_split_f32(const float* qkv, const float* rope_cos, const float* rope_sin, float* q, float* k,
+                         float* v, float* vt, int ldvt, int B, int L, int H, int Hkv, int dh, hipStream_t s);
+hipError_t attention_f32(const float* q, const float* k, const float* v, float* o, int B, int H, int Hkv, int L,
+                         int dh, bool causal, hipStream_t s);
+// gu[M][2F] (gate | up) -> a[M][F] = silu(gate) * up
+hipError_t swiglu_f32(const float* gu, float* a, int M, int F, hipStream_t s);
+// x[M][F] = gelu(x)
+hipError_t gelu_f32(float* x, size_t n, hipStream_t s);
+
+}  // namespace vla

@@ -1,0 +1,162 @@
+// Row normalisations and casts (HBM-bound): one wave per row, float4 loads,
+// the row kept in registers between the reduction and the scaled store.
+
+#include "kernels.h"
+
+namespace vla {
+namespace {
+
+template <int NCH, bool LAYERNORM, class OutT>
+__global__ __launch_bounds__(256) void norm_kernel(const float* __restrict__ x, const float* __restrict__ g,
+                                                   const float* __restrict__ bta, float eps, OutT* __restrict__ y,
+                                                   int M, int d) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= M) return;
+  const int n4 = d >> 2;
+  const f32x4* xr = (const f32x4*)(x + (size_t)row * d);
+  f32x4 v[NCH];
+  float s = 0.f;
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    int i = lane + c * 64;
+    v[c] = i < n4 ? xr[i] : f32x4{0.f, 0.f, 0.f, 0.f};
+    s += (v[c][0] + v[c][1]) + (v[c][2] + v[c][3]);
+  }
+  float mean = 0.f, rstd;
+  if (LAYERNORM) {
+    mean = warp_sum(s) / (float)d;
+    float q = 0.f;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      int i = lane + c * 64;
+      if (i < n4)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          float t = v[c][e] - mean;
+          q += t * t;
+        }
+    }
+    rstd = rsqrtf(warp_sum(q) / (float)d + eps);
+  } else {
+    float q = 0.f;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) q += v[c][e] * v[c][e];
+    rstd = rsqrtf(warp_sum(q) / (float)d + eps);
+  }
+  const f32x4* g4 = (const f32x4*)g;
+  const f32x4* b4 = (const f32x4*)bta;
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    int i = lane + c * 64;
+    if (i >= n4) continue;
+    f32x4 gg = g4[i];
+    f32x4 o;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o[e] = (v[c][e] - mean) * rstd * gg[e];
+    if (LAYERNORM) {
+      f32x4 bb = b4[i];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o[e] += bb[e];
+    }
+    if constexpr (sizeof(OutT) == 2) {
+      u32x2 w = {pack_bf2(o[0], o[1]), pack_bf2(o[2], o[3])};
+      *(u32x2*)((bf16_t*)y + (size_t)row * d + i * 4) = w;
+    } else {
+      *(f32x4*)((float*)y + (size_t)row * d + i * 4) = o;
+    }
+  }
+}
+
+template <bool LN, class OutT>
+hipError_t launch_norm(const float* x, const float* g, const float* b, float eps, OutT* y, int M, int d,
+                       hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if (d % 4 != 0) return hipErrorInvalidValue;
+  const int n4 = d / 4;
+  dim3 grid((M + 3) / 4), block(256);
+  if (n4 <= 64) hipLaunchKernelGGL((norm_kernel<1, LN, OutT>), grid, block, 0, s, x, g, b, eps, y, M, d);
+  else if (n4 <= 128) hipLaunchKernelGGL((norm_kernel<2, LN, OutT>), grid, block, 0, s, x, g, b, eps, y, M, d);
+  else if (n4 <= 256) hipLaunchKernelGGL((norm_kernel<4, LN, OutT>), grid, block, 0, s, x, g, b, eps, y, M, d);
+  else if (n4 <= 512) hipLaunchKernelGGL((norm_kernel<8, LN, OutT>), grid, block, 0, s, x, g, b, eps, y, M, d);
+  else if (n4 <= 1024) hipLaunchKernelGGL((norm_kernel<16, LN, OutT>), grid, block, 0, s, x, g, b, eps, y, M, d);
+  else if (n4 <= 2048) hipLaunchKernelGGL((norm_kernel<32, LN, OutT>), grid, block, 0, s, x, g, b, eps, y, M, d);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+__global__ void bf16_to_f32_kernel(const bf16_t* __restrict__ x, float* __restrict__ y, size_t n) {
+  size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * 8;
+  size_t stride = (size_t)gridDim.x * blockDim.x * 8;
+  for (; i < n; i += stride) {
+    if (i + 8 <= n) {
+      u32x4 w = *(const u32x4*)(x + i);
+      f32x4 a, b;
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        a[2 * e] = __uint_as_float(w[e] << 16);
+        a[2 * e + 1] = __uint_as_float(w[e] & 0xFFFF0000u);
+        b[2 * e] = __uint_as_float(w[e + 2] << 16);
+        b[2 * e + 1] = __uint_as_float(w[e + 2] & 0xFFFF0000u);
+      }
+      *(f32x4*)(y + i) = a;
+      *(f32x4*)(y + i + 4) = b;
+    } else {
+      for (size_t j = i; j < n; ++j) y[j] = bf2f(x[j]);
+    }
+  }
+}
+
+__global__ void f32_to_bf16_kernel(const float* __restrict__ x, bf16_t* __restrict__ y, size_t n) {
+  size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * 8;
+  size_t stride = (size_t)gridDim.x * blockDim.x * 8;
+  for (; i < n; i += stride) {
+    if (i + 8 <= n) {
+      f32x4 a = *(const f32x4*)(x + i), b = *(const f32x4*)(x + i + 4);
+      u32x4 w = {pack_bf2(a[0], a[1]), pack_bf2(a[2], a[3]), pack_bf2(b[0], b[1]), pack_bf2(b[2], b[3])};
+      *(u32x4*)(y + i) = w;
+    } else {
+      for (size_t j = i; j < n; ++j) y[j] = f2bf(x[j]);
+    }
+  }
+}
+
+inline unsigned ew_grid(size_t n) {
+  size_t blocks = (n / 8 + 255) / 256;
+  if (blocks < 1) blocks = 1;
+  if (blocks > 4096) blocks = 4096;
+  return (unsigned)blocks;
+}
+
+}  // namespace
+
+hipError_t rmsnorm_bf16(const float* x, const float* g, float eps, bf16_t* y, int M, int d, hipStream_t s) {
+  return launch_norm<false>(x, g, (const float*)nullptr, eps, y, M, d, s);
+}
+hipError_t layernorm_bf16(const float* x, const float* g, const float* b, float eps, bf16_t* y, int M, int d,
+                          hipStream_t s) {
+  return launch_norm<true>(x, g, b, eps, y, M, d, s);
+}
+hipError_t rmsnorm_f32(const float* x, const float* g, float eps, float* y, int M, int d, hipStream_t s) {
+  return launch_norm<false>(x, g, (const float*)nullptr, eps, y, M, d, s);
+}
+hipError_t layernorm_f32(const float* x, const float* g, const float* b, float eps, float* y, int M, int d,
+                         hipStream_t s) {
+  return launch_norm<true>(x, g, b, eps, y, M, d, s);
+}
+
+hipError_t bf16_to_f32(const bf16_t* x, float* y, size_t n, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(bf16_to_f32_kernel, dim3(ew_grid(n)), dim3(256), 0, s, x, y, n);
+  return hipGetLastError();
+}
+
+hipError_t f32_to_bf16(const float* x, bf16_t* y, size_t n, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(f32_to_bf16_kernel, dim3(ew_grid(n)), dim3(256), 0, s, x, y, n);
+  return hipGetLastError();
+}
+
+}  // namespace vla

@@ -1,0 +1,40 @@
+// Operator-level entry points (include/vla_ops.h).
+#include <hip/hip_runtime.h>
+
+#include "../../include/vla_ops.h"
+#include "kernels.h"
+
+namespace {
+vla_status status_of(hipError_t e) {
+  if (e == hipSuccess) return VLA_OK;
+  return e == hipErrorInvalidValue ? VLA_ERR_UNSUPPORTED : VLA_ERR_HIP;
+}
+}  // namespace
+
+extern "C" {
+
+vla_status vla_op_gemm_bf16(const void* A, const void* W, float* C, int M, int N, int K, void* stream) {
+  if (!A || !W || !C || M < 0 || N < 0 || K <= 0) return VLA_ERR_INVALID_ARG;
+  if (K % 64) return VLA_ERR_UNSUPPORTED;
+  return status_of(vla::gemm_bf16_store_f32((const bf16_t*)A, K, (const bf16_t*)W, K, C, N, M, N, K,
+                                            (hipStream_t)stream));
+}
+
+vla_status vla_op_attention_bf16(const void* q, const void* k, const void* vt, int ldvt, void* o, int B, int H,
+                                 int Hkv, int L, int dh, int causal, void* stream) {
+  if (!q || !k || !vt || !o || B < 0 || H <= 0 || Hkv <= 0 || L < 0) return VLA_ERR_INVALID_ARG;
+  if (H % Hkv || (dh != 64 && dh != 128) || ldvt < L || ldvt % 8) return VLA_ERR_UNSUPPORTED;
+  return status_of(vla::attention_bf16((const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)vt, ldvt, (bf16_t*)o, B, H,
+                                       Hkv, L, dh, causal != 0, (hipStream_t)stream));
+}
+
+vla_status vla_op_norm_bf16(const float* x, const float* g, const float* b, float eps, void* y, int M, int d,
+                            void* stream) {
+  if (!x || !g || !y || M < 0 || d <= 0) return VLA_ERR_INVALID_ARG;
+  if (d % 4 || d > 8192) return VLA_ERR_UNSUPPORTED;
+  hipError_t e = b ? vla::layernorm_bf16(x, g, b, eps, (bf16_t*)y, M, d, (hipStream_t)stream)
+                   : vla::rmsnorm_bf16(x, g, eps, (bf16_t*)y, M, d, (hipStream_t)stream);
+  return status_of(e);
+}
+
+}  // extern "C"

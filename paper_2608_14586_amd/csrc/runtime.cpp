@@ -1,0 +1,870 @@
+// Runtime of the VLA prefix library: context, arena sub-allocation, weight
+// packing, block sequencing on the compute stream and the frame handoff on the
+// copy stream.  Implements include/vla_prefix.h.
+
+#include <hip/hip_runtime.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <chrono>
+#include <cmath>
+#include <memory>
+#include <map>
+#include <string>
+#include <thread>
+#include <vector>
+
+#include "../../include/vla_prefix.h"
+#include "kernels.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+constexpr int NSLOT = 3;          // frames that may be in flight at once
+constexpr size_t ALIGN = 256;     // arena sub-allocation alignment
+constexpr size_t HISTORY = 256;   // finished frames whose times are kept
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+inline int round_up(int x, int a) { return (x + a - 1) / a * a; }
+
+struct Status {
+  vla_status code;
+  std::string msg;
+};
+
+[[gnu::format(printf, 2, 3)]] Status fail(vla_status c, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  return Status{c, buf};
+}
+const Status OK{VLA_OK, ""};
+
+#define HIPTRY(expr)                                                                         \
+  do {                                                                                       \
+    hipError_t e_ = (expr);                                                                  \
+    if (e_ != hipSuccess) return fail(VLA_ERR_HIP, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+size_t dtype_size(vla_dtype t) { return t == VLA_BF16 ? 2 : 4; }
+
+// Derived, validated view of one stack.
+struct Stack {
+  bool present = false;
+  vla_stack_cfg c{};
+  size_t esz = 0;
+  int hd = 0, kvd = 0, qkv_n = 0, f_pad = 0, ldvt = 0;
+  size_t m_max = 0;  // max_batch * max_tokens
+
+  struct Block {
+    void *w_qkv = nullptr, *w_o = nullptr, *w_up = nullptr, *w_down = nullptr;  // w_up: gate/up or fc1
+    float *b_qkv = nullptr, *b_o = nullptr, *b_up = nullptr, *b_down = nullptr;
+    float *n1g = nullptr, *n1b = nullptr, *n2g = nullptr, *n2b = nullptr;
+    bool loaded = false;
+  };
+  std::vector<Block> blocks;
+
+  bool bf16() const { return c.dtype == VLA_BF16; }
+  bool llm() const { return !c.norm_is_layernorm; }
+  // rows of the up projection: interleaved gate/up (LLM) or fc1 (encoder)
+  int up_rows() const { return llm() ? 2 * f_pad : f_pad; }
+};
+
+Status validate_stack(const vla_stack_cfg* c, bool is_llm, Stack* s) {
+  s->present = false;
+  if (!c) return OK;
+  const char* w = is_llm ? "llm" : "enc";
+  if (c->dtype != VLA_BF16 && c->dtype != VLA_F32) return fail(VLA_ERR_INVALID_ARG, "%s: bad dtype", w);
+  if (c->n_blocks < 0 || c->d_model <= 0 || c->n_heads <= 0 || c->n_kv_heads <= 0 || c->head_dim <= 0 ||
+      c->d_ff <= 0 || c->max_tokens <= 0 || c->max_batch <= 0)
+    return fail(VLA_ERR_INVALID_ARG, "%s: non-positive dimension", w);
+  if (c->n_heads % c->n_kv_heads) return fail(VLA_ERR_INVALID_ARG, "%s: n_heads %% n_kv_heads != 0", w);
+  if (is_llm) {
+    if (c->norm_is_layernorm || c->mlp_is_gelu || c->has_bias)
+      return fail(VLA_ERR_UNSUPPORTED, "llm stack must be RMSNorm / SwiGLU / no bias");
+  } else {
+    if (!c->norm_is_layernorm || !c->mlp_is_gelu || !c->has_bias || c->use_rope || c->causal)
+      return fail(VLA_ERR_UNSUPPORTED, "encoder stack must be LayerNorm / GELU / biases / no rope / bidirectional");
+    if (c->n_kv_heads != c->n_heads) return fail(VLA_ERR_UNSUPPORTED, "encoder stack needs n_kv_heads == n_heads");
+  }
+  if (c->d_model % 4) return fail(VLA_ERR_UNSUPPORTED, "%s: d_model must be a multiple of 4", w);
+  if (c->d_model > 8192) return fail(VLA_ERR_UNSUPPORTED, "%s: d_model > 8192", w);
+  if (c->head_dim % 2 || c->head_dim > 128) return fail(VLA_ERR_UNSUPPORTED, "%s: head_dim must be even, <= 128", w);
+  if (c->dtype == VLA_BF16) {
+    if (c->head_dim != 64 && c->head_dim != 128)
+      return fail(VLA_ERR_UNSUPPORTED, "%s: bf16 path needs head_dim 64 or 128", w);
+    if (c->d_model % 64 || (c->n_heads * c->head_dim) % 64)
+      return fail(VLA_ERR_UNSUPPORTED, "%s: bf16 path needs d_model and n_heads*head_dim multiples of 64", w);
+  }
+  if (!(c->norm_eps >= 0.f)) return fail(VLA_ERR_INVALID_ARG, "%s: norm_eps < 0", w);
+  if (c->use_rope && !(c->rope_base > 0.f)) return fail(VLA_ERR_INVALID_ARG, "%s: rope_base <= 0", w);
+  s->present = true;
+  s->c = *c;
+  s->esz = dtype_size(c->dtype);
+  s->hd = c->n_heads * c->head_dim;
+  s->kvd = c->n_kv_heads * c->head_dim;
+  s->qkv_n = s->hd + 2 * s->kvd;
+  s->f_pad = c->dtype == VLA_BF16 ? round_up(c->d_ff, 64) : c->d_ff;
+  s->ldvt = round_up(c->max_tokens, 64);
+  s->m_max = (size_t)c->max_batch * c->max_tokens;
+  s->blocks.assign(c->n_blocks, Stack::Block{});
+  return OK;
+}
+
+struct Slot {
+  uint64_t frame_id = 0;
+  bool used = false;
+  bool has_kv = false;
+  void* kv = nullptr;   // device [n_blocks][2][B][Hkv][L][dh]
+  void* hid = nullptr;  // device staging of the boundary
+  hipEvent_t ev_start = nullptr, ev_done = nullptr, ev_hid = nullptr, ev_copied = nullptr;
+  std::vector<hipEvent_t> ev_kv;
+};
+
+struct FrameTimes {
+  float gpu, xfer, total;
+};
+
+}  // namespace
+
+struct vla_ctx {
+  int device = 0;
+  Stack llm, enc;
+  char* arena = nullptr;
+  size_t arena_bytes = 0, used = 0;
+  hipStream_t compute = nullptr, copy = nullptr;
+  bool own_compute = false, own_copy = false;
+  std::string last_error;
+
+  // workspace (sized for the larger stack)
+  float* h = nullptr;      // fp32 residual
+  void* x = nullptr;       // normalised activations
+  void* q = nullptr;       // [B][H][L][dh]
+  void* ek = nullptr;      // encoder K / V (LLM writes into the slot cache)
+  void* ev = nullptr;
+  void* vt = nullptr;      // V^T
+  void* o = nullptr;       // attention output [M][H*dh]
+  void* act = nullptr;     // MLP activation
+  float* qkv_raw = nullptr;  // fp32 path only
+  void* tok = nullptr;     // staging of host-resident inputs
+  float *rope_cos = nullptr, *rope_sin = nullptr;
+  Slot slots[NSLOT];
+  int next_slot = 0;
+  std::map<uint64_t, FrameTimes> history;
+};
+
+namespace {
+
+// Arena layout, shared by vla_query_sizes and vla_create: a bump allocator
+// that only counts when base == nullptr.
+struct Bump {
+  char* base;
+  size_t off = 0;
+  void* take(size_t bytes) {
+    off = align_up(off, ALIGN);
+    void* p = base ? base + off : nullptr;
+    off += bytes;
+    return p;
+  }
+};
+
+void layout(vla_ctx* c, Bump& a) {
+  Stack* stacks[2] = {&c->llm, &c->enc};
+  for (Stack* s : stacks) {
+    if (!s->present) continue;
+    const size_t d = s->c.d_model, e = s->esz;
+    for (auto& b : s->blocks) {
+      b.w_qkv = a.take((size_t)s->qkv_n * d * e);
+      b.w_o = a.take(d * s->hd * e);
+      b.w_up = a.take((size_t)s->up_rows() * d * e);
+      b.w_down = a.take(d * s->f_pad * e);
+      b.n1g = (float*)a.take(d * 4);
+      b.n2g = (float*)a.take(d * 4);
+      if (s->c.has_bias) {
+        b.b_qkv = (float*)a.take((size_t)s->qkv_n * 4);
+        b.b_o = (float*)a.take(d * 4);
+        b.b_up = (float*)a.take((size_t)s->f_pad * 4);
+        b.b_down = (float*)a.take(d * 4);
+      }
+      if (s->c.norm_is_layernorm) {
+        b.n1b = (float*)a.take(d * 4);
+        b.n2b = (float*)a.take(d * 4);
+      }
+    }
+  }
+  size_t h = 0, x = 0, q = 0, ekv = 0, vt = 0, o = 0, act = 0, raw = 0, tok = 0;
+  for (Stack* s : stacks) {
+    if (!s->present) continue;
+    const size_t M = s->m_max, d = s->c.d_model, e = s->esz;
+    h = std::max(h, M * d * 4);
+    x = std::max(x, M * d * e);
+    q = std::max(q, M * s->hd * e);
+    o = std::max(o, M * s->hd * e);
+    vt = std::max(vt, (size_t)s->c.max_batch * s->kvd * s->ldvt * e);
+    tok = std::max(tok, M * d * e);
+    if (s->bf16())
+      act = std::max(act, M * s->f_pad * e);
+    else
+      act = std::max(act, M * (size_t)s->c.d_ff * (s->llm() ? 3 : 1) * 4), raw = std::max(raw, M * s->qkv_n * 4);
+    if (s == &c->enc) ekv = std::max(ekv, M * s->kvd * e);
+  }
+  c->h = (float*)a.take(h);
+  c->x = a.take(x);
+  c->q = a.take(q);
+  c->ek = a.take(ekv);
+  c->ev = a.take(ekv);
+  c->vt = a.take(vt);
+  c->o = a.take(o);
+  c->act = a.take(act);
+  c->qkv_raw = (float*)a.take(raw);
+  c->tok = a.take(tok);
+  int rope_len = 0, rope_half = 0;
+  if (c->llm.present && c->llm.c.use_rope) rope_len = c->llm.c.max_tokens, rope_half = c->llm.c.head_dim / 2;
+  c->rope_cos = (float*)a.take((size_t)rope_len * rope_half * 4);
+  c->rope_sin = (float*)a.take((size_t)rope_len * rope_half * 4);
+  if (c->llm.present) {
+    const Stack& s = c->llm;
+    for (auto& sl : c->slots) {
+      sl.kv = a.take((size_t)s.c.n_blocks * 2 * s.m_max * s.kvd * s.esz);
+      sl.hid = a.take(s.m_max * s.c.d_model * 4);
+    }
+  }
+  a.off = align_up(a.off, ALIGN);
+}
+
+// ------------------------------------------------------------ weight packing
+
+// bf16 QKV rows: per head, 64-row groups [32 first-half dims | their 32
+// second-half partners].  fp32: natural order.
+int qkv_packed_to_true_dim(int r, int dh) {
+  int c = r / 64, w = r % 64;
+  return w < 32 ? c * 32 + w : dh / 2 + c * 32 + (w - 32);
+}
+
+float to_f32(const void* p, size_t i, vla_dtype t) {
+  if (t == VLA_F32) return ((const float*)p)[i];
+  uint32_t u = (uint32_t)((const uint16_t*)p)[i] << 16;
+  float f;
+  memcpy(&f, &u, 4);
+  return f;
+}
+
+std::vector<float> vec_f32(const void* p, size_t n, vla_dtype t) {
+  std::vector<float> v(n);
+  for (size_t i = 0; i < n; ++i) v[i] = to_f32(p, i, t);
+  return v;
+}
+
+Status copy_h2d(void* dst, const void* src, size_t bytes) {
+  HIPTRY(hipMemcpy(dst, src, bytes, hipMemcpyHostToDevice));
+  return OK;
+}
+
+Status load_block(vla_ctx* c, Stack& s, int bi, const vla_block_weights* w) {
+  const vla_stack_cfg& k = s.c;
+  const bool llm = s.llm();
+  const size_t d = k.d_model, e = s.esz, dh = k.head_dim;
+  // required / forbidden pointers
+  if (!w->w_q || !w->w_k || !w->w_v || !w->w_o || !w->norm1_g || !w->norm2_g)
+    return fail(VLA_ERR_INVALID_ARG, "block %d: missing attention weights or norm gains", bi);
+  if (llm) {
+    if (!w->w_gate || !w->w_up || !w->w_down) return fail(VLA_ERR_INVALID_ARG, "block %d: missing SwiGLU weights", bi);
+    if (w->w_fc1 || w->w_fc2 || w->b_fc1 || w->b_fc2 || w->b_qkv || w->b_o || w->norm1_b || w->norm2_b)
+      return fail(VLA_ERR_INVALID_ARG, "block %d: decoder blocks take no biases / fc weights / norm shifts", bi);
+  } else {
+    if (!w->w_fc1 || !w->w_fc2 || !w->b_fc1 || !w->b_fc2 || !w->b_qkv || !w->b_o || !w->norm1_b || !w->norm2_b)
+      return fail(VLA_ERR_INVALID_ARG, "block %d: missing encoder weights, biases or norm shifts", bi);
+    if (w->w_gate || w->w_up || w->w_down)
+      return fail(VLA_ERR_INVALID_ARG, "block %d: encoder blocks take no SwiGLU weights", bi);
+  }
+  Stack::Block& b = s.blocks[bi];
+  b.loaded = false;
+  // QKV
+  {
+    std::vector<char> buf((size_t)s.qkv_n * d * e);
+    const void* src[3] = {w->w_q, w->w_k, w->w_v};
+    const int heads[3] = {k.n_heads, k.n_kv_heads, k.n_kv_heads};
+    size_t prow = 0;
+    for (int part = 0; part < 3; ++part)
+      for (int hh = 0; hh < heads[part]; ++hh)
+        for (size_t r = 0; r < dh; ++r, ++prow) {
+          size_t tr = hh * dh + (s.bf16() ? qkv_packed_to_true_dim((int)r, (int)dh) : r);
+          memcpy(&buf[prow * d * e], (const char*)src[part] + tr * d * e, d * e);
+        }
+    Status st = copy_h2d(b.w_qkv, buf.data(), buf.size());
+    if (st.code) return st;
+    if (k.has_bias) {
+      std::vector<float> bias(s.qkv_n);
+      const size_t offs[3] = {0, (size_t)s.hd, (size_t)(s.hd + s.kvd)};
+      prow = 0;
+      for (int part = 0; part < 3; ++part)
+        for (int hh = 0; hh < heads[part]; ++hh)
+          for (size_t r = 0; r < dh; ++r, ++prow) {
+            size_t tr = hh * dh + (s.bf16() ? qkv_packed_to_true_dim((int)r, (int)dh) : r);
+            bias[prow] = to_f32(w->b_qkv, offs[part] + tr, k.dtype);
+          }
+      if ((st = copy_h2d(b.b_qkv, bias.data(), bias.size() * 4)).code) return st;
+    }
+  }
+  Status st = copy_h2d(b.w_o, w->w_o, d * s.hd * e);
+  if (st.code) return st;
+  // up projection: interleaved gate/up (bf16), [gate; up] (fp32), or fc1
+  {
+    const size_t F = k.d_ff;
+    std::vector<char> buf((size_t)s.up_rows() * d * e, 0);
+    if (llm) {
+      for (int p = 0; p < s.up_rows(); ++p) {
+        size_t f;
+        const void* src;
+        if (s.bf16()) {
+          int g = p / 64, wi = p % 64;
+          f = g * 32 + (wi % 32);
+          src = wi < 32 ? w->w_gate : w->w_up;
+        } else {
+          f = p < (int)F ? p : p - F;
+          src = p < (int)F ? w->w_gate : w->w_up;
+        }
+        if (f < F) memcpy(&buf[(size_t)p * d * e], (const char*)src + f * d * e, d * e);
+      }
+    } else {
+      memcpy(buf.data(), w->w_fc1, F * d * e);
+    }
+    if ((st = copy_h2d(b.w_up, buf.data(), buf.size())).code) return st;
+  }
+  // down projection [d][f_pad] with zero pad columns
+  {
+    const size_t F = k.d_ff, FP = s.f_pad;
+    const void* src = llm ? w->w_down : w->w_fc2;
+    std::vector<char> buf(d * FP * e, 0);
+    for (size_t r = 0; r < d; ++r) memcpy(&buf[r * FP * e], (const char*)src + r * F * e, F * e);
+    if ((st = copy_h2d(b.w_down, buf.data(), buf.size())).code) return st;
+  }
+  auto put = [&](float* dst, const void* src, size_t n, size_t npad) -> Status {
+    std::vector<float> v = vec_f32(src, n, k.dtype);
+    v.resize(npad, 0.f);
+    return copy_h2d(dst, v.data(), npad * 4);
+  };
+  if ((st = put(b.n1g, w->norm1_g, d, d)).code) return st;
+  if ((st = put(b.n2g, w->norm2_g, d, d)).code) return st;
+  if (k.norm_is_layernorm) {
+    if ((st = put(b.n1b, w->norm1_b, d, d)).code) return st;
+    if ((st = put(b.n2b, w->norm2_b, d, d)).code) return st;
+  }
+  if (k.has_bias) {
+    if ((st = put(b.b_o, w->b_o, d, d)).code) return st;
+    if ((st = put(b.b_up, w->b_fc1, k.d_ff, s.f_pad)).code) return st;
+    if ((st = put(b.b_down, w->b_fc2, d, d)).code) return st;
+  }
+  b.loaded = true;
+  return OK;
+}
+
+// ------------------------------------------------------------- execution
+
+bool is_pinned_host(const void* p) {
+  hipPointerAttribute_t a;
+  if (hipPointerGetAttributes(&a, p) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  return a.type == hipMemoryTypeHost;
+}
+
+bool is_device(const void* p) {
+  hipPointerAttribute_t a;
+  if (hipPointerGetAttributes(&a, p) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  return a.type == hipMemoryTypeDevice || a.type == hipMemoryTypeManaged;
+}
+
+#define KTRY(expr)                                                                                   \
+  do {                                                                                               \
+    hipError_t e_ = (expr);                                                                          \
+    if (e_ != hipSuccess) return fail(VLA_ERR_HIP, "launch %s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+// input[B*L][d] (host or device, stack dtype) -> fp32 residual c->h
+Status intake(vla_ctx* c, const Stack& s, const void* in, size_t n) {
+  const void* src = in;
+  if (!is_device(in)) {
+    HIPTRY(hipMemcpyAsync(c->tok, in, n * s.esz, hipMemcpyHostToDevice, c->compute));
+    src = c->tok;
+  }
+  if (s.bf16())
+    KTRY(vla::bf16_to_f32((const bf16_t*)src, c->h, n, c->compute));
+  else
+    HIPTRY(hipMemcpyAsync(c->h, src, n * 4, hipMemcpyDeviceToDevice, c->compute));
+  return OK;
+}
+
+Status llm_block_bf16(vla_ctx* c, const Stack::Block& w, int B, int L, bf16_t* kdst, bf16_t* vdst) {
+  const Stack& s = c->llm;
+  const vla_stack_cfg& k = s.c;
+  const int M = B * L, d = k.d_model;
+  hipStream_t st = c->compute;
+  KTRY(vla::rmsnorm_bf16(c->h, w.n1g, k.norm_eps, (bf16_t*)c->x, M, d, st));
+  vla::QkvArgs qa{nullptr, k.use_rope ? c->rope_cos : nullptr, k.use_rope ? c->rope_sin : nullptr,
+                  (bf16_t*)c->q, kdst, vdst, (bf16_t*)c->vt, round_up(L, 64), L, k.n_heads, k.n_kv_heads,
+                  k.head_dim};
+  KTRY(vla::gemm_bf16_qkv((const bf16_t*)c->x, d, (const bf16_t*)w.w_qkv, d, qa, M, s.qkv_n, d, st));
+  return OK;
+}
+
+Status llm_block_bf16_rest(vla_ctx* c, const Stack::Block& w, int B, int L, const bf16_t* kdst) {
+  const Stack& s = c->llm;
+  const vla_stack_cfg& k = s.c;
+  const int M = B * L, d = k.d_model;
+  hipStream_t st = c->compute;
+  KTRY(vla::attention_bf16((const bf16_t*)c->q, kdst, (const bf16_t*)c->vt, round_up(L, 64), (bf16_t*)c->o, B,
+                           k.n_heads, k.n_kv_heads, L, k.head_dim, k.causal != 0, st));
+  KTRY(vla::gemm_bf16_residual((const bf16_t*)c->o, s.hd, (const bf16_t*)w.w_o, s.hd, c->h, d, nullptr, M, d, s.hd,
+                               st));
+  KTRY(vla::rmsnorm_bf16(c->h, w.n2g, k.norm_eps, (bf16_t*)c->x, M, d, st));
+  KTRY(vla::gemm_bf16_swiglu((const bf16_t*)c->x, d, (const bf16_t*)w.w_up, d, (bf16_t*)c->act, s.f_pad, M,
+                             2 * s.f_pad, d, st));
+  KTRY(vla::gemm_bf16_residual((const bf16_t*)c->act, s.f_pad, (const bf16_t*)w.w_down, s.f_pad, c->h, d, nullptr, M,
+                               d, s.f_pad, st));
+  return OK;
+}
+
+Status llm_block_f32(vla_ctx* c, const Stack::Block& w, int B, int L, float* kdst, float* vdst) {
+  const Stack& s = c->llm;
+  const vla_stack_cfg& k = s.c;
+  const int M = B * L, d = k.d_model;
+  hipStream_t st = c->compute;
+  float* x = (float*)c->x;
+  KTRY(vla::rmsnorm_f32(c->h, w.n1g, k.norm_eps, x, M, d, st));
+  KTRY(vla::gemm_f32(x, d, (const float*)w.w_qkv, d, c->qkv_raw, s.qkv_n, nullptr, 0, M, s.qkv_n, d, st));
+  KTRY(vla::qkv_split_f32(c->qkv_raw, k.use_rope ? c->rope_cos : nullptr, k.use_rope ? c->rope_sin : nullptr,
+                          (float*)c->q, kdst, vdst, nullptr, 0, B, L, k.n_heads, k.n_kv_heads, k.head_dim, st));
+  return OK;
+}
+
+Status llm_block_f32_rest(vla_ctx* c, const Stack::Block& w, int B, int L, const float* kdst, const float* vdst) {
+  const Stack& s = c->llm;
+  const vla_stack_cfg& k = s.c;
+  const int M = B * L, d = k.d_model, F = k.d_ff;
+  hipStream_t st = c->compute;
+  float* x = (float*)c->x;
+  float* gu = (float*)c->act;
+  float* a = gu + (size_t)M * 2 * F;
+  KTRY(vla::attention_f32((const float*)c->q, kdst, vdst, (float*)c->o, B, k.n_heads, k.n_kv_heads, L, k.head_dim,
+                          k.causal != 0, st));
+  KTRY(vla::gemm_f32((const float*)c->o, s.hd, (const float*)w.w_o, s.hd, c->h, d, nullptr, 1, M, d, s.hd, st));
+  KTRY(vla::rmsnorm_f32(c->h, w.n2g, k.norm_eps, x, M, d, st));
+  KTRY(vla::gemm_f32(x, d, (const float*)w.w_up, d, gu, 2 * F, nullptr, 0, M, 2 * F, d, st));
+  KTRY(vla::swiglu_f32(gu, a, M, F, st));
+  KTRY(vla::gemm_f32(a, F, (const float*)w.w_down, F, c->h, d, nullptr, 1, M, d, F, st));
+  return OK;
+}
+
+Status enc_block(vla_ctx* c, const Stack::Block& w, int n_img, int L) {
+  const Stack& s = c->enc;
+  const vla_stack_cfg& k = s.c;
+  const int M = n_img * L, d = k.d_model;
+  hipStream_t st = c->compute;
+  if (s.bf16()) {
+    bf16_t* x = (bf16_t*)c->x;
+    KTRY(vla::layernorm_bf16(c->h, w.n1g, w.n1b, k.norm_eps, x, M, d, st));
+    vla::QkvArgs qa{w.b_qkv, nullptr, nullptr, (bf16_t*)c->q, (bf16_t*)c->ek, (bf16_t*)c->ev, (bf16_t*)c->vt,
+                    round_up(L, 64), L, k.n_heads, k.n_kv_heads, k.head_dim};
+    KTRY(vla::gemm_bf16_qkv(x, d, (const bf16_t*)w.w_qkv, d, qa, M, s.qkv_n, d, st));
+    KTRY(vla::attention_bf16((const bf16_t*)c->q, (const bf16_t*)c->ek, (const bf16_t*)c->vt, round_up(L, 64),
+                             (bf16_t*)c->o, n_img, k.n_heads, k.n_kv_heads, L, k.head_dim, false, st));
+    KTRY(vla::gemm_bf16_residual((const bf16_t*)c->o, s.hd, (const bf16_t*)w.w_o, s.hd, c->h, d, w.b_o, M, d, s.hd,
+                                 st));
+    KTRY(vla::layernorm_bf16(c->h, w.n2g, w.n2b, k.norm_eps, x, M, d, st));
+    KTRY(vla::gemm_bf16_gelu(x, d, (const bf16_t*)w.w_up, d, (bf16_t*)c->act, s.f_pad, w.b_up, M, s.f_pad, d, st));
+    KTRY(vla::gemm_bf16_residual((const bf16_t*)c->act, s.f_pad, (const bf16_t*)w.w_down, s.f_pad, c->h, d, w.b_down,
+                                 M, d, s.f_pad, st));
+  } else {
+    float* x = (float*)c->x;
+    const int F = k.d_ff;
+    KTRY(vla::layernorm_f32(c->h, w.n1g, w.n1b, k.norm_eps, x, M, d, st));
+    KTRY(vla::gemm_f32(x, d, (const float*)w.w_qkv, d, c->qkv_raw, s.qkv_n, w.b_qkv, 0, M, s.qkv_n, d, st));
+    KTRY(vla::qkv_split_f32(c->qkv_raw, nullptr, nullptr, (float*)c->q, (float*)c->ek, (float*)c->ev, nullptr, 0,
+                            n_img, L, k.n_heads, k.n_kv_heads, k.head_dim, st));
+    KTRY(vla::attention_f32((const float*)c->q, (const float*)c->ek, (const float*)c->ev, (float*)c->o, n_img,
+                            k.n_heads, k.n_kv_heads, L, k.head_dim, false, st));
+    KTRY(vla::gemm_f32((const float*)c->o, s.hd, (const float*)w.w_o, s.hd, c->h, d, w.b_o, 1, M, d, s.hd, st));
+    KTRY(vla::layernorm_f32(c->h, w.n2g, w.n2b, k.norm_eps, x, M, d, st));
+    float* a = (float*)c->act;
+    KTRY(vla::gemm_f32(x, d, (const float*)w.w_up, d, a, F, w.b_up, 0, M, F, d, st));
+    KTRY(vla::gelu_f32(a, (size_t)M * F, st));
+    KTRY(vla::gemm_f32(a, F, (const float*)w.w_down, F, c->h, d, w.b_down, 1, M, d, F, st));
+  }
+  return OK;
+}
+
+Status retire_slot(vla_ctx* c, Slot& sl) {
+  if (!sl.used) return OK;
+  HIPTRY(hipEventSynchronize(sl.ev_copied));
+  FrameTimes t{};
+  HIPTRY(hipEventElapsedTime(&t.gpu, sl.ev_start, sl.ev_done));
+  HIPTRY(hipEventElapsedTime(&t.xfer, sl.ev_hid, sl.ev_copied));
+  HIPTRY(hipEventElapsedTime(&t.total, sl.ev_start, sl.ev_copied));
+  c->history[sl.frame_id] = t;
+  while (c->history.size() > HISTORY) c->history.erase(c->history.begin());
+  sl.used = false;
+  return OK;
+}
+
+Status run_blocks(vla_ctx* c, uint64_t frame_id, const void* tokens, int B, int L, int k0, int k1,
+                  vla_boundary* out) {
+  if (!c->llm.present) return fail(VLA_ERR_INVALID_ARG, "context has no decoder stack");
+  const Stack& s = c->llm;
+  if (!tokens || !out || !out->hidden) return fail(VLA_ERR_INVALID_ARG, "NULL tokens / boundary / hidden buffer");
+  if (out->out_dtype != VLA_BF16 && out->out_dtype != VLA_F32) return fail(VLA_ERR_INVALID_ARG, "bad out_dtype");
+  if (k0 < 0 || k1 < k0) return fail(VLA_ERR_INVALID_ARG, "need 0 <= k_begin <= k_end (got %d, %d)", k0, k1);
+  if (k1 > s.c.n_blocks) return fail(VLA_ERR_SHAPE, "k_end %d > resident blocks %d", k1, s.c.n_blocks);
+  if (B <= 0 || L <= 0) return fail(VLA_ERR_SHAPE, "B and L must be positive");
+  if (B > s.c.max_batch || L > s.c.max_tokens)
+    return fail(VLA_ERR_SHAPE, "B=%d L=%d exceed max_batch=%d max_tokens=%d", B, L, s.c.max_batch, s.c.max_tokens);
+  for (int l = k0; l < k1; ++l)
+    if (!s.blocks[l].loaded) return fail(VLA_ERR_NOT_LOADED, "decoder block %d has no weights", l);
+  const size_t n = (size_t)B * L * s.c.d_model;
+  const size_t hid_bytes = n * dtype_size(out->out_dtype);
+  const size_t layer_elems = (size_t)2 * B * s.kvd * L;
+  const size_t kv_bytes = (size_t)(k1 - k0) * layer_elems * s.esz;
+  if (out->hidden_bytes < hid_bytes)
+    return fail(VLA_ERR_SHAPE, "hidden buffer %zu bytes < %zu", out->hidden_bytes, hid_bytes);
+  const bool want_kv = out->kv != nullptr && kv_bytes > 0;
+  if (out->kv && out->kv_bytes < kv_bytes) return fail(VLA_ERR_SHAPE, "kv buffer %zu bytes < %zu", out->kv_bytes, kv_bytes);
+  if (!is_pinned_host(out->hidden)) return fail(VLA_ERR_NOT_PINNED, "hidden buffer is not pinned host memory");
+  if (out->kv && !is_pinned_host(out->kv)) return fail(VLA_ERR_NOT_PINNED, "kv buffer is not pinned host memory");
+  for (auto& sl : c->slots)
+    if (sl.used && sl.frame_id == frame_id) return fail(VLA_ERR_INVALID_ARG, "frame %llu is already in flight",
+                                                        (unsigned long long)frame_id);
+
+  Slot& sl = c->slots[c->next_slot];
+  c->next_slot = (c->next_slot + 1) % NSLOT;
+  Status st = retire_slot(c, sl);
+  if (st.code) return st;
+  c->history.erase(frame_id);
+  sl.frame_id = frame_id;
+  sl.used = true;
+  out->frame_id = frame_id;
+
+  HIPTRY(hipEventRecord(sl.ev_start, c->compute));
+  if ((st = intake(c, s, tokens, n)).code) return st;
+  for (int l = k0; l < k1; ++l) {
+    const Stack::Block& w = s.blocks[l];
+    char* kvl = (char*)sl.kv + (size_t)(l - k0) * layer_elems * s.esz;
+    void* kd = kvl;
+    void* vd = kvl + layer_elems / 2 * s.esz;
+    if (s.bf16())
+      st = llm_block_bf16(c, w, B, L, (bf16_t*)kd, (bf16_t*)vd);
+    else
+      st = llm_block_f32(c, w, B, L, (float*)kd, (float*)vd);
+    if (st.code) return st;
+    if (want_kv) {
+      HIPTRY(hipEventRecord(sl.ev_kv[l - k0], c->compute));
+      HIPTRY(hipStreamWaitEvent(c->copy, sl.ev_kv[l - k0], 0));
+      HIPTRY(hipMemcpyAsync((char*)out->kv + (size_t)(l - k0) * layer_elems * s.esz, kvl, layer_elems * s.esz,
+                            hipMemcpyDeviceToHost, c->copy));
+    }
+    if (s.bf16())
+      st = llm_block_bf16_rest(c, w, B, L, (const bf16_t*)kd);
+    else
+      st = llm_block_f32_rest(c, w, B, L, (const float*)kd, (const float*)vd);
+    if (st.code) return st;
+  }
+  if (out->out_dtype == VLA_BF16)
+    KTRY(vla::f32_to_bf16(c->h, (bf16_t*)sl.hid, n, c->compute));
+  else
+    HIPTRY(hipMemcpyAsync(sl.hid, c->h, n * 4, hipMemcpyDeviceToDevice, c->compute));
+  HIPTRY(hipEventRecord(sl.ev_done, c->compute));
+  HIPTRY(hipStreamWaitEvent(c->copy, sl.ev_done, 0));
+  HIPTRY(hipEventRecord(sl.ev_hid, c->copy));
+  HIPTRY(hipMemcpyAsync(out->hidden, sl.hid, hid_bytes, hipMemcpyDeviceToHost, c->copy));
+  HIPTRY(hipEventRecord(sl.ev_copied, c->copy));
+  // the next frame may not overwrite this slot's KV before the copies finished:
+  // retire_slot() synchronises on ev_copied before a slot is reused.
+  return OK;
+}
+
+Status run_encoder(vla_ctx* c, const void* patches, int n_img, int L, void* out_dev) {
+  if (!c->enc.present) return fail(VLA_ERR_INVALID_ARG, "context has no encoder stack");
+  const Stack& s = c->enc;
+  if (!patches || !out_dev) return fail(VLA_ERR_INVALID_ARG, "NULL patches / output");
+  if (n_img <= 0 || L <= 0) return fail(VLA_ERR_SHAPE, "n_img and L_img must be positive");
+  if (n_img > s.c.max_batch || L > s.c.max_tokens)
+    return fail(VLA_ERR_SHAPE, "n_img=%d L_img=%d exceed max_batch=%d max_tokens=%d", n_img, L, s.c.max_batch,
+                s.c.max_tokens);
+  for (int l = 0; l < s.c.n_blocks; ++l)
+    if (!s.blocks[l].loaded) return fail(VLA_ERR_NOT_LOADED, "encoder block %d has no weights", l);
+  if (!is_device(out_dev)) return fail(VLA_ERR_INVALID_ARG, "encoder output must be device memory");
+  const size_t n = (size_t)n_img * L * s.c.d_model;
+  Status st = intake(c, s, patches, n);
+  if (st.code) return st;
+  for (int l = 0; l < s.c.n_blocks; ++l)
+    if ((st = enc_block(c, s.blocks[l], n_img, L)).code) return st;
+  if (s.bf16())
+    KTRY(vla::f32_to_bf16(c->h, (bf16_t*)out_dev, n, c->compute));
+  else
+    HIPTRY(hipMemcpyAsync(out_dev, c->h, n * 4, hipMemcpyDeviceToDevice, c->compute));
+  return OK;
+}
+
+vla_status finish(vla_ctx* c, const Status& st) {
+  if (c) c->last_error = st.msg;
+  if (st.code != VLA_OK) g_last_error = st.msg;
+  return st.code;
+}
+
+Status build_rope(vla_ctx* c) {
+  const Stack& s = c->llm;
+  if (!s.present || !s.c.use_rope) return OK;
+  const int L = s.c.max_tokens, half = s.c.head_dim / 2;
+  std::vector<float> cs((size_t)L * half), sn((size_t)L * half);
+  for (int i = 0; i < half; ++i) {
+    // theta_i = base^(-2i/dh), angles formed in double precision
+    double theta = pow((double)s.c.rope_base, -2.0 * i / s.c.head_dim);
+    for (int p = 0; p < L; ++p) {
+      double phi = (double)p * theta;
+      cs[(size_t)p * half + i] = (float)cos(phi);
+      sn[(size_t)p * half + i] = (float)sin(phi);
+    }
+  }
+  Status st = copy_h2d(c->rope_cos, cs.data(), cs.size() * 4);
+  if (st.code) return st;
+  return copy_h2d(c->rope_sin, sn.data(), sn.size() * 4);
+}
+
+Status create(const vla_stack_cfg* llm, const vla_stack_cfg* enc, int device, void* arena, size_t arena_bytes,
+              void* compute, void* copy, vla_ctx** out) {
+  if (!out) return fail(VLA_ERR_INVALID_ARG, "NULL out");
+  *out = nullptr;
+  if (!llm && !enc) return fail(VLA_ERR_INVALID_ARG, "need at least one stack");
+  if (!arena) return fail(VLA_ERR_INVALID_ARG, "NULL arena");
+  std::unique_ptr<vla_ctx> c(new vla_ctx());
+  Status st = validate_stack(llm, true, &c->llm);
+  if (st.code) return st;
+  if ((st = validate_stack(enc, false, &c->enc)).code) return st;
+  Bump dry{nullptr};
+  layout(c.get(), dry);
+  if (dry.off > arena_bytes)
+    return fail(VLA_ERR_OOM, "arena of %zu bytes < %zu required", arena_bytes, dry.off);
+  if (((uintptr_t)arena) % ALIGN) return fail(VLA_ERR_INVALID_ARG, "arena must be %zu-byte aligned", ALIGN);
+  HIPTRY(hipSetDevice(device));
+  if (!is_device(arena)) return fail(VLA_ERR_INVALID_ARG, "arena is not device memory");
+  c->device = device;
+  c->arena = (char*)arena;
+  c->arena_bytes = arena_bytes;
+  Bump real{c->arena};
+  layout(c.get(), real);
+  c->used = real.off;
+  // zero the weight region so padding rows/columns are exact zeros
+  HIPTRY(hipMemset(c->arena, 0, c->used));
+  if (compute) {
+    c->compute = (hipStream_t)compute;
+  } else {
+    HIPTRY(hipStreamCreateWithFlags(&c->compute, hipStreamNonBlocking));
+    c->own_compute = true;
+  }
+  if (copy) {
+    c->copy = (hipStream_t)copy;
+  } else {
+    HIPTRY(hipStreamCreateWithFlags(&c->copy, hipStreamNonBlocking));
+    c->own_copy = true;
+  }
+  int nkv = c->llm.present ? c->llm.c.n_blocks : 0;
+  for (auto& sl : c->slots) {
+    HIPTRY(hipEventCreate(&sl.ev_start));
+    HIPTRY(hipEventCreate(&sl.ev_done));
+    HIPTRY(hipEventCreate(&sl.ev_hid));
+    HIPTRY(hipEventCreate(&sl.ev_copied));
+    sl.ev_kv.resize(nkv);
+    for (auto& e : sl.ev_kv) HIPTRY(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+  }
+  if ((st = build_rope(c.get())).code) return st;
+  HIPTRY(hipDeviceSynchronize());
+  *out = c.release();
+  return OK;
+}
+
+void destroy(vla_ctx* c) {
+  if (!c) return;
+  (void)hipSetDevice(c->device);
+  if (c->compute) (void)hipStreamSynchronize(c->compute);
+  if (c->copy) (void)hipStreamSynchronize(c->copy);
+  for (auto& sl : c->slots) {
+    for (hipEvent_t e : {sl.ev_start, sl.ev_done, sl.ev_hid, sl.ev_copied})
+      if (e) (void)hipEventDestroy(e);
+    for (hipEvent_t e : sl.ev_kv)
+      if (e) (void)hipEventDestroy(e);
+  }
+  if (c->own_compute) (void)hipStreamDestroy(c->compute);
+  if (c->own_copy) (void)hipStreamDestroy(c->copy);
+  delete c;
+}
+
+}  // namespace
+
+// ===================================================================== C ABI
+
+extern "C" {
+
+vla_status vla_query_sizes(const vla_stack_cfg* llm, const vla_stack_cfg* enc, int B, int L, int k,
+                           size_t* arena_bytes, size_t* hidden_bytes, size_t* kv_bytes) {
+  try {
+    vla_ctx tmp;
+    Status st = validate_stack(llm, true, &tmp.llm);
+    if (!st.code) st = validate_stack(enc, false, &tmp.enc);
+    if (!st.code && !llm && !enc) st = fail(VLA_ERR_INVALID_ARG, "need at least one stack");
+    if (st.code) return finish(nullptr, st);
+    Bump dry{nullptr};
+    layout(&tmp, dry);
+    if (arena_bytes) *arena_bytes = dry.off;
+    if (llm) {
+      if (B < 0 || L < 0 || k < 0) return finish(nullptr, fail(VLA_ERR_INVALID_ARG, "negative B, L or k"));
+      if (hidden_bytes) *hidden_bytes = (size_t)B * L * llm->d_model * dtype_size(llm->dtype);
+      if (kv_bytes)
+        *kv_bytes = (size_t)k * 2 * B * llm->n_kv_heads * L * llm->head_dim * dtype_size(llm->dtype);
+    } else {
+      if (hidden_bytes) *hidden_bytes = 0;
+      if (kv_bytes) *kv_bytes = 0;
+    }
+    return VLA_OK;
+  } catch (...) {
+    return finish(nullptr, fail(VLA_ERR_INVALID_ARG, "internal error"));
+  }
+}
+
+vla_status vla_create(const vla_stack_cfg* llm, const vla_stack_cfg* enc, int device, void* dev_arena,
+                      size_t arena_bytes, void* compute_stream, void* copy_stream, vla_ctx** out) {
+  try {
+    return finish(nullptr, create(llm, enc, device, dev_arena, arena_bytes, compute_stream, copy_stream, out));
+  } catch (const std::bad_alloc&) {
+    return finish(nullptr, fail(VLA_ERR_OOM, "host allocation failed"));
+  } catch (...) {
+    return finish(nullptr, fail(VLA_ERR_INVALID_ARG, "internal error"));
+  }
+}
+
+vla_status vla_load_block_weights(vla_ctx* ctx, vla_stack which, int block, const vla_block_weights* w) {
+  if (!ctx) return finish(nullptr, fail(VLA_ERR_INVALID_ARG, "NULL context"));
+  try {
+    if (!w) return finish(ctx, fail(VLA_ERR_INVALID_ARG, "NULL weights"));
+    if (which != VLA_STACK_LLM && which != VLA_STACK_ENC) return finish(ctx, fail(VLA_ERR_INVALID_ARG, "bad stack"));
+    Stack& s = which == VLA_STACK_LLM ? ctx->llm : ctx->enc;
+    if (!s.present) return finish(ctx, fail(VLA_ERR_INVALID_ARG, "context has no such stack"));
+    if (block < 0 || block >= s.c.n_blocks)
+      return finish(ctx, fail(VLA_ERR_SHAPE, "block %d outside [0, %d)", block, s.c.n_blocks));
+    if (hipSetDevice(ctx->device) != hipSuccess) return finish(ctx, fail(VLA_ERR_HIP, "hipSetDevice failed"));
+    // weights may still be read by in-flight work on the compute stream
+    if (hipStreamSynchronize(ctx->compute) != hipSuccess)
+      return finish(ctx, fail(VLA_ERR_HIP, "hipStreamSynchronize failed"));
+    return finish(ctx, load_block(ctx, s, block, w));
+  } catch (const std::bad_alloc&) {
+    return finish(ctx, fail(VLA_ERR_OOM, "host allocation failed"));
+  } catch (...) {
+    return finish(ctx, fail(VLA_ERR_INVALID_ARG, "internal error"));
+  }
+}
+
+vla_status vla_run_encoder(vla_ctx* ctx, uint64_t frame_id, const void* patches, int n_img, int L_img,
+                           void* out_dev) {
+  if (!ctx) return finish(nullptr, fail(VLA_ERR_INVALID_ARG, "NULL context"));
+  (void)frame_id;
+  try {
+    if (hipSetDevice(ctx->device) != hipSuccess) return finish(ctx, fail(VLA_ERR_HIP, "hipSetDevice failed"));
+    return finish(ctx, run_encoder(ctx, patches, n_img, L_img, out_dev));
+  } catch (...) {
+    return finish(ctx, fail(VLA_ERR_INVALID_ARG, "internal error"));
+  }
+}
+
+vla_status vla_run_blocks(vla_ctx* ctx, uint64_t frame_id, const void* tokens, int B, int L, int k_begin, int k_end,
+                          vla_boundary* out) {
+  if (!ctx) return finish(nullptr, fail(VLA_ERR_INVALID_ARG, "NULL context"));
+  try {
+    if (hipSetDevice(ctx->device) != hipSuccess) return finish(ctx, fail(VLA_ERR_HIP, "hipSetDevice failed"));
+    return finish(ctx, run_blocks(ctx, frame_id, tokens, B, L, k_begin, k_end, out));
+  } catch (...) {
+    return finish(ctx, fail(VLA_ERR_INVALID_ARG, "internal error"));
+  }
+}
+
+vla_status vla_run_prefix(vla_ctx* ctx, uint64_t frame_id, const void* tokens, int B, int L, int k,
+                          vla_boundary* out) {
+  return vla_run_blocks(ctx, frame_id, tokens, B, L, 0, k, out);
+}
+
+vla_status vla_wait_boundary(vla_ctx* ctx, uint64_t frame_id, int timeout_ms) {
+  if (!ctx) return finish(nullptr, fail(VLA_ERR_INVALID_ARG, "NULL context"));
+  try {
+    if (hipSetDevice(ctx->device) != hipSuccess) return finish(ctx, fail(VLA_ERR_HIP, "hipSetDevice failed"));
+    for (auto& sl : ctx->slots) {
+      if (!sl.used || sl.frame_id != frame_id) continue;
+      auto t0 = std::chrono::steady_clock::now();
+      for (;;) {
+        hipError_t e = hipEventQuery(sl.ev_copied);
+        if (e == hipSuccess) return finish(ctx, retire_slot(ctx, sl));
+        if (e != hipErrorNotReady) return finish(ctx, fail(VLA_ERR_HIP, "hipEventQuery: %s", hipGetErrorString(e)));
+        if (timeout_ms >= 0) {
+          auto ms = std::chrono::duration_cast<std::chrono::milliseconds>(std::chrono::steady_clock::now() - t0);
+          if (ms.count() >= timeout_ms)
+            return finish(ctx, fail(VLA_ERR_TIMEOUT, "frame %llu not done after %d ms", (unsigned long long)frame_id,
+                                    timeout_ms));
+        }
+        std::this_thread::sleep_for(std::chrono::microseconds(20));
+      }
+    }
+    if (ctx->history.count(frame_id)) return finish(ctx, OK);
+    return finish(ctx, fail(VLA_ERR_UNKNOWN_FRAME, "no frame %llu", (unsigned long long)frame_id));
+  } catch (...) {
+    return finish(ctx, fail(VLA_ERR_INVALID_ARG, "internal error"));
+  }
+}
+
+vla_status vla_frame_times(vla_ctx* ctx, uint64_t frame_id, float* t_gpu_ms, float* t_xfer_ms, float* t_total_ms) {
+  if (!ctx) return finish(nullptr, fail(VLA_ERR_INVALID_ARG, "NULL context"));
+  auto it = ctx->history.find(frame_id);
+  if (it == ctx->history.end())
+    return finish(ctx, fail(VLA_ERR_UNKNOWN_FRAME, "frame %llu has not been waited for", (unsigned long long)frame_id));
+  if (t_gpu_ms) *t_gpu_ms = it->second.gpu;
+  if (t_xfer_ms) *t_xfer_ms = it->second.xfer;
+  if (t_total_ms) *t_total_ms = it->second.total;
+  return finish(ctx, OK);
+}
+
+vla_status vla_arena_used(const vla_ctx* ctx, size_t* bytes) {
+  if (!ctx || !bytes) return VLA_ERR_INVALID_ARG;
+  *bytes = ctx->used;
+  return VLA_OK;
+}
+
+const char* vla_status_string(vla_status s) {
+  switch (s) {
+    case VLA_OK: return "ok";
+    case VLA_ERR_INVALID_ARG: return "invalid argument";
+    case VLA_ERR_SHAPE: return "shape outside the context's limits";
+    case VLA_ERR_NOT_LOADED: return "block weights not loaded";
+    case VLA_ERR_NOT_PINNED: return "host buffer not pinned";
+    case VLA_ERR_OOM: return "device arena too small";
+    case VLA_ERR_TIMEOUT: return "timed out";
+    case VLA_ERR_HIP: return "HIP runtime error";
+    case VLA_ERR_UNSUPPORTED: return "unsupported shape";
+    case VLA_ERR_UNKNOWN_FRAME: return "unknown frame id";
+  }
+  return "unknown status";
+}
+
+const char* vla_last_error(const vla_ctx* ctx) { return ctx ? ctx->last_error.c_str() : g_last_error.c_str(); }
+
+void vla_destroy(vla_ctx* ctx) {
+  try {
+    destroy(ctx);
+  } catch (...) {
+  }
+}
+
+}  // extern "C"

@@ -1,0 +1,77 @@
+"""Per-kernel parity of the HIP operators against the oracle's definitions,
+called through the C ABI (include/vla_ops.h), on ragged shapes."""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+
+pytestmark = pytest.mark.gpu
+
+
+def _dev_bf16(a_u16):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a_u16).view(np.int16)).cuda()
+
+
+@pytest.mark.parametrize("M,N,K", [(128, 128, 64), (200, 320, 128), (77, 96, 256), (1024, 1152, 896),
+                                   (33, 4096, 4096)])
+def test_gemm_bf16(M, N, K):
+    import torch
+    from paper_2608_14586_amd import binding as vb
+    A = synth.normal_bf16(synth.seed_of("gemmA", M, N, K), (M, K))
+    W = synth.normal_bf16(synth.seed_of("gemmW", M, N, K), (N, K))
+    C = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    vb.vla_op_gemm_bf16(_dev_bf16(A), _dev_bf16(W), C, M, N, K)
+    torch.cuda.synchronize()
+    ref = synth.as_f32(A).astype(np.float64) @ synth.as_f32(W).astype(np.float64).T
+    err = np.abs(C.cpu().numpy() - ref).max() / np.abs(ref).max()
+    assert err < 1e-5, err
+
+
+@pytest.mark.parametrize("B,H,Hkv,L,dh,causal", [
+    (1, 4, 4, 128, 128, True), (1, 4, 4, 200, 128, True), (2, 6, 2, 77, 64, True), (1, 14, 2, 300, 64, True),
+    (3, 4, 4, 130, 64, False), (1, 2, 2, 1024, 64, False), (1, 2, 1, 513, 128, False)])
+def test_attention_bf16(B, H, Hkv, L, dh, causal):
+    import torch
+    from paper_2608_14586_amd import binding as vb
+    tag = (B, H, Hkv, L, dh, causal)
+    q = synth.normal_bf16(synth.seed_of("q", *tag), (B, H, L, dh))
+    k = synth.normal_bf16(synth.seed_of("k", *tag), (B, Hkv, L, dh))
+    v = synth.normal_bf16(synth.seed_of("v", *tag), (B, Hkv, L, dh))
+    ldvt = (L + 63) // 64 * 64
+    vt = np.zeros((B, Hkv, dh, ldvt), np.uint16)
+    vt[..., :L] = v.transpose(0, 1, 3, 2)
+    o = torch.empty((B, L, H * dh), dtype=torch.bfloat16, device="cuda")
+    vb.vla_op_attention_bf16(_dev_bf16(q), _dev_bf16(k), _dev_bf16(vt), ldvt, o, B, H, Hkv, L, dh, causal)
+    torch.cuda.synchronize()
+    got = o.float().cpu().numpy()
+    for b in range(B):
+        ref = oracle.attention(synth.as_f32(q[b]).transpose(1, 0, 2).astype(np.float64),
+                               synth.as_f32(k[b]).transpose(1, 0, 2).astype(np.float64),
+                               synth.as_f32(v[b]).transpose(1, 0, 2).astype(np.float64), causal)
+        ref = ref.reshape(L, H * dh)
+        e = np.linalg.norm(got[b] - ref) / np.linalg.norm(ref)
+        assert e < 1e-2, (b, e)
+
+
+@pytest.mark.parametrize("M,d,ln", [(5, 256, False), (300, 896, False), (64, 4096, False), (70, 1024, True),
+                                    (9, 4096, True)])
+def test_norms_bf16(M, d, ln):
+    import torch
+    from paper_2608_14586_amd import binding as vb
+    x = synth.normal_f32(synth.seed_of("nx", M, d), (M, d), std=3.0, mean=0.5)
+    g = synth.uniform_f32(synth.seed_of("ng", d), (d,), 0.5, 1.5)
+    bta = synth.normal_f32(synth.seed_of("nb", d), (d,), std=0.1) if ln else None
+    y = torch.empty((M, d), dtype=torch.bfloat16, device="cuda")
+    tx, tg = torch.from_numpy(x).cuda(), torch.from_numpy(g).cuda()
+    tb = torch.from_numpy(bta).cuda() if ln else None
+    vb.vla_op_norm_bf16(tx, tg, tb, 1e-6, y, M, d)
+    torch.cuda.synchronize()
+    x64 = x.astype(np.float64)
+    ref = oracle.layer_norm(x64, g, bta, 1e-6) if ln else oracle.rms_norm(x64, g, 1e-6)
+    got = y.float().cpu().numpy()
+    # bf16 output: within half an ulp of bf16 (relative 2^-9) plus fp32 noise
+    assert np.all(np.abs(got - ref) <= np.abs(ref) * 2.0 ** -8 + 1e-6)
