@@ -1,0 +1,246 @@
+"""Benchmark of the GPU-resident prefix on one MI355X.
+
+One step = one frame of the partitioned pipeline's GPU stage (Sec. IV-A/C):
+the ViT-L-shaped encoder over 6 camera images x 1024 patch tokens, then the
+7B-shaped decoder blocks [0, k) as a causal prefill over 2048 tokens, then the
+handoff of the boundary hidden state and the k-layer KV cache to pinned host
+memory on a side stream (overlapping the next frame's encoder).  The headline
+is k = 16; the sweep reports k in {8, 16, 24, 32}.  Inputs and weights are
+seeded synthetic tensors already resident in HBM; weights are random-init
+N(0, 0.02) at the stated shapes.
+
+Prints ONE JSON line (rank 0, N = 1 only).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def class_work(wl, kind, k):
+    """Algorithmic FLOPs (GEMM / attention classes) or HBM bytes (norm) per
+    launch of each kernel class of one stack, from the stack shapes."""
+    if kind == "llm":
+        s, B, L = wl.llm, wl.batch, wl.seq
+        M = B * L
+        pairs = B * L * (L + 1) // 2  # causal query-key pairs per head
+    else:
+        s, B, L = wl.enc, wl.n_img, wl.img_tokens
+        M = B * L
+        pairs = B * L * L
+    d, H, Hkv, dh, F = s.d_model, s.n_heads, s.n_kv_heads, s.head_dim, s.d_ff
+    up_rows = 2 * F if kind == "llm" else F
+    return {
+        "qkv": ("flop", 2.0 * M * d * (H + 2 * Hkv) * dh),
+        "attn": ("flop", 4.0 * pairs * dh * H),
+        "oproj": ("flop", 2.0 * M * H * dh * d),
+        "mlp_up": ("flop", 2.0 * M * d * up_rows),
+        "mlp_down": ("flop", 2.0 * M * F * d),
+        "norm": ("byte", M * d * 4.0 + M * d * 2.0 + d * 4.0 * (2 if s.norm_is_layernorm else 1)),
+    }
+
+
+def frame_flops(wl, k):
+    tot = 0.0
+    for kind, n in (("llm", k), ("enc", wl.enc.n_blocks)):
+        w = class_work(wl, kind, k)
+        tot += n * sum(v for c, (u, v) in w.items() if u == "flop")
+    return tot
+
+
+def cpu_baseline(wl, k, budget_s=20.0):
+    """The oracle timed on this host on a bounded sample: decoder blocks at the
+    full sequence length and encoder blocks over all 6 images, timed until the
+    budget is spent, scaled to one frame (k decoder + 24 encoder blocks)."""
+    import numpy as np
+    import oracle
+    import synth
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    tok = synth.as_f32(synth.tokens(wl, frame=0))
+    pat = synth.as_f32(synth.patches(wl, frame=0))
+    t_llm, n_llm, t_enc, n_enc = 0.0, 0, 0.0, 0
+    t_start = time.time()
+    while (n_llm == 0 or n_enc == 0 or time.time() - t_start < budget_s) and n_llm < 4:
+        W = {n: synth.as_f32(a) for n, a in synth.llm_block_weights(wl, n_llm).items()}
+        t0 = time.time()
+        oracle.run_prefix(tok, lambda l: W, wl.llm, 1, keep_kv=False)
+        t_llm += time.time() - t0
+        n_llm += 1
+        E = {n: synth.as_f32(a) for n, a in synth.vit_block_weights(wl, n_enc).items()}
+        t0 = time.time()
+        oracle.run_encoder(pat, lambda l: E, wl.enc, n_blocks=1)
+        t_enc += time.time() - t0
+        n_enc += 1
+    per_frame = k * t_llm / n_llm + wl.enc.n_blocks * t_enc / n_enc
+    return {"value": wl.seq / per_frame, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": "%d decoder block(s) at L=%d and %d ViT block(s) over %dx%d patches, numpy fp32, "
+                      "scaled to %d decoder + %d encoder blocks per frame (%.1f s per frame)"
+                      % (n_llm, wl.seq, n_enc, wl.n_img, wl.img_tokens, k, wl.enc.n_blocks, per_frame),
+            "blas": "numpy %s" % np.__version__}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--k", type=int, default=16)
+    ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the prefix is a single-GPU stage (frames, cameras or block "
+              "ranges would shard across GPUs; see DESIGN.md). Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2608_14586_amd import binding as vb
+
+    wl = synth.CONFIGS["sweep7b"]
+    ks = sorted(set(([] if args.no_sweep else list(wl.ks)) + [args.k]))
+    kmax = max(ks)
+    s, e = wl.llm, wl.enc
+    L, n_img, L_img = wl.seq, wl.n_img, wl.img_tokens
+    llm_cfg = vb.stack_cfg(s, "bf16", max_tokens=L, max_batch=1, n_blocks=kmax)
+    enc_cfg = vb.stack_cfg(e, "bf16", max_tokens=L_img, max_batch=n_img)
+    t0 = time.time()
+    ctx = vb.Context(llm=llm_cfg, enc=enc_cfg)
+    log("arena %.2f GiB" % (ctx.arena_bytes / 2 ** 30))
+    for l in range(e.n_blocks):
+        ctx.vla_load_block_weights(vb.VLA_STACK_ENC, l, synth.vit_block_weights(wl, l))
+    for l in range(kmax):
+        ctx.vla_load_block_weights(vb.VLA_STACK_LLM, l, synth.llm_block_weights(wl, l))
+        if l % 8 == 7:
+            log("loaded %d/%d decoder blocks (%.0fs)" % (l + 1, kmax, time.time() - t0))
+    dev = torch.device("cuda:0")
+    toks = [torch.from_numpy(synth.tokens(wl, frame=f).view(np.int16)).to(dev) for f in range(2)]
+    pats = [torch.from_numpy(synth.patches(wl, frame=f).view(np.int16)).to(dev) for f in range(2)]
+    enc_out = torch.empty((n_img, L_img, e.d_model), dtype=torch.bfloat16, device=dev)
+    torch.cuda.synchronize()
+    log("weights and inputs resident (%.0fs)" % (time.time() - t0))
+
+    fid = [1000]
+
+    def run(k, n, profile=False):
+        bnds = [vb.Boundary(1, L, s.d_model, k, s.n_kv_heads, s.head_dim) for _ in range(3)]
+        ids = []
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        enc_ms = []
+        if profile:
+            ctx.vla_profile(True)
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        for i in range(n):
+            f = fid[0]
+            fid[0] += 1
+            st = ctx.compute_stream
+            if i == 0:
+                ev0.record(st)
+            ctx.vla_run_encoder(f, pats[i % 2], n_img, L_img, enc_out)
+            if i == 0:
+                ev1.record(st)
+            ctx.vla_run_prefix(f, toks[i % 2], 1, L, k, bnds[i % 3])
+            ids.append(f)
+        for f in ids[-3:]:
+            ctx.vla_wait_boundary(f, 120000)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t
+        if profile:
+            ctx.vla_profile(False)
+        enc_ms.append(ev0.elapsed_time(ev1))
+        times = [ctx.vla_frame_times(f) for f in ids[-3:]]
+        return wall * 1000.0 / n, times, enc_ms[0]
+
+    results = {}
+    for k in ks:
+        run(k, args.warmup)
+        prof = k == args.k
+        ms, times, enc_ms = run(k, args.steps, profile=prof)
+        foot = vb.vla_query_sizes(vb.stack_cfg(s, "bf16", max_tokens=L, max_batch=1, n_blocks=k), enc_cfg,
+                                  1, L, k)
+        r = {"ms_per_frame": round(ms, 3), "prefix_tokens_per_s": round(L / (ms / 1000.0), 1),
+             "t_gpu_prefix_ms": round(float(np.mean([t[0] for t in times])), 3),
+             "t_boundary_copy_ms": round(float(np.mean([t[1] for t in times])), 4),
+             "t_prefix_plus_handoff_ms": round(float(np.mean([t[2] for t in times])), 3),
+             "t_encoder_ms": round(enc_ms, 3),
+             "frame_tflops": round(frame_flops(wl, k) / 1e12, 3),
+             "mfma_frac_of_bf16_peak": round(frame_flops(wl, k) / (ms / 1000.0) / 1e12 / PEAK_BF16_TFLOPS, 4),
+             "hbm_footprint_gib": round(foot[0] / 2 ** 30, 3),
+             "handoff_bytes": foot[1] + foot[2]}
+        if prof:
+            classes = {}
+            for kind, stk, nl in (("llm", vb.VLA_STACK_LLM, k), ("enc", vb.VLA_STACK_ENC, e.n_blocks)):
+                work = class_work(wl, kind, k)
+                for ci, cname in enumerate(vb.KERNEL_CLASSES):
+                    tot, cnt = ctx.vla_profile_read(stk, ci)
+                    if cnt == 0:
+                        continue
+                    ent = {"ms_total": round(tot, 4), "launches": cnt, "avg_us": round(tot / cnt * 1000, 2)}
+                    if cname in work:
+                        unit, per = work[cname]
+                        avg_s = tot / cnt / 1000.0
+                        if unit == "flop":
+                            ent["tflops"] = round(per / avg_s / 1e12, 1)
+                            ent["frac"] = round(per / avg_s / 1e12 / PEAK_BF16_TFLOPS, 4)
+                        else:
+                            ent["gbs"] = round(per / avg_s / 1e9, 1)
+                            ent["frac"] = round(per / avg_s / 1e9 / PEAK_HBM_GBS, 4)
+                        ent["per_launch"] = per
+                    classes["%s.%s" % (kind, cname)] = ent
+            r["kernels"] = classes
+        results[k] = r
+        log("k=%d: %s" % (k, json.dumps({kk: v for kk, v in r.items() if kk != "kernels"})))
+
+    head = results[args.k]
+    kern = head["kernels"]
+    dom_name = max((n for n in kern if "tflops" in kern[n] or "gbs" in kern[n]), key=lambda n: kern[n]["ms_total"])
+    dom = kern[dom_name]
+    roofline = {"kernel": dom_name, "bound": "mfma" if "tflops" in dom else "hbm",
+                "achieved": dom.get("tflops", dom.get("gbs")), "peak": PEAK_BF16_TFLOPS if "tflops" in dom else PEAK_HBM_GBS,
+                "unit": "TFLOP/s" if "tflops" in dom else "GB/s", "frac": dom["frac"], "traffic": None,
+                "per_launch": dom["per_launch"], "avg_launch_us": dom["avg_us"]}
+    out = {
+        "metric": "GPU-prefix tokens/s at boundary k=%d (frame: ViT-L encoder 6x1024 + 7B-shaped decoder blocks "
+                  "[0,k) over 2048 tokens + boundary/KV handoff to pinned host)" % args.k,
+        "value": head["prefix_tokens_per_s"], "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": head["ms_per_frame"], "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "sweep7b: encoder 24x ViT-L block (d=1024, 16x64, GELU 4096) over 6 images x 1024 "
+                               "patches; decoder 7B-shaped blocks (d=4096, 32x128 MHA, SwiGLU 11008, RoPE) [0,k) "
+                               "over 1x2048 tokens; bf16 weights N(0,0.02), inputs N(0,1)",
+                   "k": args.k, "seq_len": L, "batch": 1, "n_img": n_img, "img_tokens": L_img},
+        "mfma_frac_of_bf16_peak": head["mfma_frac_of_bf16_peak"],
+        "roofline": roofline,
+        "kernels": kern,
+        "sweep": {str(k): {kk: v for kk, v in r.items() if kk != "kernels"} for k, r in results.items()},
+    }
+    ctx.vla_destroy()
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a bounded sample")
+        out["cpu_baseline"] = cpu_baseline(wl, args.k)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -98,7 +98,8 @@ typedef struct {
 
 /*
  * Caller-owned, caller-allocated PINNED host memory receiving one frame's
- * handoff.  hidden: [B][L][d] in out_dtype (bf16 requires a bf16 stack).
+ * handoff.  hidden: [B][L][d] in out_dtype (either dtype for either stack;
+ * f32 from a bf16 stack is the un-rounded fp32 residual).
  * kv: [k_end-k_begin][2][B][n_kv_heads][L][head_dim] in the stack's dtype,
  * K after RoPE, V as projected; may be NULL (kv_bytes 0) to skip the KV copy.
  * frame_id is written by the library.  The buffers must stay untouched until
@@ -141,15 +142,18 @@ vla_status vla_run_encoder(vla_ctx *ctx, uint64_t frame_id, const void *patches,
  * blocks are copied to `out` on the copy stream, each layer's KV as soon as
  * that layer has written it.  k = 0 hands back the input (Eq. (5) with no
  * blocks).  Enqueued; returns after launch.  Equivalent to
- * vla_run_blocks(ctx, frame_id, tokens, B, L, 0, k, out). */
+ * vla_run_blocks(ctx, frame_id, tokens, <stack dtype>, B, L, 0, k, out). */
 vla_status vla_run_prefix(vla_ctx *ctx, uint64_t frame_id, const void *tokens, int B, int L, int k,
                           vla_boundary *out);
 
 /* Decoder blocks [k_begin, k_end) over an intermediate state h^(k_begin)
- * given as `tokens` (positions still start at 0): one stage of the block
- * pipeline of Eq. (6).  KV in `out` covers the blocks run. */
-vla_status vla_run_blocks(vla_ctx *ctx, uint64_t frame_id, const void *tokens, int B, int L, int k_begin,
-                          int k_end, vla_boundary *out);
+ * given as `tokens` in element type in_dtype (positions still start at 0):
+ * one stage of the block pipeline of Eq. (6).  An f32 input continues the
+ * fp32 residual stream exactly, so chaining f32 boundaries of adjacent
+ * ranges reproduces one run over their union bit for bit.  KV in `out` covers
+ * the blocks run. */
+vla_status vla_run_blocks(vla_ctx *ctx, uint64_t frame_id, const void *tokens, vla_dtype in_dtype, int B, int L,
+                          int k_begin, int k_end, vla_boundary *out);
 
 /* Block the host until frame_id's handoff is complete (its host buffers are
  * then readable), or timeout_ms elapses (< 0: wait forever). */
@@ -162,6 +166,25 @@ vla_status vla_wait_boundary(vla_ctx *ctx, uint64_t frame_id, int timeout_ms);
  * pointer may be NULL. */
 vla_status vla_frame_times(vla_ctx *ctx, uint64_t frame_id, float *t_gpu_ms, float *t_xfer_ms,
                            float *t_total_ms);
+
+/* Kernel classes timed by the profiler, per stack. */
+typedef enum {
+  VLA_K_NORM = 0,     /* RMSNorm / LayerNorm (both per block) */
+  VLA_K_QKV = 1,      /* QKV projection + RoPE + cache write */
+  VLA_K_ATTN = 2,     /* attention */
+  VLA_K_OPROJ = 3,    /* output projection + residual */
+  VLA_K_MLP_UP = 4,   /* gate/up + SwiGLU, or fc1 + GELU */
+  VLA_K_MLP_DOWN = 5, /* down / fc2 + residual */
+  VLA_K_OTHER = 6,    /* intake, boundary cast (fp32 path: its extra kernels) */
+  VLA_K_COUNT = 7
+} vla_kernel_class;
+
+/* Start (enable != 0, clearing previous totals) or stop timing every kernel
+ * launch with a pair of HIP events on the compute stream. */
+vla_status vla_profile(vla_ctx *ctx, int enable);
+/* Totals since vla_profile(ctx, 1) for one stack and class: summed kernel
+ * time in ms and launch count.  Synchronises the compute stream. */
+vla_status vla_profile_read(vla_ctx *ctx, vla_stack which, vla_kernel_class cls, double *ms_total, int *launches);
 
 /* Bytes of the arena in use after the loads so far (weights + workspace). */
 vla_status vla_arena_used(const vla_ctx *ctx, size_t *bytes);

@@ -23,6 +23,7 @@ STATUS = {0: "VLA_OK", -1: "VLA_ERR_INVALID_ARG", -2: "VLA_ERR_SHAPE", -3: "VLA_
           -8: "VLA_ERR_UNSUPPORTED", -9: "VLA_ERR_UNKNOWN_FRAME"}
 VLA_BF16, VLA_F32 = 0, 1
 VLA_STACK_LLM, VLA_STACK_ENC = 0, 1
+KERNEL_CLASSES = ["norm", "qkv", "attn", "oproj", "mlp_up", "mlp_down", "other"]
 
 
 class VlaError(RuntimeError):
@@ -72,7 +73,9 @@ def lib():
             "vla_load_block_weights": [c_void_p, c_int, c_int, P(vla_block_weights)],
             "vla_run_encoder": [c_void_p, c_uint64, c_void_p, c_int, c_int, c_void_p],
             "vla_run_prefix": [c_void_p, c_uint64, c_void_p, c_int, c_int, c_int, P(vla_boundary)],
-            "vla_run_blocks": [c_void_p, c_uint64, c_void_p, c_int, c_int, c_int, c_int, P(vla_boundary)],
+            "vla_run_blocks": [c_void_p, c_uint64, c_void_p, c_int, c_int, c_int, c_int, c_int, P(vla_boundary)],
+            "vla_profile": [c_void_p, c_int],
+            "vla_profile_read": [c_void_p, c_int, c_int, P(ctypes.c_double), P(c_int)],
             "vla_wait_boundary": [c_void_p, c_uint64, c_int],
             "vla_frame_times": [c_void_p, c_uint64, P(c_float), P(c_float), P(c_float)],
             "vla_arena_used": [c_void_p, P(c_size_t)],
@@ -192,9 +195,18 @@ class Context:
     def vla_run_prefix(self, frame_id: int, tokens, B: int, L: int, k: int, out: Boundary):
         _check(lib().vla_run_prefix(self.h, frame_id, _ptr(tokens), B, L, k, ctypes.byref(out.c)), self.h)
 
-    def vla_run_blocks(self, frame_id: int, tokens, B: int, L: int, k_begin: int, k_end: int, out: Boundary):
-        _check(lib().vla_run_blocks(self.h, frame_id, _ptr(tokens), B, L, k_begin, k_end, ctypes.byref(out.c)),
-               self.h)
+    def vla_run_blocks(self, frame_id: int, tokens, in_dtype: int, B: int, L: int, k_begin: int, k_end: int,
+                       out: Boundary):
+        _check(lib().vla_run_blocks(self.h, frame_id, _ptr(tokens), in_dtype, B, L, k_begin, k_end,
+                                    ctypes.byref(out.c)), self.h)
+
+    def vla_profile(self, enable: bool):
+        _check(lib().vla_profile(self.h, int(enable)), self.h)
+
+    def vla_profile_read(self, which: int, cls: int):
+        ms, n = ctypes.c_double(), c_int()
+        _check(lib().vla_profile_read(self.h, which, cls, ctypes.byref(ms), ctypes.byref(n)), self.h)
+        return ms.value, n.value
 
     def vla_wait_boundary(self, frame_id: int, timeout_ms: int = -1):
         _check(lib().vla_wait_boundary(self.h, frame_id, timeout_ms), self.h)

@@ -156,6 +156,18 @@ struct vla_ctx {
   Slot slots[NSLOT];
   int next_slot = 0;
   std::map<uint64_t, FrameTimes> history;
+
+  // kernel profiler: event pairs around each launch on the compute stream
+  struct ProfRec {
+    int idx;
+    hipEvent_t a, b;
+  };
+  bool prof_on = false;
+  std::vector<hipEvent_t> prof_pool;
+  size_t prof_used = 0;
+  std::vector<ProfRec> prof_recs;
+  double prof_ms[2][VLA_K_COUNT] = {};
+  int prof_n[2][VLA_K_COUNT] = {};
 };
 
 namespace {
@@ -384,21 +396,73 @@ bool is_device(const void* p) {
   return a.type == hipMemoryTypeDevice || a.type == hipMemoryTypeManaged;
 }
 
+Status prof_event(vla_ctx* c, hipEvent_t* e) {
+  if (c->prof_used == c->prof_pool.size()) {
+    hipEvent_t ev;
+    HIPTRY(hipEventCreate(&ev));
+    c->prof_pool.push_back(ev);
+  }
+  *e = c->prof_pool[c->prof_used++];
+  return OK;
+}
+
+Status prof_drain(vla_ctx* c) {
+  HIPTRY(hipStreamSynchronize(c->compute));
+  for (const auto& r : c->prof_recs) {
+    float ms = 0.f;
+    HIPTRY(hipEventElapsedTime(&ms, r.a, r.b));
+    c->prof_ms[r.idx / VLA_K_COUNT][r.idx % VLA_K_COUNT] += ms;
+    c->prof_n[r.idx / VLA_K_COUNT][r.idx % VLA_K_COUNT] += 1;
+  }
+  c->prof_recs.clear();
+  c->prof_used = 0;
+  return OK;
+}
+
 #define KTRY(expr)                                                                                   \
   do {                                                                                               \
     hipError_t e_ = (expr);                                                                          \
     if (e_ != hipSuccess) return fail(VLA_ERR_HIP, "launch %s: %s", #expr, hipGetErrorString(e_)); \
   } while (0)
 
-// input[B*L][d] (host or device, stack dtype) -> fp32 residual c->h
-Status intake(vla_ctx* c, const Stack& s, const void* in, size_t n) {
+// Launch `expr` on the compute stream; with the profiler on, bracket it with
+// a pair of events attributed to (stack, class).
+#define PLAUNCH(c, stk, cls, expr)                                                          \
+  do {                                                                                      \
+    hipEvent_t a_ = nullptr, b_ = nullptr;                                                  \
+    if ((c)->prof_on) {                                                                     \
+      Status s_ = prof_event((c), &a_);                                                     \
+      if (s_.code) return s_;                                                               \
+      HIPTRY(hipEventRecord(a_, (c)->compute));                                             \
+    }                                                                                       \
+    KTRY(expr);                                                                             \
+    if ((c)->prof_on) {                                                                     \
+      Status s_ = prof_event((c), &b_);                                                     \
+      if (s_.code) return s_;                                                               \
+      HIPTRY(hipEventRecord(b_, (c)->compute));                                             \
+      (c)->prof_recs.push_back(vla_ctx::ProfRec{(stk) * VLA_K_COUNT + (cls), a_, b_});      \
+      if ((c)->prof_recs.size() >= (1u << 16)) {                                            \
+        Status d_ = prof_drain(c);                                                          \
+        if (d_.code) return d_;                                                             \
+      }                                                                                     \
+    }                                                                                       \
+  } while (0)
+
+// input[B*L][d] (host or device, element type in_dt) -> fp32 residual c->h
+Status intake(vla_ctx* c, int stk, vla_dtype in_dt, const void* in, size_t n) {
   const void* src = in;
   if (!is_device(in)) {
-    HIPTRY(hipMemcpyAsync(c->tok, in, n * s.esz, hipMemcpyHostToDevice, c->compute));
+    // host input: fp32 goes straight into the residual, bf16 through the
+    // input staging buffer
+    if (in_dt == VLA_F32) {
+      HIPTRY(hipMemcpyAsync(c->h, in, n * 4, hipMemcpyHostToDevice, c->compute));
+      return OK;
+    }
+    HIPTRY(hipMemcpyAsync(c->tok, in, n * 2, hipMemcpyHostToDevice, c->compute));
     src = c->tok;
   }
-  if (s.bf16())
-    KTRY(vla::bf16_to_f32((const bf16_t*)src, c->h, n, c->compute));
+  if (in_dt == VLA_BF16)
+    PLAUNCH(c, stk, VLA_K_OTHER, vla::bf16_to_f32((const bf16_t*)src, c->h, n, c->compute));
   else
     HIPTRY(hipMemcpyAsync(c->h, src, n * 4, hipMemcpyDeviceToDevice, c->compute));
   return OK;
@@ -409,11 +473,11 @@ Status llm_block_bf16(vla_ctx* c, const Stack::Block& w, int B, int L, bf16_t* k
   const vla_stack_cfg& k = s.c;
   const int M = B * L, d = k.d_model;
   hipStream_t st = c->compute;
-  KTRY(vla::rmsnorm_bf16(c->h, w.n1g, k.norm_eps, (bf16_t*)c->x, M, d, st));
+  PLAUNCH(c, VLA_STACK_LLM, VLA_K_NORM, vla::rmsnorm_bf16(c->h, w.n1g, k.norm_eps, (bf16_t*)c->x, M, d, st));
   vla::QkvArgs qa{nullptr, k.use_rope ? c->rope_cos : nullptr, k.use_rope ? c->rope_sin : nullptr,
                   (bf16_t*)c->q, kdst, vdst, (bf16_t*)c->vt, round_up(L, 64), L, k.n_heads, k.n_kv_heads,
                   k.head_dim};
-  KTRY(vla::gemm_bf16_qkv((const bf16_t*)c->x, d, (const bf16_t*)w.w_qkv, d, qa, M, s.qkv_n, d, st));
+  PLAUNCH(c, VLA_STACK_LLM, VLA_K_QKV, vla::gemm_bf16_qkv((const bf16_t*)c->x, d, (const bf16_t*)w.w_qkv, d, qa, M, s.qkv_n, d, st));
   return OK;
 }
 
@@ -422,14 +486,14 @@ Status llm_block_bf16_rest(vla_ctx* c, const Stack::Block& w, int B, int L, cons
   const vla_stack_cfg& k = s.c;
   const int M = B * L, d = k.d_model;
   hipStream_t st = c->compute;
-  KTRY(vla::attention_bf16((const bf16_t*)c->q, kdst, (const bf16_t*)c->vt, round_up(L, 64), (bf16_t*)c->o, B,
+  PLAUNCH(c, VLA_STACK_LLM, VLA_K_ATTN, vla::attention_bf16((const bf16_t*)c->q, kdst, (const bf16_t*)c->vt, round_up(L, 64), (bf16_t*)c->o, B,
                            k.n_heads, k.n_kv_heads, L, k.head_dim, k.causal != 0, st));
-  KTRY(vla::gemm_bf16_residual((const bf16_t*)c->o, s.hd, (const bf16_t*)w.w_o, s.hd, c->h, d, nullptr, M, d, s.hd,
+  PLAUNCH(c, VLA_STACK_LLM, VLA_K_OPROJ, vla::gemm_bf16_residual((const bf16_t*)c->o, s.hd, (const bf16_t*)w.w_o, s.hd, c->h, d, nullptr, M, d, s.hd,
                                st));
-  KTRY(vla::rmsnorm_bf16(c->h, w.n2g, k.norm_eps, (bf16_t*)c->x, M, d, st));
-  KTRY(vla::gemm_bf16_swiglu((const bf16_t*)c->x, d, (const bf16_t*)w.w_up, d, (bf16_t*)c->act, s.f_pad, M,
+  PLAUNCH(c, VLA_STACK_LLM, VLA_K_NORM, vla::rmsnorm_bf16(c->h, w.n2g, k.norm_eps, (bf16_t*)c->x, M, d, st));
+  PLAUNCH(c, VLA_STACK_LLM, VLA_K_MLP_UP, vla::gemm_bf16_swiglu((const bf16_t*)c->x, d, (const bf16_t*)w.w_up, d, (bf16_t*)c->act, s.f_pad, M,
                              2 * s.f_pad, d, st));
-  KTRY(vla::gemm_bf16_residual((const bf16_t*)c->act, s.f_pad, (const bf16_t*)w.w_down, s.f_pad, c->h, d, nullptr, M,
+  PLAUNCH(c, VLA_STACK_LLM, VLA_K_MLP_DOWN, vla::gemm_bf16_residual((const bf16_t*)c->act, s.f_pad, (const bf16_t*)w.w_down, s.f_pad, c->h, d, nullptr, M,
                                d, s.f_pad, st));
   return OK;
 }
@@ -440,9 +504,9 @@ Status llm_block_f32(vla_ctx* c, const Stack::Block& w, int B, int L, float* kds
   const int M = B * L, d = k.d_model;
   hipStream_t st = c->compute;
   float* x = (float*)c->x;
-  KTRY(vla::rmsnorm_f32(c->h, w.n1g, k.norm_eps, x, M, d, st));
-  KTRY(vla::gemm_f32(x, d, (const float*)w.w_qkv, d, c->qkv_raw, s.qkv_n, nullptr, 0, M, s.qkv_n, d, st));
-  KTRY(vla::qkv_split_f32(c->qkv_raw, k.use_rope ? c->rope_cos : nullptr, k.use_rope ? c->rope_sin : nullptr,
+  PLAUNCH(c, VLA_STACK_LLM, VLA_K_NORM, vla::rmsnorm_f32(c->h, w.n1g, k.norm_eps, x, M, d, st));
+  PLAUNCH(c, VLA_STACK_LLM, VLA_K_QKV, vla::gemm_f32(x, d, (const float*)w.w_qkv, d, c->qkv_raw, s.qkv_n, nullptr, 0, M, s.qkv_n, d, st));
+  PLAUNCH(c, VLA_STACK_LLM, VLA_K_QKV, vla::qkv_split_f32(c->qkv_raw, k.use_rope ? c->rope_cos : nullptr, k.use_rope ? c->rope_sin : nullptr,
                           (float*)c->q, kdst, vdst, nullptr, 0, B, L, k.n_heads, k.n_kv_heads, k.head_dim, st));
   return OK;
 }
@@ -455,13 +519,13 @@ Status llm_block_f32_rest(vla_ctx* c, const Stack::Block& w, int B, int L, const
   float* x = (float*)c->x;
   float* gu = (float*)c->act;
   float* a = gu + (size_t)M * 2 * F;
-  KTRY(vla::attention_f32((const float*)c->q, kdst, vdst, (float*)c->o, B, k.n_heads, k.n_kv_heads, L, k.head_dim,
+  PLAUNCH(c, VLA_STACK_LLM, VLA_K_ATTN, vla::attention_f32((const float*)c->q, kdst, vdst, (float*)c->o, B, k.n_heads, k.n_kv_heads, L, k.head_dim,
                           k.causal != 0, st));
-  KTRY(vla::gemm_f32((const float*)c->o, s.hd, (const float*)w.w_o, s.hd, c->h, d, nullptr, 1, M, d, s.hd, st));
-  KTRY(vla::rmsnorm_f32(c->h, w.n2g, k.norm_eps, x, M, d, st));
-  KTRY(vla::gemm_f32(x, d, (const float*)w.w_up, d, gu, 2 * F, nullptr, 0, M, 2 * F, d, st));
-  KTRY(vla::swiglu_f32(gu, a, M, F, st));
-  KTRY(vla::gemm_f32(a, F, (const float*)w.w_down, F, c->h, d, nullptr, 1, M, d, F, st));
+  PLAUNCH(c, VLA_STACK_LLM, VLA_K_OPROJ, vla::gemm_f32((const float*)c->o, s.hd, (const float*)w.w_o, s.hd, c->h, d, nullptr, 1, M, d, s.hd, st));
+  PLAUNCH(c, VLA_STACK_LLM, VLA_K_NORM, vla::rmsnorm_f32(c->h, w.n2g, k.norm_eps, x, M, d, st));
+  PLAUNCH(c, VLA_STACK_LLM, VLA_K_MLP_UP, vla::gemm_f32(x, d, (const float*)w.w_up, d, gu, 2 * F, nullptr, 0, M, 2 * F, d, st));
+  PLAUNCH(c, VLA_STACK_LLM, VLA_K_MLP_UP, vla::swiglu_f32(gu, a, M, F, st));
+  PLAUNCH(c, VLA_STACK_LLM, VLA_K_MLP_DOWN, vla::gemm_f32(a, F, (const float*)w.w_down, F, c->h, d, nullptr, 1, M, d, F, st));
   return OK;
 }
 
@@ -472,33 +536,33 @@ Status enc_block(vla_ctx* c, const Stack::Block& w, int n_img, int L) {
   hipStream_t st = c->compute;
   if (s.bf16()) {
     bf16_t* x = (bf16_t*)c->x;
-    KTRY(vla::layernorm_bf16(c->h, w.n1g, w.n1b, k.norm_eps, x, M, d, st));
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_NORM, vla::layernorm_bf16(c->h, w.n1g, w.n1b, k.norm_eps, x, M, d, st));
     vla::QkvArgs qa{w.b_qkv, nullptr, nullptr, (bf16_t*)c->q, (bf16_t*)c->ek, (bf16_t*)c->ev, (bf16_t*)c->vt,
                     round_up(L, 64), L, k.n_heads, k.n_kv_heads, k.head_dim};
-    KTRY(vla::gemm_bf16_qkv(x, d, (const bf16_t*)w.w_qkv, d, qa, M, s.qkv_n, d, st));
-    KTRY(vla::attention_bf16((const bf16_t*)c->q, (const bf16_t*)c->ek, (const bf16_t*)c->vt, round_up(L, 64),
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_QKV, vla::gemm_bf16_qkv(x, d, (const bf16_t*)w.w_qkv, d, qa, M, s.qkv_n, d, st));
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_ATTN, vla::attention_bf16((const bf16_t*)c->q, (const bf16_t*)c->ek, (const bf16_t*)c->vt, round_up(L, 64),
                              (bf16_t*)c->o, n_img, k.n_heads, k.n_kv_heads, L, k.head_dim, false, st));
-    KTRY(vla::gemm_bf16_residual((const bf16_t*)c->o, s.hd, (const bf16_t*)w.w_o, s.hd, c->h, d, w.b_o, M, d, s.hd,
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_OPROJ, vla::gemm_bf16_residual((const bf16_t*)c->o, s.hd, (const bf16_t*)w.w_o, s.hd, c->h, d, w.b_o, M, d, s.hd,
                                  st));
-    KTRY(vla::layernorm_bf16(c->h, w.n2g, w.n2b, k.norm_eps, x, M, d, st));
-    KTRY(vla::gemm_bf16_gelu(x, d, (const bf16_t*)w.w_up, d, (bf16_t*)c->act, s.f_pad, w.b_up, M, s.f_pad, d, st));
-    KTRY(vla::gemm_bf16_residual((const bf16_t*)c->act, s.f_pad, (const bf16_t*)w.w_down, s.f_pad, c->h, d, w.b_down,
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_NORM, vla::layernorm_bf16(c->h, w.n2g, w.n2b, k.norm_eps, x, M, d, st));
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_MLP_UP, vla::gemm_bf16_gelu(x, d, (const bf16_t*)w.w_up, d, (bf16_t*)c->act, s.f_pad, w.b_up, M, s.f_pad, d, st));
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_MLP_DOWN, vla::gemm_bf16_residual((const bf16_t*)c->act, s.f_pad, (const bf16_t*)w.w_down, s.f_pad, c->h, d, w.b_down,
                                  M, d, s.f_pad, st));
   } else {
     float* x = (float*)c->x;
     const int F = k.d_ff;
-    KTRY(vla::layernorm_f32(c->h, w.n1g, w.n1b, k.norm_eps, x, M, d, st));
-    KTRY(vla::gemm_f32(x, d, (const float*)w.w_qkv, d, c->qkv_raw, s.qkv_n, w.b_qkv, 0, M, s.qkv_n, d, st));
-    KTRY(vla::qkv_split_f32(c->qkv_raw, nullptr, nullptr, (float*)c->q, (float*)c->ek, (float*)c->ev, nullptr, 0,
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_NORM, vla::layernorm_f32(c->h, w.n1g, w.n1b, k.norm_eps, x, M, d, st));
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_QKV, vla::gemm_f32(x, d, (const float*)w.w_qkv, d, c->qkv_raw, s.qkv_n, w.b_qkv, 0, M, s.qkv_n, d, st));
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_QKV, vla::qkv_split_f32(c->qkv_raw, nullptr, nullptr, (float*)c->q, (float*)c->ek, (float*)c->ev, nullptr, 0,
                             n_img, L, k.n_heads, k.n_kv_heads, k.head_dim, st));
-    KTRY(vla::attention_f32((const float*)c->q, (const float*)c->ek, (const float*)c->ev, (float*)c->o, n_img,
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_ATTN, vla::attention_f32((const float*)c->q, (const float*)c->ek, (const float*)c->ev, (float*)c->o, n_img,
                             k.n_heads, k.n_kv_heads, L, k.head_dim, false, st));
-    KTRY(vla::gemm_f32((const float*)c->o, s.hd, (const float*)w.w_o, s.hd, c->h, d, w.b_o, 1, M, d, s.hd, st));
-    KTRY(vla::layernorm_f32(c->h, w.n2g, w.n2b, k.norm_eps, x, M, d, st));
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_OPROJ, vla::gemm_f32((const float*)c->o, s.hd, (const float*)w.w_o, s.hd, c->h, d, w.b_o, 1, M, d, s.hd, st));
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_NORM, vla::layernorm_f32(c->h, w.n2g, w.n2b, k.norm_eps, x, M, d, st));
     float* a = (float*)c->act;
-    KTRY(vla::gemm_f32(x, d, (const float*)w.w_up, d, a, F, w.b_up, 0, M, F, d, st));
-    KTRY(vla::gelu_f32(a, (size_t)M * F, st));
-    KTRY(vla::gemm_f32(a, F, (const float*)w.w_down, F, c->h, d, w.b_down, 1, M, d, F, st));
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_MLP_UP, vla::gemm_f32(x, d, (const float*)w.w_up, d, a, F, w.b_up, 0, M, F, d, st));
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_MLP_UP, vla::gelu_f32(a, (size_t)M * F, st));
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_MLP_DOWN, vla::gemm_f32(a, F, (const float*)w.w_down, F, c->h, d, w.b_down, 1, M, d, F, st));
   }
   return OK;
 }
@@ -516,12 +580,13 @@ Status retire_slot(vla_ctx* c, Slot& sl) {
   return OK;
 }
 
-Status run_blocks(vla_ctx* c, uint64_t frame_id, const void* tokens, int B, int L, int k0, int k1,
-                  vla_boundary* out) {
+Status run_blocks(vla_ctx* c, uint64_t frame_id, const void* tokens, vla_dtype in_dt, int B, int L, int k0,
+                  int k1, vla_boundary* out) {
   if (!c->llm.present) return fail(VLA_ERR_INVALID_ARG, "context has no decoder stack");
   const Stack& s = c->llm;
   if (!tokens || !out || !out->hidden) return fail(VLA_ERR_INVALID_ARG, "NULL tokens / boundary / hidden buffer");
   if (out->out_dtype != VLA_BF16 && out->out_dtype != VLA_F32) return fail(VLA_ERR_INVALID_ARG, "bad out_dtype");
+  if (in_dt != VLA_BF16 && in_dt != VLA_F32) return fail(VLA_ERR_INVALID_ARG, "bad in_dtype");
   if (k0 < 0 || k1 < k0) return fail(VLA_ERR_INVALID_ARG, "need 0 <= k_begin <= k_end (got %d, %d)", k0, k1);
   if (k1 > s.c.n_blocks) return fail(VLA_ERR_SHAPE, "k_end %d > resident blocks %d", k1, s.c.n_blocks);
   if (B <= 0 || L <= 0) return fail(VLA_ERR_SHAPE, "B and L must be positive");
@@ -553,7 +618,7 @@ Status run_blocks(vla_ctx* c, uint64_t frame_id, const void* tokens, int B, int 
   out->frame_id = frame_id;
 
   HIPTRY(hipEventRecord(sl.ev_start, c->compute));
-  if ((st = intake(c, s, tokens, n)).code) return st;
+  if ((st = intake(c, VLA_STACK_LLM, in_dt, tokens, n)).code) return st;
   for (int l = k0; l < k1; ++l) {
     const Stack::Block& w = s.blocks[l];
     char* kvl = (char*)sl.kv + (size_t)(l - k0) * layer_elems * s.esz;
@@ -577,7 +642,7 @@ Status run_blocks(vla_ctx* c, uint64_t frame_id, const void* tokens, int B, int 
     if (st.code) return st;
   }
   if (out->out_dtype == VLA_BF16)
-    KTRY(vla::f32_to_bf16(c->h, (bf16_t*)sl.hid, n, c->compute));
+    PLAUNCH(c, VLA_STACK_LLM, VLA_K_OTHER, vla::f32_to_bf16(c->h, (bf16_t*)sl.hid, n, c->compute));
   else
     HIPTRY(hipMemcpyAsync(sl.hid, c->h, n * 4, hipMemcpyDeviceToDevice, c->compute));
   HIPTRY(hipEventRecord(sl.ev_done, c->compute));
@@ -602,12 +667,12 @@ Status run_encoder(vla_ctx* c, const void* patches, int n_img, int L, void* out_
     if (!s.blocks[l].loaded) return fail(VLA_ERR_NOT_LOADED, "encoder block %d has no weights", l);
   if (!is_device(out_dev)) return fail(VLA_ERR_INVALID_ARG, "encoder output must be device memory");
   const size_t n = (size_t)n_img * L * s.c.d_model;
-  Status st = intake(c, s, patches, n);
+  Status st = intake(c, VLA_STACK_ENC, s.c.dtype, patches, n);
   if (st.code) return st;
   for (int l = 0; l < s.c.n_blocks; ++l)
     if ((st = enc_block(c, s.blocks[l], n_img, L)).code) return st;
   if (s.bf16())
-    KTRY(vla::f32_to_bf16(c->h, (bf16_t*)out_dev, n, c->compute));
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_OTHER, vla::f32_to_bf16(c->h, (bf16_t*)out_dev, n, c->compute));
   else
     HIPTRY(hipMemcpyAsync(out_dev, c->h, n * 4, hipMemcpyDeviceToDevice, c->compute));
   return OK;
@@ -701,6 +766,7 @@ void destroy(vla_ctx* c) {
     for (hipEvent_t e : sl.ev_kv)
       if (e) (void)hipEventDestroy(e);
   }
+  for (hipEvent_t e : c->prof_pool) (void)hipEventDestroy(e);
   if (c->own_compute) (void)hipStreamDestroy(c->compute);
   if (c->own_copy) (void)hipStreamDestroy(c->copy);
   delete c;
@@ -782,12 +848,12 @@ vla_status vla_run_encoder(vla_ctx* ctx, uint64_t frame_id, const void* patches,
   }
 }
 
-vla_status vla_run_blocks(vla_ctx* ctx, uint64_t frame_id, const void* tokens, int B, int L, int k_begin, int k_end,
-                          vla_boundary* out) {
+vla_status vla_run_blocks(vla_ctx* ctx, uint64_t frame_id, const void* tokens, vla_dtype in_dtype, int B, int L,
+                          int k_begin, int k_end, vla_boundary* out) {
   if (!ctx) return finish(nullptr, fail(VLA_ERR_INVALID_ARG, "NULL context"));
   try {
     if (hipSetDevice(ctx->device) != hipSuccess) return finish(ctx, fail(VLA_ERR_HIP, "hipSetDevice failed"));
-    return finish(ctx, run_blocks(ctx, frame_id, tokens, B, L, k_begin, k_end, out));
+    return finish(ctx, run_blocks(ctx, frame_id, tokens, in_dtype, B, L, k_begin, k_end, out));
   } catch (...) {
     return finish(ctx, fail(VLA_ERR_INVALID_ARG, "internal error"));
   }
@@ -795,7 +861,9 @@ vla_status vla_run_blocks(vla_ctx* ctx, uint64_t frame_id, const void* tokens, i
 
 vla_status vla_run_prefix(vla_ctx* ctx, uint64_t frame_id, const void* tokens, int B, int L, int k,
                           vla_boundary* out) {
-  return vla_run_blocks(ctx, frame_id, tokens, B, L, 0, k, out);
+  if (!ctx) return finish(nullptr, fail(VLA_ERR_INVALID_ARG, "NULL context"));
+  if (!ctx->llm.present) return finish(ctx, fail(VLA_ERR_INVALID_ARG, "context has no decoder stack"));
+  return vla_run_blocks(ctx, frame_id, tokens, ctx->llm.c.dtype, B, L, 0, k, out);
 }
 
 vla_status vla_wait_boundary(vla_ctx* ctx, uint64_t frame_id, int timeout_ms) {
@@ -834,6 +902,41 @@ vla_status vla_frame_times(vla_ctx* ctx, uint64_t frame_id, float* t_gpu_ms, flo
   if (t_xfer_ms) *t_xfer_ms = it->second.xfer;
   if (t_total_ms) *t_total_ms = it->second.total;
   return finish(ctx, OK);
+}
+
+vla_status vla_profile(vla_ctx* ctx, int enable) {
+  if (!ctx) return finish(nullptr, fail(VLA_ERR_INVALID_ARG, "NULL context"));
+  try {
+    if (hipSetDevice(ctx->device) != hipSuccess) return finish(ctx, fail(VLA_ERR_HIP, "hipSetDevice failed"));
+    if (enable) {
+      Status st = prof_drain(ctx);
+      if (st.code) return finish(ctx, st);
+      for (auto& row : ctx->prof_ms)
+        for (double& v : row) v = 0.0;
+      for (auto& row : ctx->prof_n)
+        for (int& v : row) v = 0;
+    }
+    ctx->prof_on = enable != 0;
+    return finish(ctx, OK);
+  } catch (...) {
+    return finish(ctx, fail(VLA_ERR_INVALID_ARG, "internal error"));
+  }
+}
+
+vla_status vla_profile_read(vla_ctx* ctx, vla_stack which, vla_kernel_class cls, double* ms_total, int* launches) {
+  if (!ctx) return finish(nullptr, fail(VLA_ERR_INVALID_ARG, "NULL context"));
+  if ((which != VLA_STACK_LLM && which != VLA_STACK_ENC) || cls < 0 || cls >= VLA_K_COUNT)
+    return finish(ctx, fail(VLA_ERR_INVALID_ARG, "bad stack or kernel class"));
+  try {
+    if (hipSetDevice(ctx->device) != hipSuccess) return finish(ctx, fail(VLA_ERR_HIP, "hipSetDevice failed"));
+    Status st = prof_drain(ctx);
+    if (st.code) return finish(ctx, st);
+    if (ms_total) *ms_total = ctx->prof_ms[which][cls];
+    if (launches) *launches = ctx->prof_n[which][cls];
+    return finish(ctx, OK);
+  } catch (...) {
+    return finish(ctx, fail(VLA_ERR_INVALID_ARG, "internal error"));
+  }
 }
 
 vla_status vla_arena_used(const vla_ctx* ctx, size_t* bytes) {

@@ -61,7 +61,8 @@ class LlmCase:
         src = tok
         if device_tokens:
             src = torch.from_numpy(tok.view(np.int16) if tok.dtype == np.uint16 else tok).cuda()
-        self.ctx.vla_run_blocks(frame, src, self.B, self.L, k0, k1, bnd)
+        in_dt = vb.VLA_BF16 if tok.dtype == np.uint16 else vb.VLA_F32
+        self.ctx.vla_run_blocks(frame, src, in_dt, self.B, self.L, k0, k1, bnd)
         self.ctx.vla_wait_boundary(frame, 120000)
         return bnd
 

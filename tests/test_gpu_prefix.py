@@ -123,6 +123,14 @@ def test_device_tokens_and_split_composition():
     b = c.run(a.hidden.numpy().copy(), frame=4, k0=2, k1=3, out_dtype="f32")
     assert np.array_equal(b.hidden.numpy(), full.hidden.numpy())
     assert np.array_equal(to_f32(b.kv[0]), to_f32(full.kv[2]))
+    # the bf16 handoff (b = 2 bytes, Eq. (11)) continued by the next stage
+    # matches the oracle continued from the same bf16 state
+    a16 = c.run(tok, frame=5, k0=0, k1=2)
+    import torch
+    h16 = a16.hidden.view(torch.int16).numpy().view(np.uint16).copy()
+    b16 = c.run(h16, frame=6, k0=2, k1=3, out_dtype="f32")
+    ref, _ = c.oracle(h16, k0=2, k1=3)
+    assert rel_l2(b16.hidden.numpy(), ref) <= 1e-2
     c.close()
 
 
@@ -144,8 +152,10 @@ def test_back_to_back_frames_and_determinism():
         assert rel_l2(to_f32(bnds[f].hidden), ref) <= 1e-2
         assert rel_l2(to_f32(bnds[f].kv), kv) <= 1e-2
     again = c.run(toks[2], frame=200)
-    assert np.array_equal(again.hidden.numpy(), bnds[2].hidden.numpy())
-    assert np.array_equal(again.kv.numpy(), bnds[2].kv.numpy())
+    import torch
+    bits = lambda t: t.view(torch.int16).numpy()
+    assert np.array_equal(bits(again.hidden), bits(bnds[2].hidden))
+    assert np.array_equal(bits(again.kv), bits(bnds[2].kv))
     c.close()
 
 
