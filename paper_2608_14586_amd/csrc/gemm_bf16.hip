@@ -5,12 +5,9 @@
 // exactly the register layout v_mfma_f32_32x32x16_bf16 wants for both of its
 // inputs: lane l holds 8 consecutive k of row (l % 32) in k-block (l / 32).
 //
-// Workgroup: 256 threads = 4 waves over a BM x BN tile; each wave owns a
-// WM x WN sub-tile of (WM/32) x (WN/32) MFMA 32x32 accumulators.  K advances
-// in BK = 64 slabs staged in LDS, double buffered: the next slab's global
-// loads are issued before the current slab's MFMAs and land in the other LDS
-// buffer afterwards, so one barrier per slab suffices.  LDS rows are padded
-// by 16 bytes to spread the 16-byte fragment reads of 32 rows over the banks.
+// Workgroup: NW waves over a BM x BN tile; each wave owns a WM x WN sub-tile
+// of (WM/32) x (WN/32) MFMA 32x32 accumulators.  K advances in BK = 64 slabs
+// moved global -> LDS by buffer_load ... lds (see the main loop below).
 //
 // Tile order: workgroup ids are first remapped so that each of the 8 XCDs
 // (which take ids round-robin) receives a contiguous range of tiles, then
@@ -26,7 +23,6 @@ namespace vla {
 namespace {
 
 constexpr int BK = 64;
-constexpr int LDS_PAD = 8;  // bf16 elements of padding per LDS row
 constexpr int GROUP_M = 8;
 
 template <int TM, int TN>
@@ -243,27 +239,35 @@ struct EpiQKV {
   }
 };
 
-// --------------------------------------------------------------------- kernel
+// ---------------------------------------------------------------- main loop
+//
+// The K slabs move global -> LDS with buffer_load ... lds (16 bytes per lane, written at M0 + 16 * lane), so no
+// VGPRs or ds_write instructions are spent on staging and the next slab's
+// loads run fully asynchronously behind the current slab's MFMAs.  LDS rows
+// are 128 bytes (BK = 64 bf16) with the 16-byte chunks XOR-swizzled by
+// ((row >> 1) & 7): each 16-lane phase of a fragment read covers all banks.
+// Buffer resources clamp ragged M / N tiles: rows past the end read as zero.
+// MFMA fragments are double buffered across the four k16 steps of a slab.
 
-template <int BM, int BN, int WM, int WN, class Epi>
-__global__ __launch_bounds__(256) void gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda,
-                                                        const bf16_t* __restrict__ W, int ldw, int M, int N, int K,
-                                                        Epi epi) {
+__device__ __forceinline__ void buffer_load_lds16(__amdgpu_buffer_rsrc_t r, void* lds, unsigned voff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, voff, 0, 0, 0);
+}
+
+template <int BM, int BN, int WM, int WN, int NW, class Epi>
+__global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __restrict__ A, int lda,
+                                                                const bf16_t* __restrict__ W, int ldw, int M, int N,
+                                                                int K, Epi epi) {
   constexpr int TM = WM / 32, TN = WN / 32;
   constexpr int WAVES_N = BN / WN;
-  static_assert((BM / WM) * (BN / WN) == 4, "4 waves per workgroup");
-  constexpr int LDR = BK + LDS_PAD;                 // LDS row stride (elements)
-  constexpr int A_CHUNKS = BM * BK / 8 / 256;       // 16-byte chunks per thread
-  constexpr int B_CHUNKS = BN * BK / 8 / 256;
-  static_assert(A_CHUNKS >= 1 && B_CHUNKS >= 1, "tile too small");
-
-  __shared__ __attribute__((aligned(16))) bf16_t sA[2][BM * LDR];
-  __shared__ __attribute__((aligned(16))) bf16_t sB[2][BN * LDR];
+  static_assert((BM / WM) * (BN / WN) == NW, "wave grid must cover the tile");
+  constexpr int ROWB = BK * 2;                             // bytes per LDS row (128)
+  constexpr int A_INST = BM / (8 * NW), B_INST = BN / (8 * NW);  // 1 KB loads per wave per slab
+  static_assert(A_INST >= 1 && B_INST >= 1, "tile too small for the wave count");
+  __shared__ __attribute__((aligned(1024))) char smem[2 * (BM + BN) * ROWB];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;
 
-  // tile scheduling: XCD-contiguous ranges, then grouped M-fastest order
   const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
   const int nwg = gridDim.x;
   int id = blockIdx.x;
@@ -275,41 +279,28 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(const bf16_t* __restrict
   const int tile_n = (id % group) / gsz;
   const int m0 = tile_m * BM, n0 = tile_n * BN;
 
-  u32x4 ra[A_CHUNKS], rb[B_CHUNKS];
-  auto gload = [&](int k0) {
+  // buffer resources over the tile's rows; rows past M / N read as zero
+  const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(A + (size_t)m0 * lda), (short)0, (int)((size_t)(M - m0) * lda * 2), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(W + (size_t)n0 * ldw), (short)0, (int)((size_t)(N - n0) * ldw * 2), 0x00020000);
+
+  // this lane's slot in each 1 KB load: row (lane / 8) of the 8-row group,
+  // LDS chunk (lane % 8) holding global chunk (lane % 8) ^ key(tile row)
+  const int lrow = lane >> 3, lslot = lane & 7;
+  auto issue = [&](int k0, int buf) {
+    char* base = smem + buf * (BM + BN) * ROWB;
 #pragma unroll
-    for (int c = 0; c < A_CHUNKS; ++c) {
-      int idx = tid + c * 256;
-      int row = idx / (BK / 8), kc = idx % (BK / 8);
-      int gr = m0 + row;
-      if (gr < M)
-        ra[c] = *(const u32x4*)(A + (size_t)gr * lda + k0 + kc * 8);
-      else
-        ra[c] = u32x4{0, 0, 0, 0};
+    for (int j = 0; j < A_INST; ++j) {
+      const int row = (wave * A_INST + j) * 8 + lrow;
+      const int ch = lslot ^ ((row >> 1) & 7);
+      buffer_load_lds16(ra, base + (wave * A_INST + j) * 1024, (unsigned)((row * lda + k0 + ch * 8) * 2));
     }
 #pragma unroll
-    for (int c = 0; c < B_CHUNKS; ++c) {
-      int idx = tid + c * 256;
-      int row = idx / (BK / 8), kc = idx % (BK / 8);
-      int gr = n0 + row;
-      if (gr < N)
-        rb[c] = *(const u32x4*)(W + (size_t)gr * ldw + k0 + kc * 8);
-      else
-        rb[c] = u32x4{0, 0, 0, 0};
-    }
-  };
-  auto lstore = [&](int buf) {
-#pragma unroll
-    for (int c = 0; c < A_CHUNKS; ++c) {
-      int idx = tid + c * 256;
-      int row = idx / (BK / 8), kc = idx % (BK / 8);
-      *(u32x4*)(&sA[buf][row * LDR + kc * 8]) = ra[c];
-    }
-#pragma unroll
-    for (int c = 0; c < B_CHUNKS; ++c) {
-      int idx = tid + c * 256;
-      int row = idx / (BK / 8), kc = idx % (BK / 8);
-      *(u32x4*)(&sB[buf][row * LDR + kc * 8]) = rb[c];
+    for (int j = 0; j < B_INST; ++j) {
+      const int row = (wave * B_INST + j) * 8 + lrow;
+      const int ch = lslot ^ ((row >> 1) & 7);
+      buffer_load_lds16(rb, base + BM * ROWB + (wave * B_INST + j) * 1024, (unsigned)((row * ldw + k0 + ch * 8) * 2));
     }
   };
 
@@ -321,32 +312,40 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(const bf16_t* __restrict
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc.v[tm][tn][r] = 0.f;
 
-  const int nk = K / BK;
-  gload(0);
-  lstore(0);
-  __syncthreads();
+  const int fi = lane & 31, fh = lane >> 5;
+  const int a_row0 = (wm * WM + fi) * ROWB, b_row0 = BM * ROWB + (wn * WN + fi) * ROWB;
+  const int key = (fi >> 1) & 7;
+  bf16x8 fa[2][TM], fb[2][TN];
+  auto frags = [&](int buf, int ks, int slot) {
+    const char* base = smem + buf * (BM + BN) * ROWB;
+    const int off = (((2 * ks + fh) ^ key) << 4);
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm) fa[slot][tm] = *(const bf16x8*)(base + a_row0 + tm * 32 * ROWB + off);
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) fb[slot][tn] = *(const bf16x8*)(base + b_row0 + tn * 32 * ROWB + off);
+  };
 
-  const int frow = lane & 31, fk = (lane >> 5) * 8;
+  const int nk = K / BK;
+  issue(0, 0);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  frags(0, 0, 0);
   for (int kt = 0; kt < nk; ++kt) {
     const int buf = kt & 1;
-    if (kt + 1 < nk) gload((kt + 1) * BK);
-    const bf16_t* a_base = &sA[buf][(wm * WM + frow) * LDR + fk];
-    const bf16_t* b_base = &sB[buf][(wn * WN + frow) * LDR + fk];
+    if (kt + 1 < nk) issue((kt + 1) * BK, buf ^ 1);
 #pragma unroll
     for (int ks = 0; ks < BK / 16; ++ks) {
-      bf16x8 fa[TM], fb[TN];
-#pragma unroll
-      for (int tm = 0; tm < TM; ++tm) fa[tm] = *(const bf16x8*)(a_base + tm * 32 * LDR + ks * 16);
-#pragma unroll
-      for (int tn = 0; tn < TN; ++tn) fb[tn] = *(const bf16x8*)(b_base + tn * 32 * LDR + ks * 16);
+      const int cur = ks & 1;
+      if (ks + 1 < BK / 16) frags(buf, ks + 1, cur ^ 1);
 #pragma unroll
       for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
         for (int tn = 0; tn < TN; ++tn)
-          acc.v[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[tm], fb[tn], acc.v[tm][tn], 0, 0, 0);
+          acc.v[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cur][tm], fb[cur][tn], acc.v[tm][tn], 0, 0, 0);
     }
-    if (kt + 1 < nk) lstore(buf ^ 1);
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
+    if (kt + 1 < nk) frags(buf ^ 1, 0, 0);
   }
 
   epi(acc, m0 + wm * WM, n0 + wn * WN, lane);
@@ -357,10 +356,20 @@ hipError_t launch(const bf16_t* A, int lda, const bf16_t* W, int ldw, int M, int
                   hipStream_t s) {
   if (M <= 0 || N <= 0) return hipSuccess;
   if (K % BK != 0 || lda % 8 != 0 || ldw % 8 != 0) return hipErrorInvalidValue;
-  constexpr int BM = 128, BN = 128;
-  int grid = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, 64, 64, Epi>), dim3(grid), dim3(256), 0, s, A, lda, W, ldw, M, N, K,
-                     epi);
+  // byte offsets inside a tile's buffer resource are 32-bit
+  if ((size_t)256 * lda * 2 >= (1u << 31) || (size_t)256 * ldw * 2 >= (1u << 31)) return hipErrorInvalidValue;
+  // 256x256 tiles (8 waves of 128x64) once they fill the chip at least twice;
+  // otherwise 128x128 tiles (4 waves of 64x64, two workgroups per CU)
+  const long tiles256 = (long)((M + 255) / 256) * ((N + 255) / 256);
+  if (tiles256 >= 512) {
+    int grid = ((M + 255) / 256) * ((N + 255) / 256);
+    hipLaunchKernelGGL((gemm_bf16_dma_kernel<256, 256, 128, 64, 8, Epi>), dim3(grid), dim3(512), 0, s, A, lda, W,
+                       ldw, M, N, K, epi);
+  } else {
+    int grid = ((M + 127) / 128) * ((N + 127) / 128);
+    hipLaunchKernelGGL((gemm_bf16_dma_kernel<128, 128, 64, 64, 4, Epi>), dim3(grid), dim3(256), 0, s, A, lda, W, ldw,
+                       M, N, K, epi);
+  }
   return hipGetLastError();
 }
 

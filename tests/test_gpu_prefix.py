@@ -29,7 +29,7 @@ def test_tiny_fp32_debug_path(perturbed):
 
 
 @pytest.mark.parametrize("name,L,k,B", [("small_llm", 300, 2, 1), ("small_llm", 128, 3, 2), ("llm7b", 256, 2, 1),
-                                        ("llm7b", 200, 1, 1)])
+                                        ("llm7b", 200, 1, 1), ("llm7b", 2048, 1, 1)])
 def test_bf16_prefix_reduced(name, L, k, B):
     c = LlmCase(name, L, k, B=B, perturbed=True)
     tok = c.tokens(frame=1)
