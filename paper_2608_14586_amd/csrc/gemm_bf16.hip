@@ -33,8 +33,43 @@ struct Acc {
 __device__ __forceinline__ int acc_row(int r, int lane) { return (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3); }
 
 // ------------------------------------------------------------------ epilogues
+//
+// Two epilogue paths.
+//  * Direct: every lane writes its accumulators straight to memory (2- or
+//    4-byte stores); used by the 256x256 tiles and the fp32-out operator.
+//  * Through LDS (128 x 128 tiles): once the K loop is done the 64 KB of slab
+//    buffers are free, so the waves park the fp32 tile in LDS row-major and
+//    the whole workgroup then walks it in 16-byte chunks: coalesced residual
+//    read-modify-writes, 16-byte bf16 stores, and the rotary embedding plus
+//    the q / K / V / V^T scatter done row-contiguously per head.
+// drain() is the second half of the LDS path: T is the tile [128][128] fp32,
+// (m0, n0) its origin, tid the thread index in the 256-thread workgroup.
+
+constexpr int ET = 128;  // LDS-epilogue tile edge
+
+__device__ __forceinline__ u32x4 pack8(const f32x4& a, const f32x4& b) {
+  return u32x4{pack_bf2(a[0], a[1]), pack_bf2(a[2], a[3]), pack_bf2(b[0], b[1]), pack_bf2(b[2], b[3])};
+}
+
+__device__ __forceinline__ f32x4 ld4(const float* p) { return *(const f32x4*)p; }
+
+// Exact GELU z * Phi(z) with Phi(z) = erfc(-z / sqrt 2) / 2, erfc from the
+// rational approximation of Abramowitz & Stegun 7.1.26 (|error| <= 1.5e-7,
+// far below bf16 resolution); erfc of |x| is formed directly, so the negative
+// tail does not cancel.
+__device__ __forceinline__ float gelu_as(float z) {
+  const float x = fabsf(z) * 0.70710678118654752f;
+  const float t = 1.f / (1.f + 0.3275911f * x);
+  const float poly = t * (0.254829592f + t * (-0.284496736f + t * (1.421413741f + t * (-1.453152027f + t * 1.061405429f))));
+  const float ec = poly * __expf(-x * x);  // erfc(x), x >= 0
+  const float phi = z >= 0.f ? 1.f - 0.5f * ec : 0.5f * ec;
+  return z * phi;
+}
+
+__device__ __forceinline__ float silu(float g) { return g / (1.f + __expf(-g)); }
 
 struct EpiStoreF32 {
+  static constexpr bool kViaLds = false, kBig = true;
   float* C;
   int ldc, M, N;
   template <int TM, int TN>
@@ -52,12 +87,17 @@ struct EpiStoreF32 {
         }
       }
   }
+  __device__ void drain(const float*, int, int, int) const {}
 };
 
-struct EpiStoreBF16 {
+// C (bf16) = acc + bias, or gelu(acc + bias) when GELU.
+template <bool GELU>
+struct EpiBF16 {
+  static constexpr bool kViaLds = true, kBig = true;
   bf16_t* C;
   const float* bias;
   int ldc, M, N;
+  __device__ __forceinline__ float op(float z) const { return GELU ? gelu_as(z) : z; }
   template <int TM, int TN>
   __device__ void operator()(const Acc<TM, TN>& a, int row0, int col0, int lane) const {
 #pragma unroll
@@ -70,13 +110,38 @@ struct EpiStoreBF16 {
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           int row = row0 + tm * 32 + acc_row(r, lane);
-          if (row < M) C[(size_t)row * ldc + col] = f2bf(a.v[tm][tn][r] + b);
+          if (row < M) C[(size_t)row * ldc + col] = f2bf(op(a.v[tm][tn][r] + b));
         }
       }
   }
+  __device__ void drain(const float* T, int m0, int n0, int tid) const {
+    // 128 rows x 16 chunks of 8 columns
+#pragma unroll 4
+    for (int j = 0; j < ET * 16 / 256; ++j) {
+      const int f = tid + 256 * j, row = f >> 4, c8 = (f & 15) * 8;
+      const int gr = m0 + row, gc = n0 + c8;
+      if (gr >= M || gc >= N) continue;
+      f32x4 x0 = ld4(T + row * ET + c8), x1 = ld4(T + row * ET + c8 + 4);
+      if (bias) {
+        f32x4 b0 = ld4(bias + gc), b1 = ld4(bias + gc + 4);
+        x0 += b0;
+        x1 += b1;
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        x0[e] = op(x0[e]);
+        x1[e] = op(x1[e]);
+      }
+      *(u32x4*)(C + (size_t)gr * ldc + gc) = pack8(x0, x1);
+    }
+  }
 };
+using EpiStoreBF16 = EpiBF16<false>;
+using EpiGelu = EpiBF16<true>;
 
+// H (fp32 residual) += acc + bias.
 struct EpiResidual {
+  static constexpr bool kViaLds = true, kBig = false;
   float* H;
   const float* bias;
   int ldh, M, N;
@@ -99,37 +164,31 @@ struct EpiResidual {
         }
       }
   }
-};
-
-struct EpiGelu {
-  bf16_t* out;
-  const float* bias;
-  int ldo, M, N;
-  template <int TM, int TN>
-  __device__ void operator()(const Acc<TM, TN>& a, int row0, int col0, int lane) const {
+  __device__ void drain(const float* T, int m0, int n0, int tid) const {
+    // 128 rows x 32 float4; all residual loads of a thread issued first
+    constexpr int NJ = ET * 32 / 256;
+    f32x4 hv[NJ];
 #pragma unroll
-    for (int tm = 0; tm < TM; ++tm)
+    for (int j = 0; j < NJ; ++j) {
+      const int f = tid + 256 * j, row = f >> 5, c4 = (f & 31) * 4;
+      const int gr = m0 + row, gc = n0 + c4;
+      hv[j] = (gr < M && gc < N) ? ld4(H + (size_t)gr * ldh + gc) : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
 #pragma unroll
-      for (int tn = 0; tn < TN; ++tn) {
-        int col = col0 + tn * 32 + (lane & 31);
-        if (col >= N) continue;
-        float b = bias ? bias[col] : 0.f;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          int row = row0 + tm * 32 + acc_row(r, lane);
-          if (row < M) {
-            float z = a.v[tm][tn][r] + b;
-            // exact GELU: z * Phi(z), Phi(z) = 0.5 * erfc(-z / sqrt(2))
-            float y = z * 0.5f * erfcf(-z * 0.70710678118654752f);
-            out[(size_t)row * ldo + col] = f2bf(y);
-          }
-        }
-      }
+    for (int j = 0; j < NJ; ++j) {
+      const int f = tid + 256 * j, row = f >> 5, c4 = (f & 31) * 4;
+      const int gr = m0 + row, gc = n0 + c4;
+      if (gr >= M || gc >= N) continue;
+      f32x4 x = ld4(T + row * ET + c4);
+      if (bias) x += ld4(bias + gc);
+      *(f32x4*)(H + (size_t)gr * ldh + gc) = hv[j] + x;
+    }
   }
 };
 
-// Pairs accumulator tiles (2p, 2p+1) = (gate, up) of the same 32 features.
+// Pairs tiles (2p, 2p+1) = (gate, up) of the same 32 features: out[M][N/2].
 struct EpiSwiGLU {
+  static constexpr bool kViaLds = true, kBig = true;
   bf16_t* out;
   int ldo, M, N;
   template <int TM, int TN>
@@ -145,92 +204,115 @@ struct EpiSwiGLU {
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           int row = row0 + tm * 32 + acc_row(r, lane);
-          if (row < M) {
-            float g = a.v[tm][2 * tp][r], u = a.v[tm][2 * tp + 1][r];
-            float s = g / (1.f + __expf(-g));
-            out[(size_t)row * ldo + f] = f2bf(s * u);
-          }
+          if (row < M) out[(size_t)row * ldo + f] = f2bf(silu(a.v[tm][2 * tp][r]) * a.v[tm][2 * tp + 1][r]);
         }
       }
   }
+  __device__ void drain(const float* T, int m0, int n0, int tid) const {
+    // 128 rows x 8 chunks of 8 output features
+#pragma unroll
+    for (int j = 0; j < ET * 8 / 256; ++j) {
+      const int f = tid + 256 * j, row = f >> 3, c = f & 7;
+      const int gsel = c >> 2, w = (c & 3) * 8;           // 64-column group, offset inside its 32
+      const int gr = m0 + row;
+      if (gr >= M || n0 + gsel * 64 >= N) continue;
+      const float* tr = T + row * ET + gsel * 64 + w;
+      f32x4 g0 = ld4(tr), g1 = ld4(tr + 4), u0 = ld4(tr + 32), u1 = ld4(tr + 36);
+      f32x4 y0, y1;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        y0[e] = silu(g0[e]) * u0[e];
+        y1[e] = silu(g1[e]) * u1[e];
+      }
+      *(u32x4*)(out + (size_t)gr * ldo + (n0 >> 1) + gsel * 32 + w) = pack8(y0, y1);
+    }
+  }
 };
 
+// QKV projection: bias, rotary embedding of q and k (each 64-column group
+// holds 32 first-half dims and their 32 second-half partners, see QkvArgs),
+// scatter to q / K / V rows and to V^T.
 struct EpiQKV {
+  static constexpr bool kViaLds = true, kBig = false;
   QkvArgs q;
   int M;
+  // column group p (multiple of 64) -> kind (0 q, 1 k, 2 v, 3 none), head, dim offset
+  __device__ __forceinline__ void classify(int p, int& kind, int& head, int& r) const {
+    const int dh = q.dh;
+    if (p < q.H * dh) {
+      kind = 0; head = p / dh; r = p % dh;
+    } else if (p < (q.H + q.Hkv) * dh) {
+      kind = 1; head = (p - q.H * dh) / dh; r = (p - q.H * dh) % dh;
+    } else if (p < (q.H + 2 * q.Hkv) * dh) {
+      kind = 2; head = (p - (q.H + q.Hkv) * dh) / dh; r = (p - (q.H + q.Hkv) * dh) % dh;
+    } else {
+      kind = 3; head = 0; r = 0;
+    }
+  }
   template <int TM, int TN>
-  __device__ void operator()(const Acc<TM, TN>& a, int row0, int col0, int lane) const {
-    static_assert(TN % 2 == 0, "qkv pairs tiles");
+  __device__ void operator()(const Acc<TM, TN>&, int, int, int) const {}  // LDS path only
+  __device__ void drain(const float* T, int m0, int n0, int tid) const {
     const int dh = q.dh, L = q.L;
-    const int i = lane & 31;
-#pragma unroll
-    for (int tp = 0; tp < TN / 2; ++tp) {
-      const int p = col0 + tp * 64;  // packed column of this 64-wide group
+    // rows: 128 tokens x 2 column groups x 4 chunks of 8 dims
+#pragma unroll 2
+    for (int j = 0; j < ET * 8 / 256; ++j) {
+      const int f = tid + 256 * j, row = f >> 3, gsel = (f >> 2) & 1, w = (f & 3) * 8;
+      const int gr = m0 + row, p = n0 + gsel * 64;
       int kind, head, r;
-      if (p < q.H * dh) {
-        kind = 0; head = p / dh; r = p % dh;
-      } else if (p < (q.H + q.Hkv) * dh) {
-        kind = 1; head = (p - q.H * dh) / dh; r = (p - q.H * dh) % dh;
-      } else if (p < (q.H + 2 * q.Hkv) * dh) {
-        kind = 2; head = (p - (q.H + q.Hkv) * dh) / dh; r = (p - (q.H + q.Hkv) * dh) % dh;
-      } else {
-        continue;
-      }
+      classify(p, kind, head, r);
+      if (gr >= M || kind == 3) continue;
       const int c = r / 64;
-      const int d1 = c * 32 + i, d2 = dh / 2 + c * 32 + i;
-      const float b1 = q.bias ? q.bias[p + i] : 0.f;
-      const float b2 = q.bias ? q.bias[p + 32 + i] : 0.f;
-      const bool rot = (kind < 2) && q.rope_cos != nullptr;
+      const int d1 = c * 32 + w, d2 = dh / 2 + c * 32 + w;
+      const float* tr = T + row * ET + gsel * 64 + w;
+      f32x4 x10 = ld4(tr), x11 = ld4(tr + 4), x20 = ld4(tr + 32), x21 = ld4(tr + 36);
+      if (q.bias) {
+        x10 += ld4(q.bias + p + w);
+        x11 += ld4(q.bias + p + w + 4);
+        x20 += ld4(q.bias + p + 32 + w);
+        x21 += ld4(q.bias + p + 36 + w);
+      }
+      const int b = gr / L, pos = gr - b * L;
+      if (kind < 2 && q.rope_cos) {
+        const float* cp = q.rope_cos + (size_t)pos * (dh / 2) + d1;
+        const float* sp = q.rope_sin + (size_t)pos * (dh / 2) + d1;
+        const f32x4 c0 = ld4(cp), c1 = ld4(cp + 4), s0 = ld4(sp), s1 = ld4(sp + 4);
+        const f32x4 y10 = x10 * c0 - x20 * s0, y11 = x11 * c1 - x21 * s1;
+        const f32x4 y20 = x20 * c0 + x10 * s0, y21 = x21 * c1 + x11 * s1;
+        x10 = y10; x11 = y11; x20 = y20; x21 = y21;
+      }
       const int nh = kind == 0 ? q.H : q.Hkv;
-      bf16_t* dst = kind == 0 ? q.q : (kind == 1 ? q.k : q.v);
+      bf16_t* dst = (kind == 0 ? q.q : (kind == 1 ? q.k : q.v)) + (((size_t)b * nh + head) * L + pos) * dh;
+      *(u32x4*)(dst + d1) = pack8(x10, x11);
+      *(u32x4*)(dst + d2) = pack8(x20, x21);
+    }
+    // V^T: one (dim, 8 consecutive tokens) chunk per item
+    for (int gsel = 0; gsel < 2; ++gsel) {
+      int kind, head, r;
+      const int p = n0 + gsel * 64;
+      classify(p, kind, head, r);
+      if (kind != 2) continue;
+      const int c = r / 64;
+#pragma unroll 2
+      for (int j = 0; j < 64 * 16 / 256; ++j) {
+        const int f = tid + 256 * j, col = f & 63, t8 = (f >> 6) * 8;
+        const int gr0 = m0 + t8;
+        if (gr0 >= M) continue;
+        const int d = (col < 32) ? c * 32 + col : dh / 2 + c * 32 + (col - 32);
+        const float bcol = q.bias ? q.bias[p + col] : 0.f;
+        float v[8];
 #pragma unroll
-      for (int tm = 0; tm < TM; ++tm) {
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          float y1[4], y2[4];
-          int rowb = row0 + tm * 32 + g * 8 + (lane >> 5) * 4;
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            float x1 = a.v[tm][2 * tp][g * 4 + j] + b1;
-            float x2 = a.v[tm][2 * tp + 1][g * 4 + j] + b2;
-            int row = rowb + j;
-            if (rot && row < M) {
-              int pos = row % L;
-              float cs = q.rope_cos[(size_t)pos * (dh / 2) + d1];
-              float sn = q.rope_sin[(size_t)pos * (dh / 2) + d1];
-              y1[j] = x1 * cs - x2 * sn;
-              y2[j] = x2 * cs + x1 * sn;
-            } else {
-              y1[j] = x1;
-              y2[j] = x2;
-            }
-            if (row < M) {
-              int b = row / L, pos = row % L;
-              size_t base = (((size_t)b * nh + head) * L + pos) * dh;
-              dst[base + d1] = f2bf(y1[j]);
-              dst[base + d2] = f2bf(y2[j]);
-            }
-          }
-          if (kind == 2) {
-            // V transposed: 4 consecutive positions of one dim per lane
-            int b0 = rowb / L, pos0 = rowb % L;
-            bool fast = (rowb + 3 < M) && (pos0 + 3 < L) && ((pos0 & 3) == 0) && ((q.ldvt & 3) == 0);
-            if (fast) {
-              size_t o1 = (((size_t)b0 * q.Hkv + head) * dh + d1) * q.ldvt + pos0;
-              size_t o2 = (((size_t)b0 * q.Hkv + head) * dh + d2) * q.ldvt + pos0;
-              u32x2 w1 = {pack_bf2(y1[0], y1[1]), pack_bf2(y1[2], y1[3])};
-              u32x2 w2 = {pack_bf2(y2[0], y2[1]), pack_bf2(y2[2], y2[3])};
-              *(u32x2*)(q.vt + o1) = w1;
-              *(u32x2*)(q.vt + o2) = w2;
-            } else {
-#pragma unroll
-              for (int j = 0; j < 4; ++j) {
-                int row = rowb + j;
-                if (row >= M) continue;
-                int b = row / L, pos = row % L;
-                q.vt[(((size_t)b * q.Hkv + head) * dh + d1) * q.ldvt + pos] = f2bf(y1[j]);
-                q.vt[(((size_t)b * q.Hkv + head) * dh + d2) * q.ldvt + pos] = f2bf(y2[j]);
-              }
+        for (int e = 0; e < 8; ++e) v[e] = T[(t8 + e) * ET + gsel * 64 + col] + bcol;
+        const int b0 = gr0 / L, pos0 = gr0 - b0 * L;
+        if (gr0 + 7 < M && pos0 + 7 < L && (pos0 & 7) == 0 && (q.ldvt & 7) == 0) {
+          u32x4 w4 = {pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]), pack_bf2(v[4], v[5]), pack_bf2(v[6], v[7])};
+          *(u32x4*)(q.vt + (((size_t)b0 * q.Hkv + head) * dh + d) * q.ldvt + pos0) = w4;
+        } else {
+          int bb = b0, pp = pos0;
+          for (int e = 0; e < 8 && gr0 + e < M; ++e) {
+            q.vt[(((size_t)bb * q.Hkv + head) * dh + d) * q.ldvt + pp] = f2bf(v[e]);
+            if (++pp == L) {
+              pp = 0;
+              ++bb;
             }
           }
         }
@@ -332,7 +414,8 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __
   frags(0, 0, 0);
   for (int kt = 0; kt < nk; ++kt) {
     const int buf = kt & 1;
-    if (kt + 1 < nk) issue((kt + 1) * BK, buf ^ 1);
+    const bool last = kt + 1 == nk;
+    if (!last) issue((kt + 1) * BK, buf ^ 1);
 #pragma unroll
     for (int ks = 0; ks < BK / 16; ++ks) {
       const int cur = ks & 1;
@@ -343,12 +426,30 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __
         for (int tn = 0; tn < TN; ++tn)
           acc.v[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cur][tm], fb[cur][tn], acc.v[tm][tn], 0, 0, 0);
     }
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    if (kt + 1 < nk) frags(buf ^ 1, 0, 0);
+    if (!last) {
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+      frags(buf ^ 1, 0, 0);
+    }
   }
 
-  epi(acc, m0 + wm * WM, n0 + wn * WN, lane);
+  if constexpr (Epi::kViaLds && BM == ET && BN == ET && NW == 4) {
+    // park the fp32 tile in the (now idle) slab buffers, then drain it
+    static_assert(ET * ET * 4 <= sizeof(smem), "tile must fit the slab buffers");
+    float* T = (float*)smem;
+    __syncthreads();
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          T[(wm * WM + tm * 32 + acc_row(r, lane)) * ET + wn * WN + tn * 32 + (lane & 31)] = acc.v[tm][tn][r];
+    __syncthreads();
+    epi.drain(T, m0, n0, tid);
+  } else {
+    epi(acc, m0 + wm * WM, n0 + wn * WN, lane);
+  }
 }
 
 template <class Epi>
@@ -361,11 +462,16 @@ hipError_t launch(const bf16_t* A, int lda, const bf16_t* W, int ldw, int M, int
   // 256x256 tiles (8 waves of 128x64) once they fill the chip at least twice;
   // otherwise 128x128 tiles (4 waves of 64x64, two workgroups per CU)
   const long tiles256 = (long)((M + 255) / 256) * ((N + 255) / 256);
-  if (tiles256 >= 512) {
-    int grid = ((M + 255) / 256) * ((N + 255) / 256);
-    hipLaunchKernelGGL((gemm_bf16_dma_kernel<256, 256, 128, 64, 8, Epi>), dim3(grid), dim3(512), 0, s, A, lda, W,
-                       ldw, M, N, K, epi);
-  } else {
+  bool big = false;
+  if constexpr (Epi::kBig) {
+    if (tiles256 >= 512) {
+      big = true;
+      int grid = ((M + 255) / 256) * ((N + 255) / 256);
+      hipLaunchKernelGGL((gemm_bf16_dma_kernel<256, 256, 128, 64, 8, Epi>), dim3(grid), dim3(512), 0, s, A, lda, W,
+                         ldw, M, N, K, epi);
+    }
+  }
+  if (!big) {
     int grid = ((M + 127) / 128) * ((N + 127) / 128);
     hipLaunchKernelGGL((gemm_bf16_dma_kernel<128, 128, 64, 64, 4, Epi>), dim3(grid), dim3(256), 0, s, A, lda, W, ldw,
                        M, N, K, epi);
@@ -382,22 +488,26 @@ hipError_t gemm_bf16_store_f32(const bf16_t* A, int lda, const bf16_t* W, int ld
 
 hipError_t gemm_bf16_store_bf16(const bf16_t* A, int lda, const bf16_t* W, int ldw, bf16_t* C, int ldc,
                                 const float* bias, int M, int N, int K, hipStream_t s) {
+  if (N % 8 || ldc % 8) return hipErrorInvalidValue;
   return launch(A, lda, W, ldw, M, N, K, EpiStoreBF16{C, bias, ldc, M, N}, s);
 }
 
 hipError_t gemm_bf16_residual(const bf16_t* A, int lda, const bf16_t* W, int ldw, float* H, int ldh,
                               const float* bias, int M, int N, int K, hipStream_t s) {
+  if (N % 4 || ldh % 4) return hipErrorInvalidValue;
   return launch(A, lda, W, ldw, M, N, K, EpiResidual{H, bias, ldh, M, N}, s);
 }
 
 hipError_t gemm_bf16_swiglu(const bf16_t* A, int lda, const bf16_t* W, int ldw, bf16_t* out, int ldo, int M, int N,
                             int K, hipStream_t s) {
   if (N % 64 != 0) return hipErrorInvalidValue;
+  if (ldo % 8) return hipErrorInvalidValue;
   return launch(A, lda, W, ldw, M, N, K, EpiSwiGLU{out, ldo, M, N}, s);
 }
 
 hipError_t gemm_bf16_gelu(const bf16_t* A, int lda, const bf16_t* W, int ldw, bf16_t* out, int ldo,
                           const float* bias, int M, int N, int K, hipStream_t s) {
+  if (N % 8 || ldo % 8) return hipErrorInvalidValue;
   return launch(A, lda, W, ldw, M, N, K, EpiGelu{out, bias, ldo, M, N}, s);
 }
 
