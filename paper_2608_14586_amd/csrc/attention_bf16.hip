@@ -13,11 +13,11 @@
 // O^T = V^T P^T wants its B operand: a lane's 8 bf16 values for keys
 // {8i + 4h + j : i in {2s, 2s+1}, j < 4} feed k-step s directly, and the A
 // fragment (V^T) is read from LDS in the same key order.  The softmax runs in
-// base 2 with log2(e)/sqrt(dh) folded into one scale.
+// base 2 with log2(e)/sqrt(dh) folded into one FMA per score.
 //
 // Causal tiles are masked per element only on the diagonal; a wave skips the
-// MFMAs of key tiles entirely beyond its last query.  Query blocks are issued
-// heaviest first.
+// MFMAs of key tiles entirely beyond its last query.  Causal query blocks are
+// issued so that co-resident workgroups carry complementary amounts of work.
 
 #include <math.h>
 
@@ -46,7 +46,12 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict
   const int id = blockIdx.x;
   const int rest = id % (H * B);
   const int qb_r = id / (H * B);
-  const int qb = CAUSAL ? (nqb - 1 - qb_r) : qb_r;
+  // causal: the first half of the grid takes the heavy query blocks in
+  // descending order, the second half the light ones ascending, so the two
+  // workgroups that share a CU (ids i and i + half the grid) sum to the same
+  // number of key tiles
+  const int heavy = (nqb + 1) / 2;
+  const int qb = !CAUSAL ? qb_r : (qb_r < heavy ? nqb - 1 - qb_r : qb_r - heavy);
   const int h = rest % H, b = rest / H;
   const int hk = h / (H / Hkv);
   const int q0 = qb * BQ;
@@ -144,23 +149,25 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict
           s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fk, fq[ks], s[t], 0, 0, 0);
         }
       }
-      // mask, scale, tile max
+      // tile max of the raw scores (the scale is positive, so it commutes
+      // with the max); masked entries become -inf
       const bool need_mask = (kb + BKV > L) || (CAUSAL && kb + BKV - 1 > qw0);
+      if (need_mask) {
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            int key = kb + t * 32 + (r >> 2) * 8 + half * 4 + (r & 3);
+            bool ok = key < L && (!CAUSAL || key <= qi);
+            s[t][r] = ok ? s[t][r] : -INFINITY;
+          }
+      }
       float mt = -INFINITY;
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          float x = s[t][r] * scale_log2;
-          if (need_mask) {
-            int key = kb + t * 32 + (r >> 2) * 8 + half * 4 + (r & 3);
-            bool ok = key < L && (!CAUSAL || key <= qi);
-            x = ok ? x : -INFINITY;
-          }
-          s[t][r] = x;
-          mt = fmaxf(mt, x);
-        }
-      mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+        for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[t][r]);
+      mt = fmaxf(mt, __shfl_xor(mt, 32, 64)) * scale_log2;
       const float m_new = fmaxf(m_run, mt);
       const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
       const float alpha = exp2f(m_run - m_use);
@@ -169,7 +176,8 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          float p = exp2f(s[t][r] - m_use);
+          // p = 2^(s * scale - m), one FMA and one exp per score
+          float p = exp2f(fmaf(s[t][r], scale_log2, -m_use));
           s[t][r] = p;
           psum += p;
         }
