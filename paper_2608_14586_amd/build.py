@@ -20,13 +20,16 @@ DEVICE_FLAGS = ["--offload-arch=" + ARCH, "-O3", "-fPIC", "-std=c++17", "-Xclang
 HOST_FLAGS = ["-O2", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-result"]
 
 SOURCES = ["gemm_bf16.hip", "attention_bf16.hip", "norm.hip", "fp32_path.hip", "runtime.cpp", "ops.cpp"]
+# Attention keeps its score and output accumulators in VGPRs: the softmax
+# touches them every key tile, and AGPR accumulators would cost a copy each way.
+EXTRA = {"attention_bf16.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 
 def _compile(src: str) -> str:
     path = os.path.join(CSRC, src)
     obj = os.path.join(OUT_DIR, src + ".o")
     if src.endswith(".hip"):
-        cmd = [HIPCC] + DEVICE_FLAGS + ["-c", path, "-o", obj]
+        cmd = [HIPCC] + DEVICE_FLAGS + EXTRA.get(src, []) + ["-c", path, "-o", obj]
     else:
         cmd = [HIPCC] + HOST_FLAGS + ["-c", path, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -136,17 +136,16 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict
     if (it + 1 < ntiles) gload(kb + BKV);
     const bool active = !CAUSAL || kb <= qw0 + 31;
     if (active && qw0 < L) {
-      // S^T for two 32-key tiles
+      // S^T for two 32-key tiles (the first k-step starts from a zero accumulator)
       f32x16 s[2];
+      const f32x16 zero = {};
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) s[t][r] = 0.f;
         const bf16_t* kbase = &sK[buf][(t * 32 + li) * LDK + half * 8];
 #pragma unroll
         for (int ks = 0; ks < DH / 16; ++ks) {
           bf16x8 fk = *(const bf16x8*)(kbase + ks * 16);
-          s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fk, fq[ks], s[t], 0, 0, 0);
+          s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fk, fq[ks], ks == 0 ? zero : s[t], 0, 0, 0);
         }
       }
       // tile max of the raw scores (the scale is positive, so it commutes
@@ -168,25 +167,33 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict
 #pragma unroll
         for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[t][r]);
       mt = fmaxf(mt, __shfl_xor(mt, 32, 64)) * scale_log2;
-      const float m_new = fmaxf(m_run, mt);
-      const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-      const float alpha = exp2f(m_run - m_use);
+      // Lazy rescaling: the running max m_run only moves (and O, l are only
+      // rescaled) when some query of the wave sees its max grow by more than
+      // 2^8; otherwise the probabilities are taken against the stale max and
+      // stay below 256, exactly representable in the same relative precision.
+      if (__any((mt > m_run + 8.f) ? 1 : 0)) {
+        const float m_new = fmaxf(m_run, mt);
+        const float alpha = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
+        l_part *= alpha;
+#pragma unroll
+        for (int t = 0; t < ND; ++t)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc_o[t][r] *= alpha;
+        m_run = m_new;
+      }
+      const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
       float psum = 0.f;
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          // p = 2^(s * scale - m), one FMA and one exp per score
-          float p = exp2f(fmaf(s[t][r], scale_log2, -m_use));
+          // p = 2^(s * scale - m), one FMA and one v_exp_f32 per score
+          // (results below 2^-126 flush to zero, which a softmax can ignore)
+          float p = __builtin_amdgcn_exp2f(fmaf(s[t][r], scale_log2, -m_use));
           s[t][r] = p;
           psum += p;
         }
-      l_part = l_part * alpha + psum;
-      m_run = m_new;
-#pragma unroll
-      for (int t = 0; t < ND; ++t)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc_o[t][r] *= alpha;
+      l_part += psum;
       // O^T += V^T P^T over 4 k-steps of 16 keys
 #pragma unroll
       for (int t = 0; t < 2; ++t)
