@@ -419,12 +419,16 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __
 #pragma unroll
     for (int ks = 0; ks < BK / 16; ++ks) {
       const int cur = ks & 1;
+      // the next step's fragment reads stay ahead of this step's MFMAs (left
+      // alone, the scheduler sinks each read onto its first use)
       if (ks + 1 < BK / 16) frags(buf, ks + 1, cur ^ 1);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
         for (int tn = 0; tn < TN; ++tn)
           acc.v[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cur][tm], fb[cur][tn], acc.v[tm][tn], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
     if (!last) {
       __builtin_amdgcn_s_waitcnt(0);
