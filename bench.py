@@ -62,12 +62,18 @@ def profiled_traffic(kernel_class):
     import re
     for path in glob.glob(os.path.join(ROOT, "profiles", "*_hbm_traffic.md")):
         for line in open(path):
-            m = re.match(r"machine-readable: kernel=(\S+) traffic_bytes=(\d+) source=(\S+) sha256_16=(\w+)", line)
+            m = re.match(r"machine-readable: kernel=(\S+) traffic_bytes=(\d+) sources=(\S+) sha256_16=(\w+)", line)
             if not m or m.group(1) != kernel_class:
                 continue
-            src = os.path.join(ROOT, m.group(3))
-            if os.path.exists(src) and hashlib.sha256(open(src, "rb").read()).hexdigest()[:16] == m.group(4):
-                return int(m.group(2))
+            h = hashlib.sha256()
+            for src in m.group(3).split(","):
+                path = os.path.join(ROOT, src)
+                if not os.path.exists(path):
+                    break
+                h.update(open(path, "rb").read())
+            else:
+                if h.hexdigest()[:16] == m.group(4):
+                    return int(m.group(2))
     return None
 
 
