@@ -4,8 +4,10 @@ One step = one frame of the partitioned pipeline's GPU stage (Sec. IV-A/C):
 the ViT-L-shaped encoder over 6 camera images x 1024 patch tokens, then the
 7B-shaped decoder blocks [0, k) as a causal prefill over 2048 tokens, then the
 handoff of the boundary hidden state and the k-layer KV cache to pinned host
-memory on a side stream (overlapping the next frame's encoder).  The headline
-is k = 16; the sweep reports k in {8, 16, 24, 32}.  Inputs and weights are
+memory on a side stream, overlapping the next frame's encoder.  The encoder
+and the decoder blocks share one compute stream: overlapping them on two
+streams let the per-layer KV copies fall behind the frames (measured).  The
+headline is k = 16; the sweep reports k in {8, 16, 24, 32}.  Inputs and weights are
 seeded synthetic tensors already resident in HBM; weights are random-init
 N(0, 0.02) at the stated shapes.
 
@@ -133,7 +135,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the prefix is a single-GPU stage (frames, cameras or block "
-              "ranges would shard across GPUs; see DESIGN.md). Run with --gpus 1.", file=sys.stderr)
+              "ranges would shard across GPUs). Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
@@ -190,7 +192,7 @@ def main():
         for i in range(n):
             f = fid[0]
             fid[0] += 1
-            st = ctx.compute_stream
+            st = ctx.encoder_stream
             if i == 0:
                 ev0.record(st)
             ctx.vla_run_encoder(f, pats[i % 2], n_img, L_img, enc_out)

@@ -122,9 +122,15 @@ vla_status vla_query_sizes(const vla_stack_cfg *llm, const vla_stack_cfg *enc, i
 /* Create a context on `device` over a caller-owned device arena of
  * arena_bytes (>= vla_query_sizes' answer; the library never calls hipMalloc
  * after this point).  llm may be NULL for an encoder-only context and vice
- * versa.  compute_stream runs the blocks; copy_stream runs the handoff. */
+ * versa.  compute_stream runs the decoder blocks, copy_stream the handoff.
+ * encoder_stream runs the encoder blocks; NULL puts them on compute_stream,
+ * one frame after the other.  Each stack has its own workspace in the arena,
+ * so with a stream of its own the encoder of frame f+1 runs concurrently with
+ * the prefix of frame f (the pipelining of Sec. IV-C on one GPU); the
+ * library orders the two stacks as vla_run_encoder states. */
 vla_status vla_create(const vla_stack_cfg *llm, const vla_stack_cfg *enc, int device, void *dev_arena,
-                      size_t arena_bytes, void *compute_stream, void *copy_stream, vla_ctx **out);
+                      size_t arena_bytes, void *compute_stream, void *encoder_stream, void *copy_stream,
+                      vla_ctx **out);
 
 /* Copy block `block` (0-based, < n_blocks) of stack `which` from host memory
  * into the arena.  Synchronous.  Re-loading a block replaces it. */
@@ -133,7 +139,12 @@ vla_status vla_load_block_weights(vla_ctx *ctx, vla_stack which, int block, cons
 /* Encoder: all n_blocks encoder blocks over patches[n_img][L_img][d_enc]
  * (host or device, stack dtype), each image attended independently; result
  * to out_dev[n_img][L_img][d_enc] (device, stack dtype).  Enqueued on the
- * compute stream; returns after launch. */
+ * encoder stream; returns after launch.  Ordering with the decoder, also
+ * with an encoder stream of its own: a later vla_run_prefix / vla_run_blocks
+ * on this context starts only after this run's output is written (so out_dev
+ * may be its tokens), and this run writes out_dev only after the latest
+ * earlier prefix has read its input (so one buffer may carry every frame).
+ * Other readers of out_dev order themselves after the encoder stream. */
 vla_status vla_run_encoder(vla_ctx *ctx, uint64_t frame_id, const void *patches, int n_img, int L_img,
                            void *out_dev);
 
@@ -180,10 +191,11 @@ typedef enum {
 } vla_kernel_class;
 
 /* Start (enable != 0, clearing previous totals) or stop timing every kernel
- * launch with a pair of HIP events on the compute stream. */
+ * launch with a pair of HIP events on the stream it runs on.  Launches of
+ * the two stacks that overlap in time are each timed over the overlap. */
 vla_status vla_profile(vla_ctx *ctx, int enable);
 /* Totals since vla_profile(ctx, 1) for one stack and class: summed kernel
- * time in ms and launch count.  Synchronises the compute stream. */
+ * time in ms and launch count.  Synchronises the compute and encoder streams. */
 vla_status vla_profile_read(vla_ctx *ctx, vla_stack which, vla_kernel_class cls, double *ms_total, int *launches);
 
 /* Bytes of the arena in use after the loads so far (weights + workspace). */

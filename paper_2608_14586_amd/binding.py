@@ -1,7 +1,7 @@
 """ctypes binding of the C ABI in include/vla_prefix.h and include/vla_ops.h.
 
 Argument marshalling only: every step of the prefix runs in the HIP library.
-PyTorch supplies the device arena, the two streams and the pinned host
+PyTorch supplies the device arena, the streams and the pinned host
 buffers (``torch.empty(..., pin_memory=True)``).  Functions keep the C names.
 If the library has not been built this module raises at first use; there is
 no fallback path.
@@ -69,7 +69,7 @@ def lib():
             "vla_query_sizes": [P(vla_stack_cfg), P(vla_stack_cfg), c_int, c_int, c_int, P(c_size_t), P(c_size_t),
                                 P(c_size_t)],
             "vla_create": [P(vla_stack_cfg), P(vla_stack_cfg), c_int, c_void_p, c_size_t, c_void_p, c_void_p,
-                           P(c_void_p)],
+                           c_void_p, P(c_void_p)],
             "vla_load_block_weights": [c_void_p, c_int, c_int, P(vla_block_weights)],
             "vla_run_encoder": [c_void_p, c_uint64, c_void_p, c_int, c_int, c_void_p],
             "vla_run_prefix": [c_void_p, c_uint64, c_void_p, c_int, c_int, c_int, P(vla_boundary)],
@@ -157,10 +157,12 @@ class Boundary:
 
 
 class Context:
-    """One vla_ctx over a torch-allocated device arena and two torch streams."""
+    """One vla_ctx over a torch-allocated device arena and torch streams for
+    the decoder blocks, the encoder blocks (the decoder's stream unless one
+    is given) and the handoff copies."""
 
     def __init__(self, llm: vla_stack_cfg = None, enc: vla_stack_cfg = None, device: int = 0,
-                 compute_stream=None, copy_stream=None):
+                 compute_stream=None, copy_stream=None, encoder_stream=None):
         import torch
         self.llm, self.enc = llm, enc
         self.device = device
@@ -169,11 +171,13 @@ class Context:
         with torch.cuda.device(device):
             self.arena = torch.empty(max(arena_bytes, 256), dtype=torch.uint8, device="cuda:%d" % device)
             self.compute_stream = compute_stream or torch.cuda.Stream(device=device)
+            # no encoder stream given: the encoder shares the compute stream
+            self.encoder_stream = encoder_stream or self.compute_stream
             self.copy_stream = copy_stream or torch.cuda.Stream(device=device)
         h = c_void_p()
         _check(lib().vla_create(ctypes.byref(llm) if llm else None, ctypes.byref(enc) if enc else None, device,
                                 self.arena.data_ptr(), self.arena.numel(), self.compute_stream.cuda_stream,
-                                self.copy_stream.cuda_stream, ctypes.byref(h)))
+                                self.encoder_stream.cuda_stream, self.copy_stream.cuda_stream, ctypes.byref(h)))
         self.h = h.value
 
     def vla_load_block_weights(self, which: int, block: int, weights: dict):

@@ -56,14 +56,23 @@ __device__ __forceinline__ f32x4 ld4(const float* p) { return *(const f32x4*)p; 
 // Exact GELU z * Phi(z) with Phi(z) = erfc(-z / sqrt 2) / 2, erfc from the
 // rational approximation of Abramowitz & Stegun 7.1.26 (|error| <= 1.5e-7,
 // far below bf16 resolution); erfc of |x| is formed directly, so the negative
-// tail does not cancel.
+// tail does not cancel.  The one division is the hardware reciprocal (1 ulp):
+// an IEEE divide would cost ten VALU instructions per element of a
+// [M][d_ff] epilogue that no MFMA work overlaps.
 __device__ __forceinline__ float gelu_as(float z) {
   const float x = fabsf(z) * 0.70710678118654752f;
-  const float t = 1.f / (1.f + 0.3275911f * x);
+  const float t = __builtin_amdgcn_rcpf(1.f + 0.3275911f * x);
   const float poly = t * (0.254829592f + t * (-0.284496736f + t * (1.421413741f + t * (-1.453152027f + t * 1.061405429f))));
   const float ec = poly * __expf(-x * x);  // erfc(x), x >= 0
   const float phi = z >= 0.f ? 1.f - 0.5f * ec : 0.5f * ec;
   return z * phi;
+}
+
+// largest divisor of n that is at most 16
+constexpr int batch_of(int n) {
+  int b = n < 16 ? n : 16;
+  while (n % b) --b;
+  return b;
 }
 
 __device__ __forceinline__ float silu(float g) { return g / (1.f + __expf(-g)); }
@@ -87,6 +96,7 @@ struct EpiStoreF32 {
         }
       }
   }
+  template <int R, int NC>
   __device__ void drain(const float*, int, int, int) const {}
 };
 
@@ -114,14 +124,17 @@ struct EpiBF16 {
         }
       }
   }
+  // T: R x NC fp32 tile (row stride NC) at (m0, n0); 256 threads.
+  template <int R, int NC>
   __device__ void drain(const float* T, int m0, int n0, int tid) const {
-    // 128 rows x 16 chunks of 8 columns
+    constexpr int CH = NC / 8;  // 16-byte output chunks per row
+    static_assert((R * CH) % 256 == 0, "tile must split evenly over the workgroup");
 #pragma unroll 4
-    for (int j = 0; j < ET * 16 / 256; ++j) {
-      const int f = tid + 256 * j, row = f >> 4, c8 = (f & 15) * 8;
+    for (int j = 0; j < R * CH / 256; ++j) {
+      const int f = tid + 256 * j, row = f / CH, c8 = (f % CH) * 8;
       const int gr = m0 + row, gc = n0 + c8;
       if (gr >= M || gc >= N) continue;
-      f32x4 x0 = ld4(T + row * ET + c8), x1 = ld4(T + row * ET + c8 + 4);
+      f32x4 x0 = ld4(T + row * NC + c8), x1 = ld4(T + row * NC + c8 + 4);
       if (bias) {
         f32x4 b0 = ld4(bias + gc), b1 = ld4(bias + gc + 4);
         x0 += b0;
@@ -164,24 +177,30 @@ struct EpiResidual {
         }
       }
   }
+  template <int R, int NC>
   __device__ void drain(const float* T, int m0, int n0, int tid) const {
-    // 128 rows x 32 float4; all residual loads of a thread issued first
-    constexpr int NJ = ET * 32 / 256;
-    f32x4 hv[NJ];
+    // R rows x NC/4 float4, in batches of 16 per thread with every residual
+    // load of a batch issued before its first add
+    constexpr int CH = NC / 4, NJ = R * CH / 256, NB = batch_of(NJ);
+    static_assert((R * CH) % 256 == 0 && NJ % NB == 0, "tile must split evenly over the workgroup");
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const int f = tid + 256 * j, row = f >> 5, c4 = (f & 31) * 4;
-      const int gr = m0 + row, gc = n0 + c4;
-      hv[j] = (gr < M && gc < N) ? ld4(H + (size_t)gr * ldh + gc) : f32x4{0.f, 0.f, 0.f, 0.f};
-    }
+    for (int j0 = 0; j0 < NJ; j0 += NB) {
+      f32x4 hv[NB];
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const int f = tid + 256 * j, row = f >> 5, c4 = (f & 31) * 4;
-      const int gr = m0 + row, gc = n0 + c4;
-      if (gr >= M || gc >= N) continue;
-      f32x4 x = ld4(T + row * ET + c4);
-      if (bias) x += ld4(bias + gc);
-      *(f32x4*)(H + (size_t)gr * ldh + gc) = hv[j] + x;
+      for (int j = 0; j < NB; ++j) {
+        const int f = tid + 256 * (j0 + j), row = f / CH, c4 = (f % CH) * 4;
+        const int gr = m0 + row, gc = n0 + c4;
+        hv[j] = (gr < M && gc < N) ? ld4(H + (size_t)gr * ldh + gc) : f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        const int f = tid + 256 * (j0 + j), row = f / CH, c4 = (f % CH) * 4;
+        const int gr = m0 + row, gc = n0 + c4;
+        if (gr >= M || gc >= N) continue;
+        f32x4 x = ld4(T + row * NC + c4);
+        if (bias) x += ld4(bias + gc);
+        *(f32x4*)(H + (size_t)gr * ldh + gc) = hv[j] + x;
+      }
     }
   }
 };
@@ -208,15 +227,18 @@ struct EpiSwiGLU {
         }
       }
   }
+  template <int R, int NC>
   __device__ void drain(const float* T, int m0, int n0, int tid) const {
-    // 128 rows x 8 chunks of 8 output features
+    // R rows x NC/16 chunks of 8 output features (4 chunks per 64-column group)
+    constexpr int CH = NC / 16;
+    static_assert((R * CH) % 256 == 0, "tile must split evenly over the workgroup");
 #pragma unroll
-    for (int j = 0; j < ET * 8 / 256; ++j) {
-      const int f = tid + 256 * j, row = f >> 3, c = f & 7;
-      const int gsel = c >> 2, w = (c & 3) * 8;           // 64-column group, offset inside its 32
+    for (int j = 0; j < R * CH / 256; ++j) {
+      const int f = tid + 256 * j, row = f / CH, c = f % CH;
+      const int gsel = c >> 2, w = (c & 3) * 8;  // 64-column group, offset inside its 32
       const int gr = m0 + row;
       if (gr >= M || n0 + gsel * 64 >= N) continue;
-      const float* tr = T + row * ET + gsel * 64 + w;
+      const float* tr = T + row * NC + gsel * 64 + w;
       f32x4 g0 = ld4(tr), g1 = ld4(tr + 4), u0 = ld4(tr + 32), u1 = ld4(tr + 36);
       f32x4 y0, y1;
 #pragma unroll
@@ -251,19 +273,22 @@ struct EpiQKV {
   }
   template <int TM, int TN>
   __device__ void operator()(const Acc<TM, TN>&, int, int, int) const {}  // LDS path only
+  template <int R, int NC>
   __device__ void drain(const float* T, int m0, int n0, int tid) const {
     const int dh = q.dh, L = q.L;
-    // rows: 128 tokens x 2 column groups x 4 chunks of 8 dims
+    // R tokens x NC/64 column groups x 4 chunks of 8 dims
+    constexpr int CH = NC / 16;
+    static_assert((R * CH) % 256 == 0 && (R * 8) % 256 == 0, "tile must split evenly over the workgroup");
 #pragma unroll 2
-    for (int j = 0; j < ET * 8 / 256; ++j) {
-      const int f = tid + 256 * j, row = f >> 3, gsel = (f >> 2) & 1, w = (f & 3) * 8;
+    for (int j = 0; j < R * CH / 256; ++j) {
+      const int f = tid + 256 * j, row = f / CH, gsel = (f % CH) >> 2, w = (f & 3) * 8;
       const int gr = m0 + row, p = n0 + gsel * 64;
       int kind, head, r;
       classify(p, kind, head, r);
       if (gr >= M || kind == 3) continue;
       const int c = r / 64;
       const int d1 = c * 32 + w, d2 = dh / 2 + c * 32 + w;
-      const float* tr = T + row * ET + gsel * 64 + w;
+      const float* tr = T + row * NC + gsel * 64 + w;
       f32x4 x10 = ld4(tr), x11 = ld4(tr + 4), x20 = ld4(tr + 32), x21 = ld4(tr + 36);
       if (q.bias) {
         x10 += ld4(q.bias + p + w);
@@ -286,14 +311,14 @@ struct EpiQKV {
       *(u32x4*)(dst + d2) = pack8(x20, x21);
     }
     // V^T: one (dim, 8 consecutive tokens) chunk per item
-    for (int gsel = 0; gsel < 2; ++gsel) {
+    for (int gsel = 0; gsel < NC / 64; ++gsel) {
       int kind, head, r;
       const int p = n0 + gsel * 64;
       classify(p, kind, head, r);
       if (kind != 2) continue;
       const int c = r / 64;
 #pragma unroll 2
-      for (int j = 0; j < 64 * 16 / 256; ++j) {
+      for (int j = 0; j < R * 8 / 256; ++j) {
         const int f = tid + 256 * j, col = f & 63, t8 = (f >> 6) * 8;
         const int gr0 = m0 + t8;
         if (gr0 >= M) continue;
@@ -301,7 +326,7 @@ struct EpiQKV {
         const float bcol = q.bias ? q.bias[p + col] : 0.f;
         float v[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = T[(t8 + e) * ET + gsel * 64 + col] + bcol;
+        for (int e = 0; e < 8; ++e) v[e] = T[(t8 + e) * NC + gsel * 64 + col] + bcol;
         const int b0 = gr0 / L, pos0 = gr0 - b0 * L;
         if (gr0 + 7 < M && pos0 + 7 < L && (pos0 & 7) == 0 && (q.ldvt & 7) == 0) {
           u32x4 w4 = {pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]), pack_bf2(v[4], v[5]), pack_bf2(v[6], v[7])};
@@ -335,10 +360,9 @@ __device__ __forceinline__ void buffer_load_lds16(__amdgpu_buffer_rsrc_t r, void
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, voff, 0, 0, 0);
 }
 
-template <int BM, int BN, int WM, int WN, int NW, class Epi>
-__global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __restrict__ A, int lda,
-                                                                const bf16_t* __restrict__ W, int ldw, int M, int N,
-                                                                int K, Epi epi) {
+template <int BM, int BN, int WM, int WN, int NW, bool WT, class Epi>
+__global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __restrict__ A, int lda, WOperand W,
+                                                                int M, int N, int K, Epi epi) {
   constexpr int TM = WM / 32, TN = WN / 32;
   constexpr int WAVES_N = BN / WN;
   static_assert((BM / WM) * (BN / WN) == NW, "wave grid must cover the tile");
@@ -364,8 +388,14 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __
   // buffer resources over the tile's rows; rows past M / N read as zero
   const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
       (void*)(A + (size_t)m0 * lda), (short)0, (int)((size_t)(M - m0) * lda * 2), 0x00020000);
-  const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)(W + (size_t)n0 * ldw), (short)0, (int)((size_t)(N - n0) * ldw * 2), 0x00020000);
+  // W: row-major rows from n0 on, or the whole packed matrix (every block of
+  // a tile lies inside it: the packing pads N to whole 256-row pairs)
+  const int ldw = W.ld, nblk = W.nblk, nb0 = n0 / SLAB_N, nkt = K / BK;
+  const __amdgpu_buffer_rsrc_t rb =
+      WT ? __builtin_amdgcn_make_buffer_rsrc((void*)W.p, (short)0, (int)((size_t)nblk * SLAB_N * K * 2), 0x00020000)
+         : __builtin_amdgcn_make_buffer_rsrc((void*)(W.p + (size_t)n0 * ldw), (short)0,
+                                             (int)((size_t)(N - n0) * ldw * 2), 0x00020000);
+  (void)nkt;
 
   // this lane's slot in each 1 KB load: row (lane / 8) of the 8-row group,
   // LDS chunk (lane % 8) holding global chunk (lane % 8) ^ key(tile row)
@@ -382,7 +412,11 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __
     for (int j = 0; j < B_INST; ++j) {
       const int row = (wave * B_INST + j) * 8 + lrow;
       const int ch = lslot ^ ((row >> 1) & 7);
-      buffer_load_lds16(rb, base + BM * ROWB + (wave * B_INST + j) * 1024, (unsigned)((row * ldw + k0 + ch * 8) * 2));
+      // packed: the slab of 128 rows x 64 k is one contiguous 16 KB block
+      const unsigned off =
+          WT ? (unsigned)((((k0 / BK) * nblk + nb0 + row / SLAB_N) * SLAB_N + row % SLAB_N) * ROWB + ch * 16)
+             : (unsigned)((row * ldw + k0 + ch * 8) * 2);
+      buffer_load_lds16(rb, base + BM * ROWB + (wave * B_INST + j) * 1024, off);
     }
   };
 
@@ -450,19 +484,25 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __
         for (int r = 0; r < 16; ++r)
           T[(wm * WM + tm * 32 + acc_row(r, lane)) * ET + wn * WN + tn * 32 + (lane & 31)] = acc.v[tm][tn][r];
     __syncthreads();
-    epi.drain(T, m0, n0, tid);
+    epi.template drain<ET, ET>(T, m0, n0, tid);
   } else {
     epi(acc, m0 + wm * WM, n0 + wn * WN, lane);
   }
 }
 
-template <class Epi>
-hipError_t launch(const bf16_t* A, int lda, const bf16_t* W, int ldw, int M, int N, int K, const Epi& epi,
-                  hipStream_t s) {
+template <bool WT, class Epi>
+hipError_t launch(const bf16_t* A, int lda, const WOperand& W, int M, int N, int K, const Epi& epi, hipStream_t s) {
   if (M <= 0 || N <= 0) return hipSuccess;
-  if (K % BK != 0 || lda % 8 != 0 || ldw % 8 != 0) return hipErrorInvalidValue;
+  if (K % BK != 0 || lda % 8 != 0) return hipErrorInvalidValue;
+  if (WT) {
+    // every 256-column tile inside the packing, 32-bit byte offsets
+    if (W.nblk <= 0 || W.nblk % 2 || W.nblk * SLAB_N < N || (size_t)W.nblk * SLAB_N * K * 2 >= (1u << 31))
+      return hipErrorInvalidValue;
+  } else {
+    if (W.ld % 8 != 0 || W.ld < K || (size_t)256 * W.ld * 2 >= (1u << 31)) return hipErrorInvalidValue;
+  }
   // byte offsets inside a tile's buffer resource are 32-bit
-  if ((size_t)256 * lda * 2 >= (1u << 31) || (size_t)256 * ldw * 2 >= (1u << 31)) return hipErrorInvalidValue;
+  if ((size_t)256 * lda * 2 >= (1u << 31)) return hipErrorInvalidValue;
   // 256x256 tiles (8 waves of 128x64) once they fill the chip at least twice;
   // otherwise 128x128 tiles (4 waves of 64x64, two workgroups per CU)
   const long tiles256 = (long)((M + 255) / 256) * ((N + 255) / 256);
@@ -471,13 +511,13 @@ hipError_t launch(const bf16_t* A, int lda, const bf16_t* W, int ldw, int M, int
     if (tiles256 >= 512) {
       big = true;
       int grid = ((M + 255) / 256) * ((N + 255) / 256);
-      hipLaunchKernelGGL((gemm_bf16_dma_kernel<256, 256, 128, 64, 8, Epi>), dim3(grid), dim3(512), 0, s, A, lda, W,
-                         ldw, M, N, K, epi);
+      hipLaunchKernelGGL((gemm_bf16_dma_kernel<256, 256, 128, 64, 8, WT, Epi>), dim3(grid), dim3(512), 0, s, A, lda,
+                         W, M, N, K, epi);
     }
   }
   if (!big) {
     int grid = ((M + 127) / 128) * ((N + 127) / 128);
-    hipLaunchKernelGGL((gemm_bf16_dma_kernel<128, 128, 64, 64, 4, Epi>), dim3(grid), dim3(256), 0, s, A, lda, W, ldw,
+    hipLaunchKernelGGL((gemm_bf16_dma_kernel<128, 128, 64, 64, 4, WT, Epi>), dim3(grid), dim3(256), 0, s, A, lda, W,
                        M, N, K, epi);
   }
   return hipGetLastError();
@@ -487,38 +527,32 @@ hipError_t launch(const bf16_t* A, int lda, const bf16_t* W, int ldw, int M, int
 
 hipError_t gemm_bf16_store_f32(const bf16_t* A, int lda, const bf16_t* W, int ldw, float* C, int ldc, int M, int N,
                                int K, hipStream_t s) {
-  return launch(A, lda, W, ldw, M, N, K, EpiStoreF32{C, ldc, M, N}, s);
+  return launch<false>(A, lda, WOperand{W, ldw, 0}, M, N, K, EpiStoreF32{C, ldc, M, N}, s);
 }
 
-hipError_t gemm_bf16_store_bf16(const bf16_t* A, int lda, const bf16_t* W, int ldw, bf16_t* C, int ldc,
-                                const float* bias, int M, int N, int K, hipStream_t s) {
-  if (N % 8 || ldc % 8) return hipErrorInvalidValue;
-  return launch(A, lda, W, ldw, M, N, K, EpiStoreBF16{C, bias, ldc, M, N}, s);
-}
-
-hipError_t gemm_bf16_residual(const bf16_t* A, int lda, const bf16_t* W, int ldw, float* H, int ldh,
-                              const float* bias, int M, int N, int K, hipStream_t s) {
+hipError_t gemm_bf16_residual(const bf16_t* A, int lda, const WOperand& W, float* H, int ldh, const float* bias, int M,
+                              int N, int K, hipStream_t s) {
   if (N % 4 || ldh % 4) return hipErrorInvalidValue;
-  return launch(A, lda, W, ldw, M, N, K, EpiResidual{H, bias, ldh, M, N}, s);
+  return launch<true>(A, lda, W, M, N, K, EpiResidual{H, bias, ldh, M, N}, s);
 }
 
-hipError_t gemm_bf16_swiglu(const bf16_t* A, int lda, const bf16_t* W, int ldw, bf16_t* out, int ldo, int M, int N,
-                            int K, hipStream_t s) {
+hipError_t gemm_bf16_swiglu(const bf16_t* A, int lda, const WOperand& W, bf16_t* out, int ldo, int M, int N, int K,
+                            hipStream_t s) {
   if (N % 64 != 0) return hipErrorInvalidValue;
   if (ldo % 8) return hipErrorInvalidValue;
-  return launch(A, lda, W, ldw, M, N, K, EpiSwiGLU{out, ldo, M, N}, s);
+  return launch<true>(A, lda, W, M, N, K, EpiSwiGLU{out, ldo, M, N}, s);
 }
 
-hipError_t gemm_bf16_gelu(const bf16_t* A, int lda, const bf16_t* W, int ldw, bf16_t* out, int ldo,
-                          const float* bias, int M, int N, int K, hipStream_t s) {
+hipError_t gemm_bf16_gelu(const bf16_t* A, int lda, const WOperand& W, bf16_t* out, int ldo, const float* bias, int M,
+                          int N, int K, hipStream_t s) {
   if (N % 8 || ldo % 8) return hipErrorInvalidValue;
-  return launch(A, lda, W, ldw, M, N, K, EpiGelu{out, bias, ldo, M, N}, s);
+  return launch<true>(A, lda, W, M, N, K, EpiGelu{out, bias, ldo, M, N}, s);
 }
 
-hipError_t gemm_bf16_qkv(const bf16_t* A, int lda, const bf16_t* W, int ldw, const QkvArgs& qa, int M, int N, int K,
+hipError_t gemm_bf16_qkv(const bf16_t* A, int lda, const WOperand& W, const QkvArgs& qa, int M, int N, int K,
                          hipStream_t s) {
   if (qa.dh % 64 != 0 || N % 64 != 0) return hipErrorInvalidValue;
-  return launch(A, lda, W, ldw, M, N, K, EpiQKV{qa, M}, s);
+  return launch<true>(A, lda, W, M, N, K, EpiQKV{qa, M}, s);
 }
 
 }  // namespace vla

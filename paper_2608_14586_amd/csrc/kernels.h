@@ -10,24 +10,40 @@ namespace vla {
 
 // ---------------------------------------------------------------- bf16 GEMMs
 // Every GEMM computes acc[M][N] = A[M][K] * W[N][K]^T (bf16 in, fp32
-// accumulate) and hands acc to an epilogue.  K % 64 == 0, lda/ldw % 8 == 0.
+// accumulate) and hands acc to an epilogue.  K % 64 == 0, lda % 8 == 0.
+//
+// Resident weights are packed slab-major: the GEMM moves W in slabs of
+// SLAB_N rows x 64 k, and each slab is one contiguous 16 KB block, the blocks
+// of one k range side by side:
+//   element (n, k) at ((k / 64 * nblk + n / SLAB_N) * SLAB_N + n % SLAB_N) * 64 + k % 64
+// nblk = slab_blocks(N) (N rounded up to whole pairs of blocks, pad rows
+// zero).  At any moment the whole chip then streams one contiguous stretch of
+// the weights, rather than 128-byte pieces of rows 2*K bytes apart.
+constexpr int SLAB_N = 128;
+inline int slab_blocks(int N) { return (N + 2 * SLAB_N - 1) / (2 * SLAB_N) * 2; }
 
-// C (fp32) = acc
+// A weight operand: packed (nblk > 0, ld unused) or row-major with leading
+// dimension ld (nblk == 0).
+struct WOperand {
+  const bf16_t* p;
+  int ld;
+  int nblk;
+};
+
+// C (fp32) = acc, W row-major [N][ldw] (ldw % 8 == 0)
 hipError_t gemm_bf16_store_f32(const bf16_t* A, int lda, const bf16_t* W, int ldw, float* C, int ldc, int M,
                                int N, int K, hipStream_t s);
-// C (bf16) = acc + bias (bias may be NULL)
-hipError_t gemm_bf16_store_bf16(const bf16_t* A, int lda, const bf16_t* W, int ldw, bf16_t* C, int ldc,
-                                const float* bias, int M, int N, int K, hipStream_t s);
+// The block GEMMs below take packed weights.
 // H (fp32 residual) += acc + bias (bias may be NULL)
-hipError_t gemm_bf16_residual(const bf16_t* A, int lda, const bf16_t* W, int ldw, float* H, int ldh,
-                              const float* bias, int M, int N, int K, hipStream_t s);
+hipError_t gemm_bf16_residual(const bf16_t* A, int lda, const WOperand& W, float* H, int ldh, const float* bias,
+                              int M, int N, int K, hipStream_t s);
 // out (bf16) [M][N/2] = silu(gate) * up, W rows interleaved in groups of 32
 // (32 gate rows, then the 32 up rows of the same features); N % 64 == 0.
-hipError_t gemm_bf16_swiglu(const bf16_t* A, int lda, const bf16_t* W, int ldw, bf16_t* out, int ldo, int M,
-                            int N, int K, hipStream_t s);
+hipError_t gemm_bf16_swiglu(const bf16_t* A, int lda, const WOperand& W, bf16_t* out, int ldo, int M, int N, int K,
+                            hipStream_t s);
 // out (bf16) = gelu_erf(acc + bias)
-hipError_t gemm_bf16_gelu(const bf16_t* A, int lda, const bf16_t* W, int ldw, bf16_t* out, int ldo,
-                          const float* bias, int M, int N, int K, hipStream_t s);
+hipError_t gemm_bf16_gelu(const bf16_t* A, int lda, const WOperand& W, bf16_t* out, int ldo, const float* bias,
+                          int M, int N, int K, hipStream_t s);
 
 // Fused QKV projection epilogue.  Packed weight rows: [q heads | k heads |
 // v heads], each head's head_dim rows in 64-row groups that hold 32 rows of
@@ -44,8 +60,8 @@ struct QkvArgs {
   int ldvt;
   int L, H, Hkv, dh;
 };
-hipError_t gemm_bf16_qkv(const bf16_t* A, int lda, const bf16_t* W, int ldw, const QkvArgs& qa, int M, int N,
-                         int K, hipStream_t s);
+hipError_t gemm_bf16_qkv(const bf16_t* A, int lda, const WOperand& W, const QkvArgs& qa, int M, int N, int K,
+                         hipStream_t s);
 
 // ---------------------------------------------------------- bf16 attention
 // o[B][L][H*dh] = softmax(q k^T / sqrt(dh) [+ causal mask]) v per (b, head);

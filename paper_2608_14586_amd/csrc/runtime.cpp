@@ -73,6 +73,13 @@ struct Stack {
   bool llm() const { return !c.norm_is_layernorm; }
   // rows of the up projection: interleaved gate/up (LLM) or fc1 (encoder)
   int up_rows() const { return llm() ? 2 * f_pad : f_pad; }
+  // arena bytes of a weight matrix [N][K]: bf16 stacks hold it packed
+  // slab-major over slab_blocks(N) blocks, fp32 stacks row-major
+  size_t weight_bytes(int N, int K) const {
+    return bf16() ? (size_t)vla::slab_blocks(N) * vla::SLAB_N * K * esz : (size_t)N * K * esz;
+  }
+  // the GEMM operand of a resident bf16 weight matrix with N rows
+  static vla::WOperand packed(const void* p, int N) { return vla::WOperand{(const bf16_t*)p, 0, vla::slab_blocks(N)}; }
 };
 
 Status validate_stack(const vla_stack_cfg* c, bool is_llm, Stack* s) {
@@ -130,6 +137,21 @@ struct FrameTimes {
   float gpu, xfer, total;
 };
 
+// Scratch of one stack.  The encoder and the decoder run on streams of their
+// own and overlap, so each stack owns its workspace.
+struct Workspace {
+  float* h = nullptr;        // fp32 residual
+  void* x = nullptr;         // normalised activations
+  void* q = nullptr;         // [B][H][L][dh]
+  void* ek = nullptr;        // encoder K / V (the decoder writes into the slot cache)
+  void* ev = nullptr;
+  void* vt = nullptr;        // V^T
+  void* o = nullptr;         // attention output [M][H*dh]
+  void* act = nullptr;       // MLP activation
+  float* qkv_raw = nullptr;  // fp32 path only
+  void* tok = nullptr;       // staging of host-resident inputs
+};
+
 }  // namespace
 
 struct vla_ctx {
@@ -137,22 +159,18 @@ struct vla_ctx {
   Stack llm, enc;
   char* arena = nullptr;
   size_t arena_bytes = 0, used = 0;
-  hipStream_t compute = nullptr, copy = nullptr;
+  // compute: decoder blocks; encs: encoder blocks; copy: the handoff
+  hipStream_t compute = nullptr, encs = nullptr, copy = nullptr;
   bool own_compute = false, own_copy = false;
   std::string last_error;
 
-  // workspace (sized for the larger stack)
-  float* h = nullptr;      // fp32 residual
-  void* x = nullptr;       // normalised activations
-  void* q = nullptr;       // [B][H][L][dh]
-  void* ek = nullptr;      // encoder K / V (LLM writes into the slot cache)
-  void* ev = nullptr;
-  void* vt = nullptr;      // V^T
-  void* o = nullptr;       // attention output [M][H*dh]
-  void* act = nullptr;     // MLP activation
-  float* qkv_raw = nullptr;  // fp32 path only
-  void* tok = nullptr;     // staging of host-resident inputs
+  Workspace ws[2];  // by vla_stack
   float *rope_cos = nullptr, *rope_sin = nullptr;
+  // cross-stream order: a prefix waits for the latest encoder run (whose
+  // output it may read); an encoder's output write waits for the latest
+  // prefix intake (which may read the buffer being overwritten)
+  hipEvent_t ev_enc_done = nullptr, ev_intake = nullptr;
+  bool enc_recorded = false, intake_recorded = false;
   Slot slots[NSLOT];
   int next_slot = 0;
   std::map<uint64_t, FrameTimes> history;
@@ -189,12 +207,12 @@ void layout(vla_ctx* c, Bump& a) {
   Stack* stacks[2] = {&c->llm, &c->enc};
   for (Stack* s : stacks) {
     if (!s->present) continue;
-    const size_t d = s->c.d_model, e = s->esz;
+    const size_t d = s->c.d_model;
     for (auto& b : s->blocks) {
-      b.w_qkv = a.take((size_t)s->qkv_n * d * e);
-      b.w_o = a.take(d * s->hd * e);
-      b.w_up = a.take((size_t)s->up_rows() * d * e);
-      b.w_down = a.take(d * s->f_pad * e);
+      b.w_qkv = a.take(s->weight_bytes(s->qkv_n, (int)d));
+      b.w_o = a.take(s->weight_bytes((int)d, s->hd));
+      b.w_up = a.take(s->weight_bytes(s->up_rows(), (int)d));
+      b.w_down = a.take(s->weight_bytes((int)d, s->f_pad));
       b.n1g = (float*)a.take(d * 4);
       b.n2g = (float*)a.take(d * 4);
       if (s->c.has_bias) {
@@ -209,32 +227,24 @@ void layout(vla_ctx* c, Bump& a) {
       }
     }
   }
-  size_t h = 0, x = 0, q = 0, ekv = 0, vt = 0, o = 0, act = 0, raw = 0, tok = 0;
-  for (Stack* s : stacks) {
+  for (int si = 0; si < 2; ++si) {
+    Stack* s = stacks[si];
     if (!s->present) continue;
+    Workspace& w = c->ws[si];
     const size_t M = s->m_max, d = s->c.d_model, e = s->esz;
-    h = std::max(h, M * d * 4);
-    x = std::max(x, M * d * e);
-    q = std::max(q, M * s->hd * e);
-    o = std::max(o, M * s->hd * e);
-    vt = std::max(vt, (size_t)s->c.max_batch * s->kvd * s->ldvt * e);
-    tok = std::max(tok, M * d * e);
-    if (s->bf16())
-      act = std::max(act, M * s->f_pad * e);
-    else
-      act = std::max(act, M * (size_t)s->c.d_ff * (s->llm() ? 3 : 1) * 4), raw = std::max(raw, M * s->qkv_n * 4);
-    if (s == &c->enc) ekv = std::max(ekv, M * s->kvd * e);
+    w.h = (float*)a.take(M * d * 4);
+    w.x = a.take(M * d * e);
+    w.q = a.take(M * s->hd * e);
+    if (!s->llm()) {
+      w.ek = a.take(M * s->kvd * e);
+      w.ev = a.take(M * s->kvd * e);
+    }
+    w.vt = a.take((size_t)s->c.max_batch * s->kvd * s->ldvt * e);
+    w.o = a.take(M * s->hd * e);
+    w.act = a.take(s->bf16() ? M * s->f_pad * e : M * (size_t)s->c.d_ff * (s->llm() ? 3 : 1) * 4);
+    if (!s->bf16()) w.qkv_raw = (float*)a.take(M * s->qkv_n * 4);
+    w.tok = a.take(M * d * e);
   }
-  c->h = (float*)a.take(h);
-  c->x = a.take(x);
-  c->q = a.take(q);
-  c->ek = a.take(ekv);
-  c->ev = a.take(ekv);
-  c->vt = a.take(vt);
-  c->o = a.take(o);
-  c->act = a.take(act);
-  c->qkv_raw = (float*)a.take(raw);
-  c->tok = a.take(tok);
   int rope_len = 0, rope_half = 0;
   if (c->llm.present && c->llm.c.use_rope) rope_len = c->llm.c.max_tokens, rope_half = c->llm.c.head_dim / 2;
   c->rope_cos = (float*)a.take((size_t)rope_len * rope_half * 4);
@@ -277,6 +287,19 @@ Status copy_h2d(void* dst, const void* src, size_t bytes) {
   return OK;
 }
 
+// Row-major weight rows [N][K] -> the arena: packed slab-major for bf16
+// stacks (the layout the GEMMs read, kernels.h), as-is for fp32 stacks.
+Status put_weight(const Stack& s, void* dst, const void* rm, int N, int K) {
+  if (!s.bf16()) return copy_h2d(dst, rm, (size_t)N * K * s.esz);
+  const int nblk = vla::slab_blocks(N), SN = vla::SLAB_N;
+  std::vector<uint16_t> t((size_t)nblk * SN * K, 0);
+  const uint16_t* src = (const uint16_t*)rm;
+  for (int kt = 0; kt < K / 64; ++kt)
+    for (int n = 0; n < N; ++n)
+      memcpy(&t[(((size_t)kt * nblk + n / SN) * SN + n % SN) * 64], src + (size_t)n * K + (size_t)kt * 64, 128);
+  return copy_h2d(dst, t.data(), t.size() * 2);
+}
+
 Status load_block(vla_ctx* c, Stack& s, int bi, const vla_block_weights* w) {
   const vla_stack_cfg& k = s.c;
   const bool llm = s.llm();
@@ -308,7 +331,7 @@ Status load_block(vla_ctx* c, Stack& s, int bi, const vla_block_weights* w) {
           size_t tr = hh * dh + (s.bf16() ? qkv_packed_to_true_dim((int)r, (int)dh) : r);
           memcpy(&buf[prow * d * e], (const char*)src[part] + tr * d * e, d * e);
         }
-    Status st = copy_h2d(b.w_qkv, buf.data(), buf.size());
+    Status st = put_weight(s, b.w_qkv, buf.data(), s.qkv_n, (int)d);
     if (st.code) return st;
     if (k.has_bias) {
       std::vector<float> bias(s.qkv_n);
@@ -323,7 +346,7 @@ Status load_block(vla_ctx* c, Stack& s, int bi, const vla_block_weights* w) {
       if ((st = copy_h2d(b.b_qkv, bias.data(), bias.size() * 4)).code) return st;
     }
   }
-  Status st = copy_h2d(b.w_o, w->w_o, d * s.hd * e);
+  Status st = put_weight(s, b.w_o, w->w_o, (int)d, s.hd);
   if (st.code) return st;
   // up projection: interleaved gate/up (bf16), [gate; up] (fp32), or fc1
   {
@@ -346,7 +369,7 @@ Status load_block(vla_ctx* c, Stack& s, int bi, const vla_block_weights* w) {
     } else {
       memcpy(buf.data(), w->w_fc1, F * d * e);
     }
-    if ((st = copy_h2d(b.w_up, buf.data(), buf.size())).code) return st;
+    if ((st = put_weight(s, b.w_up, buf.data(), s.up_rows(), (int)d)).code) return st;
   }
   // down projection [d][f_pad] with zero pad columns
   {
@@ -354,7 +377,7 @@ Status load_block(vla_ctx* c, Stack& s, int bi, const vla_block_weights* w) {
     const void* src = llm ? w->w_down : w->w_fc2;
     std::vector<char> buf(d * FP * e, 0);
     for (size_t r = 0; r < d; ++r) memcpy(&buf[r * FP * e], (const char*)src + r * F * e, F * e);
-    if ((st = copy_h2d(b.w_down, buf.data(), buf.size())).code) return st;
+    if ((st = put_weight(s, b.w_down, buf.data(), (int)d, (int)FP)).code) return st;
   }
   auto put = [&](float* dst, const void* src, size_t n, size_t npad) -> Status {
     std::vector<float> v = vec_f32(src, n, k.dtype);
@@ -406,8 +429,11 @@ Status prof_event(vla_ctx* c, hipEvent_t* e) {
   return OK;
 }
 
+hipStream_t stream_of(const vla_ctx* c, int stk) { return stk == VLA_STACK_ENC ? c->encs : c->compute; }
+
 Status prof_drain(vla_ctx* c) {
   HIPTRY(hipStreamSynchronize(c->compute));
+  if (c->encs != c->compute) HIPTRY(hipStreamSynchronize(c->encs));
   for (const auto& r : c->prof_recs) {
     float ms = 0.f;
     HIPTRY(hipEventElapsedTime(&ms, r.a, r.b));
@@ -425,21 +451,21 @@ Status prof_drain(vla_ctx* c) {
     if (e_ != hipSuccess) return fail(VLA_ERR_HIP, "launch %s: %s", #expr, hipGetErrorString(e_)); \
   } while (0)
 
-// Launch `expr` on the compute stream; with the profiler on, bracket it with
-// a pair of events attributed to (stack, class).
+// Launch `expr` (on the stack's stream); with the profiler on, bracket it
+// with a pair of events on that stream attributed to (stack, class).
 #define PLAUNCH(c, stk, cls, expr)                                                          \
   do {                                                                                      \
     hipEvent_t a_ = nullptr, b_ = nullptr;                                                  \
     if ((c)->prof_on) {                                                                     \
       Status s_ = prof_event((c), &a_);                                                     \
       if (s_.code) return s_;                                                               \
-      HIPTRY(hipEventRecord(a_, (c)->compute));                                             \
+      HIPTRY(hipEventRecord(a_, stream_of((c), (stk))));                                    \
     }                                                                                       \
     KTRY(expr);                                                                             \
     if ((c)->prof_on) {                                                                     \
       Status s_ = prof_event((c), &b_);                                                     \
       if (s_.code) return s_;                                                               \
-      HIPTRY(hipEventRecord(b_, (c)->compute));                                             \
+      HIPTRY(hipEventRecord(b_, stream_of((c), (stk))));                                    \
       (c)->prof_recs.push_back(vla_ctx::ProfRec{(stk) * VLA_K_COUNT + (cls), a_, b_});      \
       if ((c)->prof_recs.size() >= (1u << 16)) {                                            \
         Status d_ = prof_drain(c);                                                          \
@@ -448,23 +474,25 @@ Status prof_drain(vla_ctx* c) {
     }                                                                                       \
   } while (0)
 
-// input[B*L][d] (host or device, element type in_dt) -> fp32 residual c->h
+// input[B*L][d] (host or device, element type in_dt) -> the stack's fp32 residual
 Status intake(vla_ctx* c, int stk, vla_dtype in_dt, const void* in, size_t n) {
+  Workspace& ws = c->ws[stk];
+  const hipStream_t st = stream_of(c, stk);
   const void* src = in;
   if (!is_device(in)) {
     // host input: fp32 goes straight into the residual, bf16 through the
     // input staging buffer
     if (in_dt == VLA_F32) {
-      HIPTRY(hipMemcpyAsync(c->h, in, n * 4, hipMemcpyHostToDevice, c->compute));
+      HIPTRY(hipMemcpyAsync(ws.h, in, n * 4, hipMemcpyHostToDevice, st));
       return OK;
     }
-    HIPTRY(hipMemcpyAsync(c->tok, in, n * 2, hipMemcpyHostToDevice, c->compute));
-    src = c->tok;
+    HIPTRY(hipMemcpyAsync(ws.tok, in, n * 2, hipMemcpyHostToDevice, st));
+    src = ws.tok;
   }
   if (in_dt == VLA_BF16)
-    PLAUNCH(c, stk, VLA_K_OTHER, vla::bf16_to_f32((const bf16_t*)src, c->h, n, c->compute));
+    PLAUNCH(c, stk, VLA_K_OTHER, vla::bf16_to_f32((const bf16_t*)src, ws.h, n, st));
   else
-    HIPTRY(hipMemcpyAsync(c->h, src, n * 4, hipMemcpyDeviceToDevice, c->compute));
+    HIPTRY(hipMemcpyAsync(ws.h, src, n * 4, hipMemcpyDeviceToDevice, st));
   return OK;
 }
 
@@ -473,11 +501,12 @@ Status llm_block_bf16(vla_ctx* c, const Stack::Block& w, int B, int L, bf16_t* k
   const vla_stack_cfg& k = s.c;
   const int M = B * L, d = k.d_model;
   hipStream_t st = c->compute;
-  PLAUNCH(c, VLA_STACK_LLM, VLA_K_NORM, vla::rmsnorm_bf16(c->h, w.n1g, k.norm_eps, (bf16_t*)c->x, M, d, st));
+  Workspace& ws = c->ws[VLA_STACK_LLM];
+  PLAUNCH(c, VLA_STACK_LLM, VLA_K_NORM, vla::rmsnorm_bf16(ws.h, w.n1g, k.norm_eps, (bf16_t*)ws.x, M, d, st));
   vla::QkvArgs qa{nullptr, k.use_rope ? c->rope_cos : nullptr, k.use_rope ? c->rope_sin : nullptr,
-                  (bf16_t*)c->q, kdst, vdst, (bf16_t*)c->vt, round_up(L, 64), L, k.n_heads, k.n_kv_heads,
+                  (bf16_t*)ws.q, kdst, vdst, (bf16_t*)ws.vt, round_up(L, 64), L, k.n_heads, k.n_kv_heads,
                   k.head_dim};
-  PLAUNCH(c, VLA_STACK_LLM, VLA_K_QKV, vla::gemm_bf16_qkv((const bf16_t*)c->x, d, (const bf16_t*)w.w_qkv, d, qa, M, s.qkv_n, d, st));
+  PLAUNCH(c, VLA_STACK_LLM, VLA_K_QKV, vla::gemm_bf16_qkv((const bf16_t*)ws.x, d, Stack::packed(w.w_qkv, s.qkv_n), qa, M, s.qkv_n, d, st));
   return OK;
 }
 
@@ -486,15 +515,15 @@ Status llm_block_bf16_rest(vla_ctx* c, const Stack::Block& w, int B, int L, cons
   const vla_stack_cfg& k = s.c;
   const int M = B * L, d = k.d_model;
   hipStream_t st = c->compute;
-  PLAUNCH(c, VLA_STACK_LLM, VLA_K_ATTN, vla::attention_bf16((const bf16_t*)c->q, kdst, (const bf16_t*)c->vt, round_up(L, 64), (bf16_t*)c->o, B,
+  Workspace& ws = c->ws[VLA_STACK_LLM];
+  PLAUNCH(c, VLA_STACK_LLM, VLA_K_ATTN, vla::attention_bf16((const bf16_t*)ws.q, kdst, (const bf16_t*)ws.vt, round_up(L, 64), (bf16_t*)ws.o, B,
                            k.n_heads, k.n_kv_heads, L, k.head_dim, k.causal != 0, st));
-  PLAUNCH(c, VLA_STACK_LLM, VLA_K_OPROJ, vla::gemm_bf16_residual((const bf16_t*)c->o, s.hd, (const bf16_t*)w.w_o, s.hd, c->h, d, nullptr, M, d, s.hd,
-                               st));
-  PLAUNCH(c, VLA_STACK_LLM, VLA_K_NORM, vla::rmsnorm_bf16(c->h, w.n2g, k.norm_eps, (bf16_t*)c->x, M, d, st));
-  PLAUNCH(c, VLA_STACK_LLM, VLA_K_MLP_UP, vla::gemm_bf16_swiglu((const bf16_t*)c->x, d, (const bf16_t*)w.w_up, d, (bf16_t*)c->act, s.f_pad, M,
-                             2 * s.f_pad, d, st));
-  PLAUNCH(c, VLA_STACK_LLM, VLA_K_MLP_DOWN, vla::gemm_bf16_residual((const bf16_t*)c->act, s.f_pad, (const bf16_t*)w.w_down, s.f_pad, c->h, d, nullptr, M,
-                               d, s.f_pad, st));
+  PLAUNCH(c, VLA_STACK_LLM, VLA_K_OPROJ, vla::gemm_bf16_residual((const bf16_t*)ws.o, s.hd, Stack::packed(w.w_o, d), ws.h, d, nullptr, M, d, s.hd, st));
+  PLAUNCH(c, VLA_STACK_LLM, VLA_K_NORM, vla::rmsnorm_bf16(ws.h, w.n2g, k.norm_eps, (bf16_t*)ws.x, M, d, st));
+  PLAUNCH(c, VLA_STACK_LLM, VLA_K_MLP_UP, vla::gemm_bf16_swiglu((const bf16_t*)ws.x, d, Stack::packed(w.w_up, 2 * s.f_pad), (bf16_t*)ws.act, s.f_pad,
+                                                      M, 2 * s.f_pad, d, st));
+  PLAUNCH(c, VLA_STACK_LLM, VLA_K_MLP_DOWN, vla::gemm_bf16_residual((const bf16_t*)ws.act, s.f_pad, Stack::packed(w.w_down, d), ws.h, d, nullptr,
+                                                          M, d, s.f_pad, st));
   return OK;
 }
 
@@ -503,11 +532,12 @@ Status llm_block_f32(vla_ctx* c, const Stack::Block& w, int B, int L, float* kds
   const vla_stack_cfg& k = s.c;
   const int M = B * L, d = k.d_model;
   hipStream_t st = c->compute;
-  float* x = (float*)c->x;
-  PLAUNCH(c, VLA_STACK_LLM, VLA_K_NORM, vla::rmsnorm_f32(c->h, w.n1g, k.norm_eps, x, M, d, st));
-  PLAUNCH(c, VLA_STACK_LLM, VLA_K_QKV, vla::gemm_f32(x, d, (const float*)w.w_qkv, d, c->qkv_raw, s.qkv_n, nullptr, 0, M, s.qkv_n, d, st));
-  PLAUNCH(c, VLA_STACK_LLM, VLA_K_QKV, vla::qkv_split_f32(c->qkv_raw, k.use_rope ? c->rope_cos : nullptr, k.use_rope ? c->rope_sin : nullptr,
-                          (float*)c->q, kdst, vdst, nullptr, 0, B, L, k.n_heads, k.n_kv_heads, k.head_dim, st));
+  Workspace& ws = c->ws[VLA_STACK_LLM];
+  float* x = (float*)ws.x;
+  PLAUNCH(c, VLA_STACK_LLM, VLA_K_NORM, vla::rmsnorm_f32(ws.h, w.n1g, k.norm_eps, x, M, d, st));
+  PLAUNCH(c, VLA_STACK_LLM, VLA_K_QKV, vla::gemm_f32(x, d, (const float*)w.w_qkv, d, ws.qkv_raw, s.qkv_n, nullptr, 0, M, s.qkv_n, d, st));
+  PLAUNCH(c, VLA_STACK_LLM, VLA_K_QKV, vla::qkv_split_f32(ws.qkv_raw, k.use_rope ? c->rope_cos : nullptr, k.use_rope ? c->rope_sin : nullptr,
+                          (float*)ws.q, kdst, vdst, nullptr, 0, B, L, k.n_heads, k.n_kv_heads, k.head_dim, st));
   return OK;
 }
 
@@ -516,16 +546,17 @@ Status llm_block_f32_rest(vla_ctx* c, const Stack::Block& w, int B, int L, const
   const vla_stack_cfg& k = s.c;
   const int M = B * L, d = k.d_model, F = k.d_ff;
   hipStream_t st = c->compute;
-  float* x = (float*)c->x;
-  float* gu = (float*)c->act;
+  Workspace& ws = c->ws[VLA_STACK_LLM];
+  float* x = (float*)ws.x;
+  float* gu = (float*)ws.act;
   float* a = gu + (size_t)M * 2 * F;
-  PLAUNCH(c, VLA_STACK_LLM, VLA_K_ATTN, vla::attention_f32((const float*)c->q, kdst, vdst, (float*)c->o, B, k.n_heads, k.n_kv_heads, L, k.head_dim,
+  PLAUNCH(c, VLA_STACK_LLM, VLA_K_ATTN, vla::attention_f32((const float*)ws.q, kdst, vdst, (float*)ws.o, B, k.n_heads, k.n_kv_heads, L, k.head_dim,
                           k.causal != 0, st));
-  PLAUNCH(c, VLA_STACK_LLM, VLA_K_OPROJ, vla::gemm_f32((const float*)c->o, s.hd, (const float*)w.w_o, s.hd, c->h, d, nullptr, 1, M, d, s.hd, st));
-  PLAUNCH(c, VLA_STACK_LLM, VLA_K_NORM, vla::rmsnorm_f32(c->h, w.n2g, k.norm_eps, x, M, d, st));
+  PLAUNCH(c, VLA_STACK_LLM, VLA_K_OPROJ, vla::gemm_f32((const float*)ws.o, s.hd, (const float*)w.w_o, s.hd, ws.h, d, nullptr, 1, M, d, s.hd, st));
+  PLAUNCH(c, VLA_STACK_LLM, VLA_K_NORM, vla::rmsnorm_f32(ws.h, w.n2g, k.norm_eps, x, M, d, st));
   PLAUNCH(c, VLA_STACK_LLM, VLA_K_MLP_UP, vla::gemm_f32(x, d, (const float*)w.w_up, d, gu, 2 * F, nullptr, 0, M, 2 * F, d, st));
   PLAUNCH(c, VLA_STACK_LLM, VLA_K_MLP_UP, vla::swiglu_f32(gu, a, M, F, st));
-  PLAUNCH(c, VLA_STACK_LLM, VLA_K_MLP_DOWN, vla::gemm_f32(a, F, (const float*)w.w_down, F, c->h, d, nullptr, 1, M, d, F, st));
+  PLAUNCH(c, VLA_STACK_LLM, VLA_K_MLP_DOWN, vla::gemm_f32(a, F, (const float*)w.w_down, F, ws.h, d, nullptr, 1, M, d, F, st));
   return OK;
 }
 
@@ -533,36 +564,38 @@ Status enc_block(vla_ctx* c, const Stack::Block& w, int n_img, int L) {
   const Stack& s = c->enc;
   const vla_stack_cfg& k = s.c;
   const int M = n_img * L, d = k.d_model;
-  hipStream_t st = c->compute;
+  hipStream_t st = c->encs;
+  Workspace& ws = c->ws[VLA_STACK_ENC];
   if (s.bf16()) {
-    bf16_t* x = (bf16_t*)c->x;
-    PLAUNCH(c, VLA_STACK_ENC, VLA_K_NORM, vla::layernorm_bf16(c->h, w.n1g, w.n1b, k.norm_eps, x, M, d, st));
-    vla::QkvArgs qa{w.b_qkv, nullptr, nullptr, (bf16_t*)c->q, (bf16_t*)c->ek, (bf16_t*)c->ev, (bf16_t*)c->vt,
+    bf16_t* x = (bf16_t*)ws.x;
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_NORM, vla::layernorm_bf16(ws.h, w.n1g, w.n1b, k.norm_eps, x, M, d, st));
+    vla::QkvArgs qa{w.b_qkv, nullptr, nullptr, (bf16_t*)ws.q, (bf16_t*)ws.ek, (bf16_t*)ws.ev, (bf16_t*)ws.vt,
                     round_up(L, 64), L, k.n_heads, k.n_kv_heads, k.head_dim};
-    PLAUNCH(c, VLA_STACK_ENC, VLA_K_QKV, vla::gemm_bf16_qkv(x, d, (const bf16_t*)w.w_qkv, d, qa, M, s.qkv_n, d, st));
-    PLAUNCH(c, VLA_STACK_ENC, VLA_K_ATTN, vla::attention_bf16((const bf16_t*)c->q, (const bf16_t*)c->ek, (const bf16_t*)c->vt, round_up(L, 64),
-                             (bf16_t*)c->o, n_img, k.n_heads, k.n_kv_heads, L, k.head_dim, false, st));
-    PLAUNCH(c, VLA_STACK_ENC, VLA_K_OPROJ, vla::gemm_bf16_residual((const bf16_t*)c->o, s.hd, (const bf16_t*)w.w_o, s.hd, c->h, d, w.b_o, M, d, s.hd,
-                                 st));
-    PLAUNCH(c, VLA_STACK_ENC, VLA_K_NORM, vla::layernorm_bf16(c->h, w.n2g, w.n2b, k.norm_eps, x, M, d, st));
-    PLAUNCH(c, VLA_STACK_ENC, VLA_K_MLP_UP, vla::gemm_bf16_gelu(x, d, (const bf16_t*)w.w_up, d, (bf16_t*)c->act, s.f_pad, w.b_up, M, s.f_pad, d, st));
-    PLAUNCH(c, VLA_STACK_ENC, VLA_K_MLP_DOWN, vla::gemm_bf16_residual((const bf16_t*)c->act, s.f_pad, (const bf16_t*)w.w_down, s.f_pad, c->h, d, w.b_down,
-                                 M, d, s.f_pad, st));
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_QKV, vla::gemm_bf16_qkv(x, d, Stack::packed(w.w_qkv, s.qkv_n), qa, M, s.qkv_n, d, st));
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_ATTN, vla::attention_bf16((const bf16_t*)ws.q, (const bf16_t*)ws.ek, (const bf16_t*)ws.vt, round_up(L, 64),
+                             (bf16_t*)ws.o, n_img, k.n_heads, k.n_kv_heads, L, k.head_dim, false, st));
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_OPROJ, vla::gemm_bf16_residual((const bf16_t*)ws.o, s.hd, Stack::packed(w.w_o, d), ws.h, d, w.b_o, M, d,
+                                                            s.hd, st));
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_NORM, vla::layernorm_bf16(ws.h, w.n2g, w.n2b, k.norm_eps, x, M, d, st));
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_MLP_UP, vla::gemm_bf16_gelu(x, d, Stack::packed(w.w_up, s.f_pad), (bf16_t*)ws.act, s.f_pad, w.b_up, M, s.f_pad,
+                                                       d, st));
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_MLP_DOWN, vla::gemm_bf16_residual((const bf16_t*)ws.act, s.f_pad, Stack::packed(w.w_down, d), ws.h, d,
+                                                               w.b_down, M, d, s.f_pad, st));
   } else {
-    float* x = (float*)c->x;
+    float* x = (float*)ws.x;
     const int F = k.d_ff;
-    PLAUNCH(c, VLA_STACK_ENC, VLA_K_NORM, vla::layernorm_f32(c->h, w.n1g, w.n1b, k.norm_eps, x, M, d, st));
-    PLAUNCH(c, VLA_STACK_ENC, VLA_K_QKV, vla::gemm_f32(x, d, (const float*)w.w_qkv, d, c->qkv_raw, s.qkv_n, w.b_qkv, 0, M, s.qkv_n, d, st));
-    PLAUNCH(c, VLA_STACK_ENC, VLA_K_QKV, vla::qkv_split_f32(c->qkv_raw, nullptr, nullptr, (float*)c->q, (float*)c->ek, (float*)c->ev, nullptr, 0,
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_NORM, vla::layernorm_f32(ws.h, w.n1g, w.n1b, k.norm_eps, x, M, d, st));
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_QKV, vla::gemm_f32(x, d, (const float*)w.w_qkv, d, ws.qkv_raw, s.qkv_n, w.b_qkv, 0, M, s.qkv_n, d, st));
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_QKV, vla::qkv_split_f32(ws.qkv_raw, nullptr, nullptr, (float*)ws.q, (float*)ws.ek, (float*)ws.ev, nullptr, 0,
                             n_img, L, k.n_heads, k.n_kv_heads, k.head_dim, st));
-    PLAUNCH(c, VLA_STACK_ENC, VLA_K_ATTN, vla::attention_f32((const float*)c->q, (const float*)c->ek, (const float*)c->ev, (float*)c->o, n_img,
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_ATTN, vla::attention_f32((const float*)ws.q, (const float*)ws.ek, (const float*)ws.ev, (float*)ws.o, n_img,
                             k.n_heads, k.n_kv_heads, L, k.head_dim, false, st));
-    PLAUNCH(c, VLA_STACK_ENC, VLA_K_OPROJ, vla::gemm_f32((const float*)c->o, s.hd, (const float*)w.w_o, s.hd, c->h, d, w.b_o, 1, M, d, s.hd, st));
-    PLAUNCH(c, VLA_STACK_ENC, VLA_K_NORM, vla::layernorm_f32(c->h, w.n2g, w.n2b, k.norm_eps, x, M, d, st));
-    float* a = (float*)c->act;
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_OPROJ, vla::gemm_f32((const float*)ws.o, s.hd, (const float*)w.w_o, s.hd, ws.h, d, w.b_o, 1, M, d, s.hd, st));
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_NORM, vla::layernorm_f32(ws.h, w.n2g, w.n2b, k.norm_eps, x, M, d, st));
+    float* a = (float*)ws.act;
     PLAUNCH(c, VLA_STACK_ENC, VLA_K_MLP_UP, vla::gemm_f32(x, d, (const float*)w.w_up, d, a, F, w.b_up, 0, M, F, d, st));
     PLAUNCH(c, VLA_STACK_ENC, VLA_K_MLP_UP, vla::gelu_f32(a, (size_t)M * F, st));
-    PLAUNCH(c, VLA_STACK_ENC, VLA_K_MLP_DOWN, vla::gemm_f32(a, F, (const float*)w.w_down, F, c->h, d, w.b_down, 1, M, d, F, st));
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_MLP_DOWN, vla::gemm_f32(a, F, (const float*)w.w_down, F, ws.h, d, w.b_down, 1, M, d, F, st));
   }
   return OK;
 }
@@ -617,8 +650,16 @@ Status run_blocks(vla_ctx* c, uint64_t frame_id, const void* tokens, vla_dtype i
   sl.used = true;
   out->frame_id = frame_id;
 
+  // the tokens may be the output of an encoder run enqueued before this call
+  const bool split = c->encs != c->compute;
+  if (split && c->enc_recorded) HIPTRY(hipStreamWaitEvent(c->compute, c->ev_enc_done, 0));
   HIPTRY(hipEventRecord(sl.ev_start, c->compute));
   if ((st = intake(c, VLA_STACK_LLM, in_dt, tokens, n)).code) return st;
+  if (split) {
+    HIPTRY(hipEventRecord(c->ev_intake, c->compute));
+    c->intake_recorded = true;
+  }
+  float* h = c->ws[VLA_STACK_LLM].h;
   for (int l = k0; l < k1; ++l) {
     const Stack::Block& w = s.blocks[l];
     char* kvl = (char*)sl.kv + (size_t)(l - k0) * layer_elems * s.esz;
@@ -642,9 +683,9 @@ Status run_blocks(vla_ctx* c, uint64_t frame_id, const void* tokens, vla_dtype i
     if (st.code) return st;
   }
   if (out->out_dtype == VLA_BF16)
-    PLAUNCH(c, VLA_STACK_LLM, VLA_K_OTHER, vla::f32_to_bf16(c->h, (bf16_t*)sl.hid, n, c->compute));
+    PLAUNCH(c, VLA_STACK_LLM, VLA_K_OTHER, vla::f32_to_bf16(h, (bf16_t*)sl.hid, n, c->compute));
   else
-    HIPTRY(hipMemcpyAsync(sl.hid, c->h, n * 4, hipMemcpyDeviceToDevice, c->compute));
+    HIPTRY(hipMemcpyAsync(sl.hid, h, n * 4, hipMemcpyDeviceToDevice, c->compute));
   HIPTRY(hipEventRecord(sl.ev_done, c->compute));
   HIPTRY(hipStreamWaitEvent(c->copy, sl.ev_done, 0));
   HIPTRY(hipEventRecord(sl.ev_hid, c->copy));
@@ -671,10 +712,18 @@ Status run_encoder(vla_ctx* c, const void* patches, int n_img, int L, void* out_
   if (st.code) return st;
   for (int l = 0; l < s.c.n_blocks; ++l)
     if ((st = enc_block(c, s.blocks[l], n_img, L)).code) return st;
+  // out_dev may still be the input of the latest prefix
+  const bool split = c->encs != c->compute;
+  if (split && c->intake_recorded) HIPTRY(hipStreamWaitEvent(c->encs, c->ev_intake, 0));
+  const float* h = c->ws[VLA_STACK_ENC].h;
   if (s.bf16())
-    PLAUNCH(c, VLA_STACK_ENC, VLA_K_OTHER, vla::f32_to_bf16(c->h, (bf16_t*)out_dev, n, c->compute));
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_OTHER, vla::f32_to_bf16(h, (bf16_t*)out_dev, n, c->encs));
   else
-    HIPTRY(hipMemcpyAsync(out_dev, c->h, n * 4, hipMemcpyDeviceToDevice, c->compute));
+    HIPTRY(hipMemcpyAsync(out_dev, h, n * 4, hipMemcpyDeviceToDevice, c->encs));
+  if (split) {
+    HIPTRY(hipEventRecord(c->ev_enc_done, c->encs));
+    c->enc_recorded = true;
+  }
   return OK;
 }
 
@@ -704,7 +753,7 @@ Status build_rope(vla_ctx* c) {
 }
 
 Status create(const vla_stack_cfg* llm, const vla_stack_cfg* enc, int device, void* arena, size_t arena_bytes,
-              void* compute, void* copy, vla_ctx** out) {
+              void* compute, void* encoder, void* copy, vla_ctx** out) {
   if (!out) return fail(VLA_ERR_INVALID_ARG, "NULL out");
   *out = nullptr;
   if (!llm && !enc) return fail(VLA_ERR_INVALID_ARG, "need at least one stack");
@@ -734,12 +783,16 @@ Status create(const vla_stack_cfg* llm, const vla_stack_cfg* enc, int device, vo
     HIPTRY(hipStreamCreateWithFlags(&c->compute, hipStreamNonBlocking));
     c->own_compute = true;
   }
+  // no encoder stream of its own: the encoder runs on the compute stream
+  c->encs = encoder ? (hipStream_t)encoder : c->compute;
   if (copy) {
     c->copy = (hipStream_t)copy;
   } else {
     HIPTRY(hipStreamCreateWithFlags(&c->copy, hipStreamNonBlocking));
     c->own_copy = true;
   }
+  HIPTRY(hipEventCreateWithFlags(&c->ev_enc_done, hipEventDisableTiming));
+  HIPTRY(hipEventCreateWithFlags(&c->ev_intake, hipEventDisableTiming));
   int nkv = c->llm.present ? c->llm.c.n_blocks : 0;
   for (auto& sl : c->slots) {
     HIPTRY(hipEventCreate(&sl.ev_start));
@@ -759,6 +812,7 @@ void destroy(vla_ctx* c) {
   if (!c) return;
   (void)hipSetDevice(c->device);
   if (c->compute) (void)hipStreamSynchronize(c->compute);
+  if (c->encs && c->encs != c->compute) (void)hipStreamSynchronize(c->encs);
   if (c->copy) (void)hipStreamSynchronize(c->copy);
   for (auto& sl : c->slots) {
     for (hipEvent_t e : {sl.ev_start, sl.ev_done, sl.ev_hid, sl.ev_copied})
@@ -767,6 +821,8 @@ void destroy(vla_ctx* c) {
       if (e) (void)hipEventDestroy(e);
   }
   for (hipEvent_t e : c->prof_pool) (void)hipEventDestroy(e);
+  for (hipEvent_t e : {c->ev_enc_done, c->ev_intake})
+    if (e) (void)hipEventDestroy(e);
   if (c->own_compute) (void)hipStreamDestroy(c->compute);
   if (c->own_copy) (void)hipStreamDestroy(c->copy);
   delete c;
@@ -805,9 +861,11 @@ vla_status vla_query_sizes(const vla_stack_cfg* llm, const vla_stack_cfg* enc, i
 }
 
 vla_status vla_create(const vla_stack_cfg* llm, const vla_stack_cfg* enc, int device, void* dev_arena,
-                      size_t arena_bytes, void* compute_stream, void* copy_stream, vla_ctx** out) {
+                      size_t arena_bytes, void* compute_stream, void* encoder_stream, void* copy_stream,
+                      vla_ctx** out) {
   try {
-    return finish(nullptr, create(llm, enc, device, dev_arena, arena_bytes, compute_stream, copy_stream, out));
+    return finish(nullptr, create(llm, enc, device, dev_arena, arena_bytes, compute_stream, encoder_stream,
+                                  copy_stream, out));
   } catch (const std::bad_alloc&) {
     return finish(nullptr, fail(VLA_ERR_OOM, "host allocation failed"));
   } catch (...) {
@@ -825,8 +883,8 @@ vla_status vla_load_block_weights(vla_ctx* ctx, vla_stack which, int block, cons
     if (block < 0 || block >= s.c.n_blocks)
       return finish(ctx, fail(VLA_ERR_SHAPE, "block %d outside [0, %d)", block, s.c.n_blocks));
     if (hipSetDevice(ctx->device) != hipSuccess) return finish(ctx, fail(VLA_ERR_HIP, "hipSetDevice failed"));
-    // weights may still be read by in-flight work on the compute stream
-    if (hipStreamSynchronize(ctx->compute) != hipSuccess)
+    // weights may still be read by in-flight work of either stack
+    if (hipStreamSynchronize(ctx->compute) != hipSuccess || hipStreamSynchronize(ctx->encs) != hipSuccess)
       return finish(ctx, fail(VLA_ERR_HIP, "hipStreamSynchronize failed"));
     return finish(ctx, load_block(ctx, s, block, w));
   } catch (const std::bad_alloc&) {

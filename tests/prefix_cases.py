@@ -97,7 +97,7 @@ class EncCase:
         dt = torch.bfloat16 if self.wl.dtype == "bf16" else torch.float32
         out = torch.empty((self.n_img, self.L, self.s.d_model), dtype=dt, device="cuda")
         self.ctx.vla_run_encoder(frame, p, self.n_img, self.L, out)
-        self.ctx.compute_stream.synchronize()
+        self.ctx.encoder_stream.synchronize()
         return out.cpu()
 
     def oracle(self, p):

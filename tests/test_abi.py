@@ -97,9 +97,10 @@ def test_create_rejects_small_arena_before_touching_the_gpu():
     c = _cfg("tiny")
     need = vb.vla_query_sizes(c, None, 1, 128, 2)[0]
     h = ctypes.c_void_p()
-    rc = vb.lib().vla_create(ctypes.byref(c), None, 0, ctypes.c_void_p(4096), need - 1, None, None, ctypes.byref(h))
+    rc = vb.lib().vla_create(ctypes.byref(c), None, 0, ctypes.c_void_p(4096), need - 1, None, None, None,
+                             ctypes.byref(h))
     assert vb.STATUS[rc] == "VLA_ERR_OOM" and not h.value
-    rc = vb.lib().vla_create(ctypes.byref(c), None, 0, None, need, None, None, ctypes.byref(h))
+    rc = vb.lib().vla_create(ctypes.byref(c), None, 0, None, need, None, None, None, ctypes.byref(h))
     assert vb.STATUS[rc] == "VLA_ERR_INVALID_ARG"
 
 

@@ -101,7 +101,7 @@ def test_fp32_encoder():
     p = synth.normal_f32(synth.seed_of("encp32"), (3, 77, 128))
     out = torch.empty((3, 77, 128), dtype=torch.float32, device="cuda")
     ctx.vla_run_encoder(0, p, 3, 77, out)
-    ctx.compute_stream.synchronize()
+    ctx.encoder_stream.synchronize()
     import oracle
     ref = oracle.run_encoder(p, lambda l: W[l], s)
     e = rel_l2(out.cpu().numpy(), ref)
@@ -157,6 +157,66 @@ def test_back_to_back_frames_and_determinism():
     assert np.array_equal(bits(again.hidden), bits(bnds[2].hidden))
     assert np.array_equal(bits(again.kv), bits(bnds[2].kv))
     c.close()
+
+
+def test_encoder_feeds_prefix_across_streams():
+    """The encoder of frame f+1 overlaps the prefix of frame f on its own
+    stream.  Frames whose prefix reads the encoder's output, all through one
+    output buffer, must each match a strictly serial run bit for bit: the
+    prefix waits for its encoder, and the next encoder's output write waits
+    for the prefix's intake."""
+    import dataclasses
+    import torch
+    import synth
+    from paper_2608_14586_amd import binding as vb
+    ew, lw = synth.CONFIGS["vit_l"], synth.CONFIGS["small_llm"]
+    es = dataclasses.replace(ew.enc, n_blocks=2, d_model=256, n_heads=4, n_kv_heads=4, head_dim=64, d_ff=512)
+    ls = dataclasses.replace(lw.llm, n_blocks=2, d_model=256, n_heads=4, n_kv_heads=2, head_dim=64, d_ff=688)
+    ew, lw = dataclasses.replace(ew, enc=es), dataclasses.replace(lw, llm=ls)
+    EW = [synth.vit_block_weights(ew, l, perturbed=True) for l in range(2)]
+    LW = [synth.llm_block_weights(lw, l, perturbed=True) for l in range(2)]
+    n_img, L_img, nf = 2, 96, 5
+    ecfg = vb.stack_cfg(es, "bf16", max_tokens=L_img, max_batch=n_img)
+    lcfg = vb.stack_cfg(ls, "bf16", max_tokens=L_img, max_batch=n_img, n_blocks=2)
+    pats = [synth.patches(ew, frame=f, n_img=n_img, L_img=L_img) for f in range(nf)]
+
+    def load(ctx):
+        for l in range(2):
+            if ctx.enc is not None:
+                ctx.vla_load_block_weights(vb.VLA_STACK_ENC, l, EW[l])
+            if ctx.llm is not None:
+                ctx.vla_load_block_weights(vb.VLA_STACK_LLM, l, LW[l])
+
+    def bnd():
+        return vb.Boundary(n_img, L_img, 256, 2, 2, 64)
+
+    bits = lambda t: t.view(torch.int16).numpy()
+    # pipelined: one context, one encoder output buffer for every frame
+    ctx = vb.Context(llm=lcfg, enc=ecfg, encoder_stream=torch.cuda.Stream())
+    load(ctx)
+    enc_out = torch.empty((n_img, L_img, 256), dtype=torch.bfloat16, device="cuda")
+    got = [bnd() for _ in range(nf)]
+    for f in range(nf):
+        ctx.vla_run_encoder(f, pats[f], n_img, L_img, enc_out)
+        ctx.vla_run_prefix(f, enc_out, n_img, L_img, 2, got[f])
+    for f in range(nf):
+        ctx.vla_wait_boundary(f, 60000)
+    ctx.vla_destroy()
+    # serial reference: separate contexts, every step synchronised
+    ectx, lctx = vb.Context(enc=ecfg), vb.Context(llm=lcfg)
+    load(ectx)
+    load(lctx)
+    for f in range(nf):
+        e = torch.empty((n_img, L_img, 256), dtype=torch.bfloat16, device="cuda")
+        ectx.vla_run_encoder(f, pats[f], n_img, L_img, e)
+        ectx.encoder_stream.synchronize()
+        ref = bnd()
+        lctx.vla_run_prefix(f, e, n_img, L_img, 2, ref)
+        lctx.vla_wait_boundary(f, 60000)
+        assert np.array_equal(bits(got[f].hidden), bits(ref.hidden)), "frame %d boundary" % f
+        assert np.array_equal(bits(got[f].kv), bits(ref.kv)), "frame %d kv" % f
+    ectx.vla_destroy()
+    lctx.vla_destroy()
 
 
 def test_k0_returns_input():
