@@ -35,13 +35,14 @@ __device__ __forceinline__ int acc_row(int r, int lane) { return (r >> 2) * 8 + 
 // ------------------------------------------------------------------ epilogues
 //
 // Two epilogue paths.
-//  * Direct: every lane writes its accumulators straight to memory (2- or
-//    4-byte stores); used by the 256x256 tiles and the fp32-out operator.
-//  * Through LDS (128 x 128 tiles): once the K loop is done the 64 KB of slab
-//    buffers are free, so the waves park the fp32 tile in LDS row-major and
-//    the whole workgroup then walks it in 16-byte chunks: coalesced residual
-//    read-modify-writes, 16-byte bf16 stores, and the rotary embedding plus
-//    the q / K / V / V^T scatter done row-contiguously per head.
+//  * Direct: every lane writes its accumulators straight to memory (4-byte
+//    stores); used by the fp32-out operator.
+//  * Through LDS: once the K loop is done the slab buffers are free, so the
+//    waves park the fp32 tile in LDS row-major (128 x 128 tiles at once,
+//    256 x 256 tiles one 128-row half at a time) and 256-thread groups then
+//    walk it in 16-byte chunks: coalesced residual read-modify-writes,
+//    16-byte bf16 stores, and the rotary embedding plus the q / K / V / V^T
+//    scatter done row-contiguously per head.
 // drain() is the second half of the LDS path: T is the tile [128][128] fp32,
 // (m0, n0) its origin, tid the thread index in the 256-thread workgroup.
 
@@ -485,6 +486,27 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __
           T[(wm * WM + tm * 32 + acc_row(r, lane)) * ET + wn * WN + tn * 32 + (lane & 31)] = acc.v[tm][tn][r];
     __syncthreads();
     epi.template drain<ET, ET>(T, m0, n0, tid);
+  } else if constexpr (Epi::kViaLds && NW == 8 && BM == 2 * WM) {
+    // 256 x 256 tiles: park one wave row (BM/2 x BN fp32, the size of the slab
+    // buffers) at a time; two 256-thread groups drain BM/4 rows each
+    static_assert((BM / 2) * BN * 4 <= sizeof(smem), "half tile must fit the slab buffers");
+    float* T = (float*)smem;
+    const int grp = tid >> 8, t = tid & 255;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      __syncthreads();
+      if (wm == h) {
+#pragma unroll
+        for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+          for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+              T[(tm * 32 + acc_row(r, lane)) * BN + wn * WN + tn * 32 + (lane & 31)] = acc.v[tm][tn][r];
+      }
+      __syncthreads();
+      epi.template drain<BM / 4, BN>(T + grp * (BM / 4) * BN, m0 + h * (BM / 2) + grp * (BM / 4), n0, t);
+    }
   } else {
     epi(acc, m0 + wm * WM, n0 + wn * WN, lane);
   }
