@@ -38,15 +38,13 @@ __device__ __forceinline__ int acc_row(int r, int lane) { return (r >> 2) * 8 + 
 //  * Direct: every lane writes its accumulators straight to memory (4-byte
 //    stores); used by the fp32-out operator.
 //  * Through LDS: once the K loop is done the slab buffers are free, so the
-//    waves park the fp32 tile in LDS row-major (128 x 128 tiles at once,
-//    256 x 256 tiles one 128-row half at a time) and 256-thread groups then
-//    walk it in 16-byte chunks: coalesced residual read-modify-writes,
-//    16-byte bf16 stores, and the rotary embedding plus the q / K / V / V^T
-//    scatter done row-contiguously per head.
+//    waves park the fp32 tile in LDS row-major, one wave row (half the tile's
+//    rows) at a time, and 256-thread groups then walk it in 16-byte chunks:
+//    coalesced residual read-modify-writes, 16-byte bf16 stores, and the
+//    rotary embedding plus the q / K / V / V^T scatter done row-contiguously
+//    per head.
 // drain() is the second half of the LDS path: T is the tile [128][128] fp32,
 // (m0, n0) its origin, tid the thread index in the 256-thread workgroup.
-
-constexpr int ET = 128;  // LDS-epilogue tile edge
 
 __device__ __forceinline__ u32x4 pack8(const f32x4& a, const f32x4& b) {
   return u32x4{pack_bf2(a[0], a[1]), pack_bf2(a[2], a[3]), pack_bf2(b[0], b[1]), pack_bf2(b[2], b[3])};
@@ -391,12 +389,11 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __
       (void*)(A + (size_t)m0 * lda), (short)0, (int)((size_t)(M - m0) * lda * 2), 0x00020000);
   // W: row-major rows from n0 on, or the whole packed matrix (every block of
   // a tile lies inside it: the packing pads N to whole 256-row pairs)
-  const int ldw = W.ld, nblk = W.nblk, nb0 = n0 / SLAB_N, nkt = K / BK;
+  const int ldw = W.ld, nblk = W.nblk, nb0 = n0 / SLAB_N;
   const __amdgpu_buffer_rsrc_t rb =
       WT ? __builtin_amdgcn_make_buffer_rsrc((void*)W.p, (short)0, (int)((size_t)nblk * SLAB_N * K * 2), 0x00020000)
          : __builtin_amdgcn_make_buffer_rsrc((void*)(W.p + (size_t)n0 * ldw), (short)0,
                                              (int)((size_t)(N - n0) * ldw * 2), 0x00020000);
-  (void)nkt;
 
   // this lane's slot in each 1 KB load: row (lane / 8) of the 8-row group,
   // LDS chunk (lane % 8) holding global chunk (lane % 8) ^ key(tile row)
@@ -433,8 +430,9 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __
   const int a_row0 = (wm * WM + fi) * ROWB, b_row0 = BM * ROWB + (wn * WN + fi) * ROWB;
   const int key = (fi >> 1) & 7;
   bf16x8 fa[2][TM], fb[2][TN];
-  auto frags = [&](int buf, int ks, int slot) {
-    const char* base = smem + buf * (BM + BN) * ROWB;
+  // fragments of k16 step ks of slab s (buffer s & 1) into register slot `slot`
+  auto frags = [&](int s, int ks, int slot) {
+    const char* base = smem + (s & 1) * (BM + BN) * ROWB;
     const int off = (((2 * ks + fh) ^ key) << 4);
 #pragma unroll
     for (int tm = 0; tm < TM; ++tm) fa[slot][tm] = *(const bf16x8*)(base + a_row0 + tm * 32 * ROWB + off);
@@ -448,15 +446,14 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __
   __syncthreads();
   frags(0, 0, 0);
   for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    const bool last = kt + 1 == nk;
-    if (!last) issue((kt + 1) * BK, buf ^ 1);
+    // the other buffer was last read before the previous slab's barrier
+    if (kt + 1 < nk) issue((kt + 1) * BK, (kt + 1) & 1);
 #pragma unroll
     for (int ks = 0; ks < BK / 16; ++ks) {
       const int cur = ks & 1;
       // the next step's fragment reads stay ahead of this step's MFMAs (left
       // alone, the scheduler sinks each read onto its first use)
-      if (ks + 1 < BK / 16) frags(buf, ks + 1, cur ^ 1);
+      if (ks + 1 < BK / 16) frags(kt, ks + 1, cur ^ 1);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int tm = 0; tm < TM; ++tm)
@@ -465,31 +462,21 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __
           acc.v[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cur][tm], fb[cur][tn], acc.v[tm][tn], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
-    if (!last) {
-      __builtin_amdgcn_s_waitcnt(0);
+    if (kt + 1 < nk) {
+      // the next slab's loads; this wave's fragment reads are consumed
+      __builtin_amdgcn_s_waitcnt(0x0F70);
       __syncthreads();
-      frags(buf ^ 1, 0, 0);
+      frags(kt + 1, 0, 0);
     }
   }
+  __builtin_amdgcn_s_waitcnt(0);
 
-  if constexpr (Epi::kViaLds && BM == ET && BN == ET && NW == 4) {
-    // park the fp32 tile in the (now idle) slab buffers, then drain it
-    static_assert(ET * ET * 4 <= sizeof(smem), "tile must fit the slab buffers");
-    float* T = (float*)smem;
-    __syncthreads();
-#pragma unroll
-    for (int tm = 0; tm < TM; ++tm)
-#pragma unroll
-      for (int tn = 0; tn < TN; ++tn)
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-          T[(wm * WM + tm * 32 + acc_row(r, lane)) * ET + wn * WN + tn * 32 + (lane & 31)] = acc.v[tm][tn][r];
-    __syncthreads();
-    epi.template drain<ET, ET>(T, m0, n0, tid);
-  } else if constexpr (Epi::kViaLds && NW == 8 && BM == 2 * WM) {
-    // 256 x 256 tiles: park one wave row (BM/2 x BN fp32, the size of the slab
-    // buffers) at a time; two 256-thread groups drain BM/4 rows each
+  if constexpr (Epi::kViaLds) {
+    // Park one wave row (BM/2 x BN fp32) at a time in the idle slab buffers;
+    // 256-thread groups then drain BM/4 (8 waves) or BM/2 (4 waves) rows each.
+    static_assert(BM == 2 * WM, "two wave rows");
     static_assert((BM / 2) * BN * 4 <= sizeof(smem), "half tile must fit the slab buffers");
+    constexpr int GROUPS = NW / 4, RG = BM / 2 / GROUPS;
     float* T = (float*)smem;
     const int grp = tid >> 8, t = tid & 255;
 #pragma unroll
@@ -505,7 +492,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __
               T[(tm * 32 + acc_row(r, lane)) * BN + wn * WN + tn * 32 + (lane & 31)] = acc.v[tm][tn][r];
       }
       __syncthreads();
-      epi.template drain<BM / 4, BN>(T + grp * (BM / 4) * BN, m0 + h * (BM / 2) + grp * (BM / 4), n0, t);
+      epi.template drain<RG, BN>(T + grp * RG * BN, m0 + h * (BM / 2) + grp * RG, n0, t);
     }
   } else {
     epi(acc, m0 + wm * WM, n0 + wn * WN, lane);
