@@ -24,8 +24,10 @@ vla_status vla_op_gemm_bf16(const void *A, const void *W, float *C, int M, int N
 /* Scaled dot-product attention of the blocks: o[B][L][H*dh] (bf16) =
  * softmax(q k^T / sqrt(dh), causal mask if `causal`) v per (b, head), query
  * head h reading KV head h / (H / Hkv).  q[B][H][L][dh], k[B][Hkv][L][dh],
- * vt[B][Hkv][dh][ldvt] = V transposed (ldvt >= L, ldvt % 8 == 0), all bf16.
- * dh in {64, 128}. */
+ * vt[B][Hkv][dh][ldvt] = V transposed with the keys of every group of 16
+ * stored in the order [0-3, 8-11, 4-7, 12-15] (column c holds key c with
+ * bits 2 and 3 swapped), the order the MFMA consumes them; ldvt >= L rounded
+ * up to 16, ldvt % 16 == 0; columns of keys >= L are never used.  All bf16.  dh in {64, 128}. */
 vla_status vla_op_attention_bf16(const void *q, const void *k, const void *vt, int ldvt, void *o, int B, int H,
                                  int Hkv, int L, int dh, int causal, void *stream);
 

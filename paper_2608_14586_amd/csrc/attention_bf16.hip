@@ -11,9 +11,11 @@
 // running max/sum needs a single cross-half exchange (lane ^ 32) instead of a
 // 32-lane reduction, and the probabilities already sit where the PV product
 // O^T = V^T P^T wants its B operand: a lane's 8 bf16 values for keys
-// {8i + 4h + j : i in {2s, 2s+1}, j < 4} feed k-step s directly, and the A
-// fragment (V^T) is read from LDS in the same key order.  The softmax runs in
-// base 2 with log2(e)/sqrt(dh) folded into one FMA per score.
+// {16s + 4h + j, 16s + 8 + 4h + j : j < 4} feed k-step s directly.  V^T is
+// stored with the keys of every 16-key group in the order
+// [0-3, 8-11, 4-7, 12-15] (bits 2 and 3 of the key index swapped), so the A
+// fragment of those same keys is one contiguous 16-byte read.  The softmax
+// runs in base 2 with log2(e)/sqrt(dh) folded into one FMA per score.
 //
 // Causal tiles are masked per element only on the diagonal; a wave skips the
 // MFMAs of key tiles entirely beyond its last query.  Causal query blocks are
@@ -27,6 +29,9 @@ namespace vla {
 namespace {
 
 constexpr int BQ = 128, BKV = 64, PADK = 8, PADV = 8;
+
+// key index <-> stored V^T column: bits 2 and 3 swapped (an involution)
+__device__ __forceinline__ int swap23(int t) { return (t & ~12) | ((t & 4) << 1) | ((t & 8) >> 1); }
 
 template <int DH, bool CAUSAL>
 __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
@@ -88,16 +93,18 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict
     for (int c = 0; c < VCH; ++c) {
       int idx = tid + c * 256;
       int d = idx / (BKV / 8), cc = idx % (BKV / 8);
-      int key = kb + cc * 8;
-      const bf16_t* src = vh + (size_t)d * ldvt + key;
-      if (key + 8 <= L) {
+      int pos = kb + cc * 8;  // stored column; it holds key pos ^ swap23
+      const bf16_t* src = vh + (size_t)d * ldvt + pos;
+      if ((pos & ~15) + 16 <= L) {
         rv[c] = *(const u32x4*)src;
       } else {
+        // columns of keys >= L are zero (their probabilities are zero too)
         uint32_t w[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          uint32_t lo = (key + 2 * e < L) ? src[2 * e] : 0u;
-          uint32_t hi = (key + 2 * e + 1 < L) ? src[2 * e + 1] : 0u;
+          const int k0 = swap23(pos + 2 * e), k1 = swap23(pos + 2 * e + 1);
+          uint32_t lo = k0 < L ? src[2 * e] : 0u;
+          uint32_t hi = k1 < L ? src[2 * e + 1] : 0u;
           w[e] = lo | (hi << 16);
         }
         rv[c] = u32x4{w[0], w[1], w[2], w[3]};
@@ -211,17 +218,12 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict
             cv.u[3] = pack_bf2(s[t][(2 * ih + 1) * 4 + 2], s[t][(2 * ih + 1) * 4 + 3]);
             fp = cv.v;
           }
-          const int key0 = t * 32 + (2 * ih) * 8 + half * 4;
+          // stored columns 16 (2t + ih) + 8 half .. + 7 hold this lane's 8 keys
+          const int col = t * 32 + ih * 16 + half * 8;
 #pragma unroll
           for (int dt = 0; dt < ND; ++dt) {
-            const bf16_t* vrow = &sV[buf][(dt * 32 + li) * LDV];
-            union {
-              u32x2 w[2];
-              bf16x8 v;
-            } cvv;
-            cvv.w[0] = *(const u32x2*)(vrow + key0);
-            cvv.w[1] = *(const u32x2*)(vrow + key0 + 8);
-            acc_o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cvv.v, fp, acc_o[dt], 0, 0, 0);
+            const bf16x8 fv = *(const bf16x8*)&sV[buf][(dt * 32 + li) * LDV + col];
+            acc_o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fv, fp, acc_o[dt], 0, 0, 0);
           }
         }
     }
@@ -260,7 +262,8 @@ hipError_t launch_attn(const bf16_t* q, const bf16_t* k, const bf16_t* vt, int l
 hipError_t attention_bf16(const bf16_t* q, const bf16_t* k, const bf16_t* vt, int ldvt, bf16_t* o, int B, int H,
                           int Hkv, int L, int dh, bool causal, hipStream_t s) {
   if (B <= 0 || L <= 0 || H <= 0) return hipSuccess;
-  if (Hkv <= 0 || H % Hkv != 0 || ldvt < L || ldvt % 8 != 0) return hipErrorInvalidValue;
+  if (Hkv <= 0 || H % Hkv != 0 || ldvt < (L + 15) / 16 * 16 || ldvt % 16 != 0)
+    return hipErrorInvalidValue;
   if (dh == 128) return causal ? launch_attn<128, true>(q, k, vt, ldvt, o, B, H, Hkv, L, s)
                                : launch_attn<128, false>(q, k, vt, ldvt, o, B, H, Hkv, L, s);
   if (dh == 64) return causal ? launch_attn<64, true>(q, k, vt, ldvt, o, B, H, Hkv, L, s)

@@ -277,7 +277,7 @@ struct EpiQKV {
     const int dh = q.dh, L = q.L;
     // R tokens x NC/64 column groups x 4 chunks of 8 dims
     constexpr int CH = NC / 16;
-    static_assert((R * CH) % 256 == 0 && (R * 8) % 256 == 0, "tile must split evenly over the workgroup");
+    static_assert((R * CH) % 256 == 0 && (R * 4) % 256 == 0, "tile must split evenly over the workgroup");
 #pragma unroll 2
     for (int j = 0; j < R * CH / 256; ++j) {
       const int f = tid + 256 * j, row = f / CH, gsel = (f % CH) >> 2, w = (f & 3) * 8;
@@ -309,31 +309,36 @@ struct EpiQKV {
       *(u32x4*)(dst + d1) = pack8(x10, x11);
       *(u32x4*)(dst + d2) = pack8(x20, x21);
     }
-    // V^T: one (dim, 8 consecutive tokens) chunk per item
+    // V^T: one (dim, 16 consecutive tokens) chunk per item.  Inside every
+    // 16-token group the columns hold the keys in the order
+    // [0-3, 8-11, 4-7, 12-15] (bits 2 and 3 of the key index swapped), the
+    // order in which the attention's PV product consumes them.
     for (int gsel = 0; gsel < NC / 64; ++gsel) {
       int kind, head, r;
       const int p = n0 + gsel * 64;
       classify(p, kind, head, r);
       if (kind != 2) continue;
       const int c = r / 64;
-#pragma unroll 2
-      for (int j = 0; j < R * 8 / 256; ++j) {
-        const int f = tid + 256 * j, col = f & 63, t8 = (f >> 6) * 8;
-        const int gr0 = m0 + t8;
+#pragma unroll
+      for (int j = 0; j < R * 4 / 256; ++j) {
+        const int f = tid + 256 * j, col = f & 63, t16 = (f >> 6) * 16;
+        const int gr0 = m0 + t16;
         if (gr0 >= M) continue;
         const int d = (col < 32) ? c * 32 + col : dh / 2 + c * 32 + (col - 32);
         const float bcol = q.bias ? q.bias[p + col] : 0.f;
-        float v[8];
+        float v[16];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = T[(t8 + e) * NC + gsel * 64 + col] + bcol;
+        for (int e = 0; e < 16; ++e) v[e] = T[(t16 + e) * NC + gsel * 64 + col] + bcol;
         const int b0 = gr0 / L, pos0 = gr0 - b0 * L;
-        if (gr0 + 7 < M && pos0 + 7 < L && (pos0 & 7) == 0 && (q.ldvt & 7) == 0) {
-          u32x4 w4 = {pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]), pack_bf2(v[4], v[5]), pack_bf2(v[6], v[7])};
-          *(u32x4*)(q.vt + (((size_t)b0 * q.Hkv + head) * dh + d) * q.ldvt + pos0) = w4;
+        bf16_t* row = q.vt + (((size_t)b0 * q.Hkv + head) * dh + d) * q.ldvt;
+        if (gr0 + 15 < M && pos0 + 15 < L && (pos0 & 15) == 0 && (q.ldvt & 15) == 0) {
+          *(u32x4*)(row + pos0) = u32x4{pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]), pack_bf2(v[8], v[9]), pack_bf2(v[10], v[11])};
+          *(u32x4*)(row + pos0 + 8) = u32x4{pack_bf2(v[4], v[5]), pack_bf2(v[6], v[7]), pack_bf2(v[12], v[13]), pack_bf2(v[14], v[15])};
         } else {
           int bb = b0, pp = pos0;
-          for (int e = 0; e < 8 && gr0 + e < M; ++e) {
-            q.vt[(((size_t)bb * q.Hkv + head) * dh + d) * q.ldvt + pp] = f2bf(v[e]);
+          for (int e = 0; e < 16 && gr0 + e < M; ++e) {
+            const int sw = (pp & ~12) | ((pp & 4) << 1) | ((pp & 8) >> 1);
+            q.vt[(((size_t)bb * q.Hkv + head) * dh + d) * q.ldvt + sw] = f2bf(v[e]);
             if (++pp == L) {
               pp = 0;
               ++bb;

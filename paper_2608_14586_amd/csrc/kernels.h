@@ -56,7 +56,8 @@ struct QkvArgs {
   bf16_t* q;   // [B][H][L][dh]
   bf16_t* k;   // [B][Hkv][L][dh]
   bf16_t* v;   // [B][Hkv][L][dh]
-  bf16_t* vt;  // [B][Hkv][dh][ldvt] (V transposed, for the attention's PV product)
+  bf16_t* vt;  // [B][Hkv][dh][ldvt] (V transposed, keys of each 16-group in the order
+               // [0-3, 8-11, 4-7, 12-15], for the attention's PV product)
   int ldvt;
   int L, H, Hkv, dh;
 };
@@ -66,7 +67,8 @@ hipError_t gemm_bf16_qkv(const bf16_t* A, int lda, const WOperand& W, const QkvA
 // ---------------------------------------------------------- bf16 attention
 // o[B][L][H*dh] = softmax(q k^T / sqrt(dh) [+ causal mask]) v per (b, head);
 // query head h reads KV head h / (H / Hkv).  q [B][H][L][dh], k [B][Hkv][L][dh],
-// vt [B][Hkv][dh][ldvt].  dh in {64, 128}.
+// vt [B][Hkv][dh][ldvt] in the key order of QkvArgs::vt, ldvt % 16 == 0.
+// dh in {64, 128}.
 hipError_t attention_bf16(const bf16_t* q, const bf16_t* k, const bf16_t* vt, int ldvt, bf16_t* o, int B, int H,
                           int Hkv, int L, int dh, bool causal, hipStream_t s);
 

@@ -23,7 +23,7 @@ vla_status vla_op_gemm_bf16(const void* A, const void* W, float* C, int M, int N
 vla_status vla_op_attention_bf16(const void* q, const void* k, const void* vt, int ldvt, void* o, int B, int H,
                                  int Hkv, int L, int dh, int causal, void* stream) {
   if (!q || !k || !vt || !o || B < 0 || H <= 0 || Hkv <= 0 || L < 0) return VLA_ERR_INVALID_ARG;
-  if (H % Hkv || (dh != 64 && dh != 128) || ldvt < L || ldvt % 8) return VLA_ERR_UNSUPPORTED;
+  if (H % Hkv || (dh != 64 && dh != 128) || ldvt < (L + 15) / 16 * 16 || ldvt % 16) return VLA_ERR_UNSUPPORTED;
   return status_of(vla::attention_bf16((const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)vt, ldvt, (bf16_t*)o, B, H,
                                        Hkv, L, dh, causal != 0, (hipStream_t)stream));
 }

@@ -41,9 +41,12 @@ def test_attention_bf16(B, H, Hkv, L, dh, causal):
     q = synth.normal_bf16(synth.seed_of("q", *tag), (B, H, L, dh))
     k = synth.normal_bf16(synth.seed_of("k", *tag), (B, Hkv, L, dh))
     v = synth.normal_bf16(synth.seed_of("v", *tag), (B, Hkv, L, dh))
-    ldvt = (L + 63) // 64 * 64
+    ldvt = (L + 15) // 16 * 16 if L % 2 else (L + 63) // 64 * 64  # tight and padded strides
     vt = np.zeros((B, Hkv, dh, ldvt), np.uint16)
-    vt[..., :L] = v.transpose(0, 1, 3, 2)
+    # column c holds key c with bits 2 and 3 swapped (the layout the op documents)
+    cols = np.arange(L)
+    cols = (cols & ~12) | ((cols & 4) << 1) | ((cols & 8) >> 1)
+    vt[..., cols] = v.transpose(0, 1, 3, 2)
     o = torch.empty((B, L, H * dh), dtype=torch.bfloat16, device="cuda")
     vb.vla_op_attention_bf16(_dev_bf16(q), _dev_bf16(k), _dev_bf16(vt), ldvt, o, B, H, Hkv, L, dh, causal)
     torch.cuda.synchronize()
