@@ -12,6 +12,13 @@ seeded synthetic tensors already resident in HBM; weights are random-init
 N(0, 0.02) at the stated shapes.
 
 Prints ONE JSON line (rank 0, N = 1 only).
+
+``--pipeline`` measures the whole partitioned model instead (Eq. (6), Sec.
+IV-C): the GPU stage (encoder + decoder blocks [0, k)), the boundary handoff
+and the host suffix (blocks [k, 32) on the CPU), run frame by frame and as the
+cross-frame pipeline, for each k in ``--pipeline-ks``; it prints one JSON line
+of per-k stage times and stream intervals (T_G, T_X, T_C of Eq. (8)-(10), the
+serial frame time of Eq. (12), the pipelined interval against Eq. (13)).
 """
 from __future__ import annotations
 
@@ -122,6 +129,123 @@ def cpu_baseline(wl, k, budget_s=20.0):
             "blas": "numpy %s" % np.__version__}
 
 
+def pipeline_bench(args):
+    """Stage times and stream interval of the partitioned model per k."""
+    import numpy as np
+    import torch
+    import synth
+    from paper_2608_14586_amd import binding as vb
+
+    wl = synth.CONFIGS["sweep7b"]
+    s, e = wl.llm, wl.enc
+    N = s.n_blocks
+    L, n_img, L_img = wl.seq, wl.n_img, wl.img_tokens
+    ks = sorted(int(k) for k in args.pipeline_ks.split(","))
+    if not all(0 < k <= N for k in ks):
+        raise SystemExit("--pipeline-ks must lie in (0, %d]" % N)
+    kmax = max(ks)
+    nf = args.pipeline_frames
+    ctx = vb.Context(llm=vb.stack_cfg(s, "bf16", max_tokens=L, max_batch=1, n_blocks=kmax),
+                     enc=vb.stack_cfg(e, "bf16", max_tokens=L_img, max_batch=n_img))
+    for l in range(e.n_blocks):
+        ctx.vla_load_block_weights(vb.VLA_STACK_ENC, l, synth.vit_block_weights(wl, l))
+    for l in range(kmax):
+        ctx.vla_load_block_weights(vb.VLA_STACK_LLM, l, synth.llm_block_weights(wl, l))
+    dev = torch.device("cuda:0")
+    toks = [torch.from_numpy(synth.tokens(wl, frame=f).view(np.int16)).to(dev) for f in range(2)]
+    pats = [torch.from_numpy(synth.patches(wl, frame=f).view(np.int16)).to(dev) for f in range(2)]
+    enc_out = torch.empty((n_img, L_img, e.d_model), dtype=torch.bfloat16, device=dev)
+    torch.cuda.synchronize()
+    cs = ctx.compute_stream
+    fid = [5000]
+    res = {}
+    threads = None
+    for k in ks:
+        sfx = None
+        if k < N:
+            t0 = time.time()
+            sfx = vb.Suffix(vb.stack_cfg(s, "bf16", max_tokens=L), k, N, args.pipeline_threads)
+            for l in range(k, N):
+                sfx.vla_suffix_load_block_weights(l, synth.llm_block_weights(wl, l))
+            threads = sfx.vla_suffix_threads()
+            log("k=%d: host suffix [%d,%d) loaded on %d threads (%.0fs)" % (k, k, N, threads, time.time() - t0))
+        bnds = [vb.Boundary(1, L, s.d_model, k, s.n_kv_heads, s.head_dim, with_kv=False) for _ in range(3)]
+        outs = [np.empty((1, L, s.d_model), np.float32) for _ in range(3)]
+
+        def gpu_stage(i, b):
+            f = fid[0]
+            fid[0] += 1
+            ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            ev[0].record(cs)
+            ctx.vla_run_encoder(f, pats[i % 2], n_img, L_img, enc_out)
+            ctx.vla_run_prefix(f, toks[i % 2], 1, L, k, b)
+            ev[1].record(cs)
+            return f, ev
+
+        # frame by frame: T_G + T_X + T_C on one frame's critical path (Eq. (12))
+        serial, tg, tx, tc = [], [], [], []
+        for i in range(nf + 1):
+            t = time.perf_counter()
+            f, ev = gpu_stage(i, bnds[0])
+            ctx.vla_wait_boundary(f, 600000)
+            t1 = time.perf_counter()
+            if sfx is not None:
+                hb = bnds[0].hidden.view(torch.int16).numpy().view(np.uint16)
+                sfx.vla_suffix_run(hb, vb.VLA_BF16, 1, L, outs[0])
+            t2 = time.perf_counter()
+            if i == 0:
+                continue  # warm-up
+            serial.append((t2 - t) * 1000)
+            tg.append(ev[0].elapsed_time(ev[1]))
+            tx.append(ctx.vla_frame_times(f)[1])
+            tc.append((t2 - t1) * 1000)
+        # cross-frame pipeline: the GPU runs frame i+1 while the host runs frame i
+        pops = []
+        if sfx is not None:
+            pipe = vb.Pipeline(ctx, sfx, depth=2)
+            pending = 0
+            for i in range(nf + 2):
+                if pending == 2:
+                    pipe.vla_pipeline_pop(600000)
+                    pops.append(time.perf_counter())
+                    pending -= 1
+                f, _ = gpu_stage(i, bnds[i % 3])
+                pipe.vla_pipeline_push(f, bnds[i % 3], 1, L, outs[i % 3])
+                pending += 1
+            while pending:
+                pipe.vla_pipeline_pop(600000)
+                pops.append(time.perf_counter())
+                pending -= 1
+            pipe.vla_pipeline_destroy()
+            pops = pops[2:]  # steady state
+        else:
+            for i in range(nf + 2):
+                f, _ = gpu_stage(i, bnds[i % 3])
+                if i >= 2:
+                    ctx.vla_wait_boundary(f - 2, 600000)
+                    pops.append(time.perf_counter())
+        stream = (pops[-1] - pops[0]) * 1000 / (len(pops) - 1)
+        T = {"T_G_ms": float(np.mean(tg)), "T_X_ms": float(np.mean(tx)), "T_C_ms": float(np.mean(tc))}
+        res[str(k)] = {**{n: round(v, 3) for n, v in T.items()},
+                       "suffix_blocks": N - k,
+                       "T_frame_serial_ms": round(float(np.mean(serial)), 3),
+                       "T_stream_ms": round(stream, 3),
+                       "eq13_max_ms": round(max(T["T_G_ms"], T["T_X_ms"] + T["T_C_ms"]), 3),
+                       "F_exec_hz": round(1000.0 / stream, 2)}
+        log("k=%d: %s" % (k, res[str(k)]))
+        del sfx
+    best = min(res, key=lambda k: res[k]["T_stream_ms"])
+    out = {"metric": "stream interval of the partitioned model (GPU encoder + blocks [0,k), host blocks [k,%d))" % N,
+           "value": res[best]["T_stream_ms"], "unit": "ms", "higher_is_better": False, "best_k": int(best),
+           "n_gpus": 1, "frames": nf, "dtype": "bf16", "data": "synthetic",
+           "config": {"workload": "sweep7b encoder 24x ViT-L over 6x1024 + %d 7B-shaped decoder blocks over 1x%d "
+                                  "tokens, boundary bf16 to pinned host" % (N, L),
+                      "host_threads": threads},
+           "per_k": res}
+    ctx.vla_destroy()
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -132,6 +256,11 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (HBM counter calibration)")
+    ap.add_argument("--pipeline", action="store_true",
+                    help="measure the partitioned model (GPU prefix + host suffix) instead of the GPU prefix")
+    ap.add_argument("--pipeline-ks", default="16,24,28,31,32")
+    ap.add_argument("--pipeline-frames", type=int, default=4)
+    ap.add_argument("--pipeline-threads", type=int, default=0, help="host suffix threads (0: all)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the prefix is a single-GPU stage (frames, cameras or block "
@@ -140,6 +269,10 @@ def main():
 
     import numpy as np
     import torch
+
+    if args.pipeline:
+        pipeline_bench(args)
+        return
 
     if args.copy_calibration:
         n = args.copy_calibration * 2 ** 20 // 4

@@ -1,4 +1,5 @@
-"""ctypes binding of the C ABI in include/vla_prefix.h and include/vla_ops.h.
+"""ctypes binding of the C ABI in include/vla_prefix.h, include/vla_ops.h and
+include/vla_suffix.h.
 
 Argument marshalling only: every step of the prefix runs in the HIP library.
 PyTorch supplies the device arena, the streams and the pinned host
@@ -83,6 +84,13 @@ def lib():
             "vla_op_attention_bf16": [c_void_p, c_void_p, c_void_p, c_int, c_void_p, c_int, c_int, c_int, c_int,
                                       c_int, c_int, c_void_p],
             "vla_op_norm_bf16": [c_void_p, c_void_p, c_void_p, c_float, c_void_p, c_int, c_int, c_void_p],
+            "vla_suffix_create": [P(vla_stack_cfg), c_int, c_int, c_int, P(c_void_p)],
+            "vla_suffix_load_block_weights": [c_void_p, c_int, P(vla_block_weights)],
+            "vla_suffix_run": [c_void_p, c_void_p, c_int, c_int, c_int, c_void_p],
+            "vla_suffix_threads": [c_void_p, P(c_int)],
+            "vla_pipeline_create": [c_void_p, c_void_p, c_int, P(c_void_p)],
+            "vla_pipeline_push": [c_void_p, c_uint64, P(vla_boundary), c_int, c_int, c_void_p],
+            "vla_pipeline_pop": [c_void_p, P(c_uint64), P(c_float), P(c_float), c_int],
         }
         for name, args in sig.items():
             fn = getattr(L, name)
@@ -94,6 +102,9 @@ def lib():
         L.vla_last_error.restype = c_char_p
         L.vla_destroy.argtypes = [c_void_p]
         L.vla_destroy.restype = None
+        for name in ("vla_suffix_destroy", "vla_pipeline_destroy"):
+            getattr(L, name).argtypes = [c_void_p]
+            getattr(L, name).restype = None
         _lib = L
     return _lib
 
@@ -156,6 +167,22 @@ class Boundary:
         return self.c.frame_id
 
 
+def _block_weights(weights: dict):
+    """A vla_block_weights over contiguous copies of the arrays (kept alive by
+    the returned list)."""
+    w = vla_block_weights()
+    keep = []
+    for name, arr in weights.items():
+        if arr is None:
+            continue
+        if name not in _WEIGHT_FIELDS:
+            raise KeyError(name)
+        arr = np.ascontiguousarray(arr)
+        keep.append(arr)
+        setattr(w, name, arr.ctypes.data)
+    return w, keep
+
+
 class Context:
     """One vla_ctx over a torch-allocated device arena and torch streams for
     the decoder blocks, the encoder blocks (the decoder's stream unless one
@@ -181,16 +208,7 @@ class Context:
         self.h = h.value
 
     def vla_load_block_weights(self, which: int, block: int, weights: dict):
-        w = vla_block_weights()
-        keep = []
-        for name, arr in weights.items():
-            if arr is None:
-                continue
-            if name not in _WEIGHT_FIELDS:
-                raise KeyError(name)
-            arr = np.ascontiguousarray(arr)
-            keep.append(arr)
-            setattr(w, name, arr.ctypes.data)
+        w, keep = _block_weights(weights)
         _check(lib().vla_load_block_weights(self.h, which, block, ctypes.byref(w)), self.h)
 
     def vla_run_encoder(self, frame_id: int, patches, n_img: int, L_img: int, out_dev):
@@ -254,3 +272,73 @@ def vla_op_norm_bf16(x, g, b, eps, y, M, d, stream=None):
 
 def vla_status_string(code: int) -> str:
     return lib().vla_status_string(code).decode()
+
+
+# ----------------------------------------------------------- host suffix
+
+class Suffix:
+    """One vla_suffix: decoder blocks [k_begin, k_end) on the host CPU."""
+
+    def __init__(self, llm: vla_stack_cfg, k_begin: int, k_end: int, n_threads: int = 0):
+        h = c_void_p()
+        _check(lib().vla_suffix_create(ctypes.byref(llm), k_begin, k_end, n_threads, ctypes.byref(h)))
+        self.h = h.value
+        self.d = llm.d_model
+
+    def vla_suffix_load_block_weights(self, block: int, weights: dict):
+        w, keep = _block_weights(weights)
+        _check(lib().vla_suffix_load_block_weights(self.h, block, ctypes.byref(w)))
+
+    def vla_suffix_run(self, h, in_dtype: int, B: int, L: int, out):
+        _check(lib().vla_suffix_run(self.h, _ptr(h), in_dtype, B, L, _ptr(out)))
+
+    def vla_suffix_threads(self) -> int:
+        n = c_int()
+        _check(lib().vla_suffix_threads(self.h, ctypes.byref(n)))
+        return n.value
+
+    def vla_suffix_destroy(self):
+        if getattr(self, "h", None):
+            lib().vla_suffix_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.vla_suffix_destroy()
+        except Exception:
+            pass
+
+
+class Pipeline:
+    """One vla_pipeline: a consumer thread running `suffix` on the boundaries
+    of `ctx`, in push order."""
+
+    def __init__(self, ctx: Context, suffix: Suffix, depth: int):
+        h = c_void_p()
+        _check(lib().vla_pipeline_create(ctx.h, suffix.h, depth, ctypes.byref(h)))
+        self.h = h.value
+        self._held = {}
+
+    def vla_pipeline_push(self, frame_id: int, b: Boundary, B: int, L: int, out):
+        _check(lib().vla_pipeline_push(self.h, frame_id, ctypes.byref(b.c), B, L, _ptr(out)))
+        self._held[frame_id] = (b, out)
+
+    def vla_pipeline_pop(self, timeout_ms: int = -1):
+        """(frame_id, t_wait_ms, t_cpu_ms) of the oldest pushed frame."""
+        f, tw, tc = c_uint64(), c_float(), c_float()
+        code = lib().vla_pipeline_pop(self.h, ctypes.byref(f), ctypes.byref(tw), ctypes.byref(tc), timeout_ms)
+        self._held.pop(f.value, None)
+        _check(code)
+        return f.value, tw.value, tc.value
+
+    def vla_pipeline_destroy(self):
+        if getattr(self, "h", None):
+            lib().vla_pipeline_destroy(self.h)
+            self.h = None
+            self._held.clear()
+
+    def __del__(self):
+        try:
+            self.vla_pipeline_destroy()
+        except Exception:
+            pass

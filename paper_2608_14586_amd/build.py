@@ -19,10 +19,15 @@ DEVICE_FLAGS = ["--offload-arch=" + ARCH, "-O3", "-fPIC", "-std=c++17", "-Xclang
                 "-packed-fp32-ops", "-Wno-unused-result"]
 HOST_FLAGS = ["-O2", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-result"]
 
-SOURCES = ["gemm_bf16.hip", "attention_bf16.hip", "norm.hip", "fp32_path.hip", "runtime.cpp", "ops.cpp"]
+SOURCES = ["gemm_bf16.hip", "attention_bf16.hip", "norm.hip", "fp32_path.hip", "runtime.cpp", "ops.cpp",
+           "host_suffix.cpp", "host_suffix_api.cpp"]
 # Attention keeps its score and output accumulators in VGPRs: the softmax
 # touches them every key tile, and AGPR accumulators would cost a copy each way.
-EXTRA = {"attention_bf16.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+EXTRA = {"attention_bf16.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+         # the host suffix executor: AVX-512 BF16 kernels, entered only after a CPU check
+         "host_suffix.cpp": ["--offload-host-only", "-O3", "-mavx512f", "-mavx512bw", "-mavx512vl", "-mavx512bf16",
+                             "-mfma"],
+         "host_suffix_api.cpp": ["--offload-host-only"]}
 
 
 def _compile(src: str) -> str:
@@ -31,7 +36,7 @@ def _compile(src: str) -> str:
     if src.endswith(".hip"):
         cmd = [HIPCC] + DEVICE_FLAGS + EXTRA.get(src, []) + ["-c", path, "-o", obj]
     else:
-        cmd = [HIPCC] + HOST_FLAGS + ["-c", path, "-o", obj]
+        cmd = [HIPCC] + HOST_FLAGS + EXTRA.get(src, []) + ["-c", path, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("hipcc failed for %s:\n%s\n%s" % (src, " ".join(cmd), r.stderr[-6000:]))

@@ -188,6 +188,13 @@ struct vla_ctx {
   int prof_n[2][VLA_K_COUNT] = {};
 };
 
+// Device and copy stream of a context, for the host pipeline consumer
+// (host_suffix_api.cpp), which marks the end of a frame's copies there.
+namespace vla {
+int ctx_device(const vla_ctx* c) { return c->device; }
+hipStream_t ctx_copy_stream(const vla_ctx* c) { return c->copy; }
+}  // namespace vla
+
 namespace {
 
 // Arena layout, shared by vla_query_sizes and vla_create: a bump allocator
