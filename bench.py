@@ -129,6 +129,81 @@ def cpu_baseline(wl, k, budget_s=20.0):
             "blas": "numpy %s" % np.__version__}
 
 
+def gpu_stage_factory(ctx, pats, toks, enc_out, n_img, L_img, L, fid):
+    """gpu_stage(i, k, boundary): the GPU stage of one frame (encoder +
+    decoder blocks [0, k)) enqueued, with events around it on the compute
+    stream; returns (frame id, (start, end) events)."""
+    import torch
+
+    def gpu_stage(i, k, b):
+        f = fid[0]
+        fid[0] += 1
+        ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+        ev[0].record(ctx.compute_stream)
+        ctx.vla_run_encoder(f, pats[i % 2], n_img, L_img, enc_out)
+        ctx.vla_run_prefix(f, toks[i % 2], 1, L, k, b)
+        ev[1].record(ctx.compute_stream)
+        return f, ev
+    return gpu_stage
+
+
+def adaptive_run(args, ctx, gpu_stage, wl, N):
+    """Closed loop with the partition controller (Sec. IV-D): each frame's
+    partition point comes from Phi over the dynamic zone [N - 8, N], which
+    learns the stage model from the frames it observes.  The first half runs
+    alone; in the second half another module declares a share of the GPU
+    (u_gpu), which Phi trades against the host stage."""
+    import numpy as np
+    import synth
+    from paper_2608_14586_amd import binding as vb
+
+    s = wl.llm
+    L = wl.seq
+    k_lo, k_hi, k0 = N - 8, N, N - 6
+    sfx = vb.Suffix(vb.stack_cfg(s, "bf16", max_tokens=L), k_lo, N, args.pipeline_threads)
+    for l in range(k_lo, N):
+        sfx.vla_suffix_load_block_weights(l, synth.llm_block_weights(wl, l))
+    # uninformative priors: one ms per block on each side, nothing fixed
+    phi = vb.Sched(N, k_lo, k_hi, k0, 0.0, 1.0, 1.0, 0.0, backlog_hi=2)
+    pipe = vb.Pipeline(ctx, sfx, depth=2)
+    bnds = [vb.Boundary(1, L, s.d_model, k_hi, s.n_kv_heads, s.head_dim, with_kv=False) for _ in range(3)]
+    outs = [np.empty((1, L, s.d_model), np.float32) for _ in range(3)]
+    n = args.pipeline_adaptive
+    pending = []  # (frame id, k, events, push index)
+    trace = []
+    last_pop = [None]
+
+    def pop_one():
+        f, tw, tc = pipe.vla_pipeline_pop(600000)
+        fid, k, ev, i = pending.pop(0)
+        assert f == fid
+        ctx.vla_wait_boundary(f, 600000)  # already copied: retires the slot, records T_X
+        tg = ev[0].elapsed_time(ev[1])
+        tx = ctx.vla_frame_times(f)[1]
+        phi.vla_sched_observe(k, tg, tx, tc)
+        now = time.perf_counter()
+        trace[i].update({"T_G_ms": round(tg, 2), "T_X_ms": round(tx, 3), "T_C_ms": round(tc, 1),
+                         "interval_ms": None if last_pop[0] is None else round((now - last_pop[0]) * 1000, 1)})
+        last_pop[0] = now
+
+    for i in range(n):
+        u_gpu = 0.0 if i < n // 2 else 0.95
+        if len(pending) == 2:
+            pop_one()
+        k = phi.vla_sched_decide(u_gpu, 0.0, pipe.vla_pipeline_backlog(), 0.0)
+        f, ev = gpu_stage(i, k, bnds[i % 3])
+        pipe.vla_pipeline_push(f, bnds[i % 3], 1, L, k, outs[i % 3])
+        pending.append((f, k, ev, i))
+        trace.append({"frame": i, "u_gpu": u_gpu, "k": k})
+    while pending:
+        pop_one()
+    pipe.vla_pipeline_destroy()
+    a, b, c, x = phi.vla_sched_model()
+    log("adaptive: k per frame %s; model a=%.1f b=%.3f c=%.1f x=%.3f ms" % ([t["k"] for t in trace], a, b, c, x))
+    return {"zone": [k_lo, k_hi], "k_init": k0, "model_ms": {"a": round(a, 2), "b": round(b, 3), "c": round(c, 1),
+                                                             "x": round(x, 3)}, "frames": trace}
+
+
 def pipeline_bench(args):
     """Stage times and stream interval of the partitioned model per k."""
     import numpy as np
@@ -210,7 +285,7 @@ def pipeline_bench(args):
                     pops.append(time.perf_counter())
                     pending -= 1
                 f, _ = gpu_stage(i, bnds[i % 3])
-                pipe.vla_pipeline_push(f, bnds[i % 3], 1, L, outs[i % 3])
+                pipe.vla_pipeline_push(f, bnds[i % 3], 1, L, k, outs[i % 3])
                 pending += 1
             while pending:
                 pipe.vla_pipeline_pop(600000)
@@ -234,6 +309,8 @@ def pipeline_bench(args):
                        "F_exec_hz": round(1000.0 / stream, 2)}
         log("k=%d: %s" % (k, res[str(k)]))
         del sfx
+    adaptive = adaptive_run(args, ctx, gpu_stage_factory(ctx, pats, toks, enc_out, n_img, L_img, L, fid),
+                            wl, N) if args.pipeline_adaptive > 0 else None
     best = min(res, key=lambda k: res[k]["T_stream_ms"])
     out = {"metric": "stream interval of the partitioned model (GPU encoder + blocks [0,k), host blocks [k,%d))" % N,
            "value": res[best]["T_stream_ms"], "unit": "ms", "higher_is_better": False, "best_k": int(best),
@@ -242,6 +319,8 @@ def pipeline_bench(args):
                                   "tokens, boundary bf16 to pinned host" % (N, L),
                       "host_threads": threads},
            "per_k": res}
+    if adaptive is not None:
+        out["adaptive"] = adaptive
     ctx.vla_destroy()
     print(json.dumps(out), flush=True)
 
@@ -261,6 +340,8 @@ def main():
     ap.add_argument("--pipeline-ks", default="16,24,28,31,32")
     ap.add_argument("--pipeline-frames", type=int, default=4)
     ap.add_argument("--pipeline-threads", type=int, default=0, help="host suffix threads (0: all)")
+    ap.add_argument("--pipeline-adaptive", type=int, default=20, metavar="FRAMES",
+                    help="frames of the closed loop with the partition controller (0: skip)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the prefix is a single-GPU stage (frames, cameras or block "

@@ -87,10 +87,17 @@ def lib():
             "vla_suffix_create": [P(vla_stack_cfg), c_int, c_int, c_int, P(c_void_p)],
             "vla_suffix_load_block_weights": [c_void_p, c_int, P(vla_block_weights)],
             "vla_suffix_run": [c_void_p, c_void_p, c_int, c_int, c_int, c_void_p],
+            "vla_suffix_run_from": [c_void_p, c_int, c_void_p, c_int, c_int, c_int, c_void_p],
             "vla_suffix_threads": [c_void_p, P(c_int)],
             "vla_pipeline_create": [c_void_p, c_void_p, c_int, P(c_void_p)],
-            "vla_pipeline_push": [c_void_p, c_uint64, P(vla_boundary), c_int, c_int, c_void_p],
+            "vla_pipeline_push": [c_void_p, c_uint64, P(vla_boundary), c_int, c_int, c_int, c_void_p],
             "vla_pipeline_pop": [c_void_p, P(c_uint64), P(c_float), P(c_float), c_int],
+            "vla_pipeline_backlog": [c_void_p, P(c_int)],
+            "vla_sched_create": [c_int, c_int, c_int, c_int, c_float, c_float, c_float, c_float, c_int, P(c_void_p)],
+            "vla_sched_observe": [c_void_p, c_int, c_float, c_float, c_float],
+            "vla_sched_predict": [c_void_p, c_int, c_float, c_float, P(c_float), P(c_float), P(c_float)],
+            "vla_sched_decide": [c_void_p, c_float, c_float, c_int, c_float, P(c_int)],
+            "vla_sched_model": [c_void_p, P(c_float), P(c_float), P(c_float), P(c_float)],
         }
         for name, args in sig.items():
             fn = getattr(L, name)
@@ -102,7 +109,7 @@ def lib():
         L.vla_last_error.restype = c_char_p
         L.vla_destroy.argtypes = [c_void_p]
         L.vla_destroy.restype = None
-        for name in ("vla_suffix_destroy", "vla_pipeline_destroy"):
+        for name in ("vla_suffix_destroy", "vla_pipeline_destroy", "vla_sched_destroy"):
             getattr(L, name).argtypes = [c_void_p]
             getattr(L, name).restype = None
         _lib = L
@@ -292,6 +299,9 @@ class Suffix:
     def vla_suffix_run(self, h, in_dtype: int, B: int, L: int, out):
         _check(lib().vla_suffix_run(self.h, _ptr(h), in_dtype, B, L, _ptr(out)))
 
+    def vla_suffix_run_from(self, k: int, h, in_dtype: int, B: int, L: int, out):
+        _check(lib().vla_suffix_run_from(self.h, k, _ptr(h), in_dtype, B, L, _ptr(out)))
+
     def vla_suffix_threads(self) -> int:
         n = c_int()
         _check(lib().vla_suffix_threads(self.h, ctypes.byref(n)))
@@ -319,9 +329,14 @@ class Pipeline:
         self.h = h.value
         self._held = {}
 
-    def vla_pipeline_push(self, frame_id: int, b: Boundary, B: int, L: int, out):
-        _check(lib().vla_pipeline_push(self.h, frame_id, ctypes.byref(b.c), B, L, _ptr(out)))
+    def vla_pipeline_push(self, frame_id: int, b: Boundary, B: int, L: int, k: int, out):
+        _check(lib().vla_pipeline_push(self.h, frame_id, ctypes.byref(b.c), B, L, k, _ptr(out)))
         self._held[frame_id] = (b, out)
+
+    def vla_pipeline_backlog(self) -> int:
+        n = c_int()
+        _check(lib().vla_pipeline_backlog(self.h, ctypes.byref(n)))
+        return n.value
 
     def vla_pipeline_pop(self, timeout_ms: int = -1):
         """(frame_id, t_wait_ms, t_cpu_ms) of the oldest pushed frame."""
@@ -340,5 +355,46 @@ class Pipeline:
     def __del__(self):
         try:
             self.vla_pipeline_destroy()
+        except Exception:
+            pass
+
+
+class Sched:
+    """One vla_sched: the partition controller over the dynamic zone [k_lo, k_hi]."""
+
+    def __init__(self, n_blocks, k_lo, k_hi, k_init, a_ms, b_ms, c_ms, x_ms, backlog_hi=2):
+        h = c_void_p()
+        _check(lib().vla_sched_create(n_blocks, k_lo, k_hi, k_init, a_ms, b_ms, c_ms, x_ms, backlog_hi,
+                                      ctypes.byref(h)))
+        self.h = h.value
+
+    def vla_sched_observe(self, k, t_g_ms, t_x_ms, t_c_ms):
+        _check(lib().vla_sched_observe(self.h, k, t_g_ms, t_x_ms, t_c_ms))
+
+    def vla_sched_predict(self, k, u_gpu=0.0, u_cpu=0.0):
+        """(T_G', T_C', T_stream) predicted for partition point k."""
+        g, c, t = c_float(), c_float(), c_float()
+        _check(lib().vla_sched_predict(self.h, k, u_gpu, u_cpu, ctypes.byref(g), ctypes.byref(c), ctypes.byref(t)))
+        return g.value, c.value, t.value
+
+    def vla_sched_decide(self, u_gpu=0.0, u_cpu=0.0, backlog=0, gpu_budget_ms=0.0) -> int:
+        k = c_int()
+        _check(lib().vla_sched_decide(self.h, u_gpu, u_cpu, backlog, gpu_budget_ms, ctypes.byref(k)))
+        return k.value
+
+    def vla_sched_model(self):
+        """(a, b, c, x) in ms."""
+        a, b, c, x = c_float(), c_float(), c_float(), c_float()
+        _check(lib().vla_sched_model(self.h, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c), ctypes.byref(x)))
+        return a.value, b.value, c.value, x.value
+
+    def vla_sched_destroy(self):
+        if getattr(self, "h", None):
+            lib().vla_sched_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.vla_sched_destroy()
         except Exception:
             pass

@@ -20,14 +20,15 @@ DEVICE_FLAGS = ["--offload-arch=" + ARCH, "-O3", "-fPIC", "-std=c++17", "-Xclang
 HOST_FLAGS = ["-O2", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-result"]
 
 SOURCES = ["gemm_bf16.hip", "attention_bf16.hip", "norm.hip", "fp32_path.hip", "runtime.cpp", "ops.cpp",
-           "host_suffix.cpp", "host_suffix_api.cpp"]
+           "host_suffix.cpp", "host_suffix_api.cpp", "sched.cpp"]
 # Attention keeps its score and output accumulators in VGPRs: the softmax
 # touches them every key tile, and AGPR accumulators would cost a copy each way.
 EXTRA = {"attention_bf16.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
          # the host suffix executor: AVX-512 BF16 kernels, entered only after a CPU check
          "host_suffix.cpp": ["--offload-host-only", "-O3", "-mavx512f", "-mavx512bw", "-mavx512vl", "-mavx512bf16",
                              "-mfma"],
-         "host_suffix_api.cpp": ["--offload-host-only"]}
+         "host_suffix_api.cpp": ["--offload-host-only"],
+         "sched.cpp": ["--offload-host-only"]}
 
 
 def _compile(src: str) -> str:

@@ -539,7 +539,7 @@ static void block_fwd(Suffix* s, const Block& w, int B, int L) {
   });
 }
 
-bool run(Suffix* s, const void* in, bool in_f32, int B, int L, float* out) {
+bool run(Suffix* s, int k, const void* in, bool in_f32, int B, int L, float* out) {
   const Cfg& c = s->c;
   const int M = B * L, d = c.d, hd = c.H * c.dh, kvd = c.Hkv * c.dh;
   const int dpad = (d + 1) / 2 * 2, hdpad = (hd + 1) / 2 * 2;
@@ -560,7 +560,7 @@ bool run(Suffix* s, const void* in, bool in_f32, int B, int L, float* out) {
     const uint16_t* hb = (const uint16_t*)in;
     for (size_t i = 0; i < (size_t)M * d; ++i) s->h[i] = bf2f(hb[i]);
   }
-  for (const Block& b : s->blocks) block_fwd(s, b, B, L);
+  for (int l = k; l < s->k_end; ++l) block_fwd(s, s->blocks[l - s->k_begin], B, L);
   std::memcpy(out, s->h.data(), sizeof(float) * (size_t)M * d);
   return true;
 }

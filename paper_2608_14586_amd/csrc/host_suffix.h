@@ -25,8 +25,9 @@ void destroy(Suffix* s);
 int threads(const Suffix* s);
 bool load_block(Suffix* s, int block, const Weights& w);
 bool all_loaded(const Suffix* s);
-// blocks [k_begin, k_end) over h (bf16, or f32 when in_f32) [B][L][d] -> out f32 [B][L][d]
-bool run(Suffix* s, const void* in, bool in_f32, int B, int L, float* out);
+// blocks [k, k_end) over h (bf16, or f32 when in_f32) [B][L][d] -> out f32 [B][L][d];
+// k_begin <= k <= k_end
+bool run(Suffix* s, int k, const void* in, bool in_f32, int B, int L, float* out);
 
 }  // namespace host
 }  // namespace vla

@@ -82,16 +82,22 @@ vla_status vla_suffix_load_block_weights(vla_suffix* s, int block, const vla_blo
   }
 }
 
-vla_status vla_suffix_run(vla_suffix* s, const void* h, vla_dtype in_dtype, int B, int L, float* out) {
+vla_status vla_suffix_run_from(vla_suffix* s, int k, const void* h, vla_dtype in_dtype, int B, int L, float* out) {
   if (!s || !h || !out || B <= 0 || L <= 0) return VLA_ERR_INVALID_ARG;
   if (in_dtype != VLA_BF16 && in_dtype != VLA_F32) return VLA_ERR_INVALID_ARG;
+  if (k < s->k_begin || k > s->k_end) return VLA_ERR_INVALID_ARG;
   if (!vla::host::all_loaded(s->impl)) return VLA_ERR_NOT_LOADED;
   try {
-    vla::host::run(s->impl, h, in_dtype == VLA_F32, B, L, out);
+    vla::host::run(s->impl, k, h, in_dtype == VLA_F32, B, L, out);
     return VLA_OK;
   } catch (...) {
     return VLA_ERR_OOM;
   }
+}
+
+vla_status vla_suffix_run(vla_suffix* s, const void* h, vla_dtype in_dtype, int B, int L, float* out) {
+  if (!s) return VLA_ERR_INVALID_ARG;
+  return vla_suffix_run_from(s, s->k_begin, h, in_dtype, B, L, out);
 }
 
 vla_status vla_suffix_threads(const vla_suffix* s, int* n) {
@@ -116,7 +122,7 @@ struct vla_pipeline {
     hipEvent_t ev = nullptr;
     const void* h = nullptr;
     vla_dtype dt = VLA_BF16;
-    int B = 0, L = 0;
+    int B = 0, L = 0, k = 0;
     float* out = nullptr;
     bool done = false;
     vla_status st = VLA_OK;
@@ -150,7 +156,7 @@ struct vla_pipeline {
       vla_status st = hipEventSynchronize(j->ev) == hipSuccess ? VLA_OK : VLA_ERR_HIP;
       const float tw = (float)ms_since(t0);
       auto t1 = std::chrono::steady_clock::now();
-      if (st == VLA_OK) st = vla_suffix_run(s, j->h, j->dt, j->B, j->L, j->out);
+      if (st == VLA_OK) st = vla_suffix_run_from(s, j->k, j->h, j->dt, j->B, j->L, j->out);
       const float tc = (float)ms_since(t1);
       {
         std::lock_guard<std::mutex> g(mu);
@@ -193,8 +199,10 @@ vla_status vla_pipeline_create(vla_ctx* ctx, vla_suffix* s, int depth, vla_pipel
   }
 }
 
-vla_status vla_pipeline_push(vla_pipeline* p, uint64_t frame_id, const vla_boundary* b, int B, int L, float* out) {
+vla_status vla_pipeline_push(vla_pipeline* p, uint64_t frame_id, const vla_boundary* b, int B, int L, int k,
+                             float* out) {
   if (!p || !b || !b->hidden || !out || B <= 0 || L <= 0) return VLA_ERR_INVALID_ARG;
+  if (k < p->s->k_begin || k > p->s->k_end) return VLA_ERR_INVALID_ARG;
   const size_t need = (size_t)B * L * p->s->cfg.d * (b->out_dtype == VLA_F32 ? 4 : 2);
   if (b->hidden_bytes < need) return VLA_ERR_SHAPE;
   auto j = std::make_shared<vla_pipeline::Job>();
@@ -203,6 +211,7 @@ vla_status vla_pipeline_push(vla_pipeline* p, uint64_t frame_id, const vla_bound
   j->dt = b->out_dtype;
   j->B = B;
   j->L = L;
+  j->k = k;
   j->out = out;
   std::unique_lock<std::mutex> lk(p->mu);
   p->cv_space.wait(lk, [&] { return (int)p->all.size() < p->depth; });
@@ -234,6 +243,13 @@ vla_status vla_pipeline_pop(vla_pipeline* p, uint64_t* frame_id, float* t_wait_m
   if (t_wait_ms) *t_wait_ms = j->t_wait;
   if (t_cpu_ms) *t_cpu_ms = j->t_cpu;
   return j->st;
+}
+
+vla_status vla_pipeline_backlog(vla_pipeline* p, int* n) {
+  if (!p || !n) return VLA_ERR_INVALID_ARG;
+  std::lock_guard<std::mutex> g(p->mu);
+  *n = (int)p->all.size();
+  return VLA_OK;
 }
 
 void vla_pipeline_destroy(vla_pipeline* p) {

@@ -51,7 +51,7 @@ def test_pipeline_frames_in_order_and_match_direct_suffix(out_dtype):
             got[fid] = outs[(fid - 100) % 3].copy()
             assert tc > 0.0 and tw >= 0.0
         ctx.vla_run_prefix(100 + f, tok, B, L, K, bnds[f % 3])
-        pipe.vla_pipeline_push(100 + f, bnds[f % 3], B, L, outs[f % 3])
+        pipe.vla_pipeline_push(100 + f, bnds[f % 3], B, L, K, outs[f % 3])
     for _ in range(3):
         fid, _, _ = pipe.vla_pipeline_pop(60000)
         popped.append(fid)
@@ -89,7 +89,7 @@ def test_pipeline_rejects_bad_push():
     pipe = vb.Pipeline(ctx, sfx, depth=1)
     small = vb.Boundary(1, 8, SHAPE.d_model, K, SHAPE.n_kv_heads, SHAPE.head_dim, with_kv=False)
     with pytest.raises(vb.VlaError) as e:
-        pipe.vla_pipeline_push(1, small, WL.batch, WL.seq, outs[0])
+        pipe.vla_pipeline_push(1, small, WL.batch, WL.seq, K, outs[0])
     assert e.value.name == "VLA_ERR_SHAPE"
     with pytest.raises(vb.VlaError) as e:
         pipe.vla_pipeline_pop(0)

@@ -87,6 +87,25 @@ def test_suffix_deterministic_across_thread_counts():
     assert np.array_equal(outs[0], outs[1]) and np.array_equal(outs[0], outs[2])
 
 
+def test_suffix_run_from_inner_partition_point():
+    # a frame whose partition point moved inside the dynamic zone runs only
+    # the blocks after it: equal to a suffix built for that range
+    wl, W = _case("sfx_from", 4, 128, 2, 1, 64, 320)
+    h = synth.f32_to_bf16(synth.normal_f32(synth.seed_of("sfx_from_h"), (1, 50, 128)))
+    wide = _suffix(wl, W, 1, 4)
+    narrow = _suffix(wl, W, 3, 4)
+    a = np.empty((1, 50, 128), np.float32)
+    b = np.empty((1, 50, 128), np.float32)
+    wide.vla_suffix_run_from(3, h, vb.VLA_BF16, 1, 50, a)
+    narrow.vla_suffix_run(h, vb.VLA_BF16, 1, 50, b)
+    assert np.array_equal(a, b)
+    wide.vla_suffix_run_from(4, h, vb.VLA_BF16, 1, 50, a)   # k = k_end: the boundary itself
+    assert np.array_equal(a, synth.as_f32(h))
+    with pytest.raises(vb.VlaError) as e:
+        wide.vla_suffix_run_from(0, h, vb.VLA_BF16, 1, 50, a)
+    assert e.value.name == "VLA_ERR_INVALID_ARG"
+
+
 def test_suffix_gain_matters():
     # a dropped or swapped norm gain must not pass the parity bar
     wl, W = _case("sfx_gain", 1, 128, 2, 2, 64, 320)
