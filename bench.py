@@ -129,6 +129,86 @@ def cpu_baseline(wl, k, budget_s=20.0):
             "blas": "numpy %s" % np.__version__}
 
 
+def decode_bench(args):
+    """Decode steps across the boundary: decoder blocks [0, k) for one new
+    token per sequence after a 2048-token prefix, over the KV cache the prefix
+    handed over.  A step streams the k blocks' weights once, so it is priced
+    against HBM bandwidth."""
+    import numpy as np
+    import torch
+    import synth
+    from paper_2608_14586_amd import binding as vb
+
+    wl = synth.CONFIGS["sweep7b"]
+    s = wl.llm
+    L, k, B, T = wl.seq, args.k, args.decode_batch, args.decode_steps
+    d, Hkv, dh, H, F = s.d_model, s.n_kv_heads, s.head_dim, s.n_heads, s.d_ff
+    L_cap = L + T + 8
+    ctx = vb.Context(llm=vb.stack_cfg(s, "bf16", max_tokens=L_cap, max_batch=B, n_blocks=k))
+    for l in range(k):
+        ctx.vla_load_block_weights(vb.VLA_STACK_LLM, l, synth.llm_block_weights(wl, l))
+    toks = synth.tokens(wl, frame=3, B=B, L=L + T)
+    bnd = vb.Boundary(B, L, d, k, Hkv, dh)
+    ctx.vla_run_prefix(1, np.ascontiguousarray(toks[:, :L]), B, L, k, bnd)
+    ctx.vla_wait_boundary(1, 600000)
+    cache = torch.zeros((k, 2, B, Hkv, L_cap, dh), dtype=torch.bfloat16, device="cuda")
+    cache[:, :, :, :, :L] = bnd.kv.cuda()
+    xs = torch.from_numpy(np.ascontiguousarray(toks[:, L:]).view(np.int16)).cuda()  # [B][T][d]
+    xs = [xs[:, t].contiguous() for t in range(T)]
+    outs = [vb.Boundary(B, 1, d, 0, Hkv, dh, with_kv=False) for _ in range(4)]
+    fid = [100]
+
+    def steps(n, t0, profile=False):
+        if profile:
+            ctx.vla_profile(True)
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        ids = []
+        for i in range(n):
+            f = fid[0]
+            fid[0] += 1
+            ctx.vla_decode_step(f, xs[(t0 + i) % T], B, L + (t0 + i) % T, k, cache, L_cap, outs[i % 4])
+            ids.append(f)
+        for f in ids[-3:]:
+            ctx.vla_wait_boundary(f, 600000)
+        torch.cuda.synchronize()
+        dt = (time.perf_counter() - t) * 1000 / n
+        if profile:
+            ctx.vla_profile(False)
+        return dt
+
+    steps(4, 0)
+    ms = steps(T, 0)
+    steps(T, 0, profile=True)
+    w_bytes = k * 2 * (d * (H + 2 * Hkv) * dh + H * dh * d + d * 2 * F + F * d)
+    kv_bytes = k * 2 * B * Hkv * (L + T // 2) * dh * 2  # cache rows read per step (mean position)
+    kern = {}
+    cls_bytes = {"qkv": d * (H + 2 * Hkv) * dh * 2, "oproj": H * dh * d * 2, "mlp_up": d * 2 * F * 2,
+                 "mlp_down": F * d * 2, "attn": 2 * B * Hkv * (L + T // 2) * dh * 2}
+    for ci, cname in enumerate(vb.KERNEL_CLASSES):
+        tot, cnt = ctx.vla_profile_read(vb.VLA_STACK_LLM, ci)
+        if cnt == 0:
+            continue
+        ent = {"avg_us": round(tot / cnt * 1000, 2), "launches": cnt}
+        if cname in cls_bytes:
+            ent["gbs"] = round(cls_bytes[cname] / (tot / cnt / 1000) / 1e9, 1)
+            ent["frac"] = round(ent["gbs"] / PEAK_HBM_GBS, 4)
+        kern[cname] = ent
+    achieved = (w_bytes + kv_bytes) / (ms / 1000) / 1e9
+    out = {"metric": "decode step time across the boundary (blocks [0,%d), %d sequence(s), after a %d-token prefix)"
+                     % (k, B, L),
+           "value": round(ms, 4), "unit": "ms/step", "higher_is_better": False, "n_gpus": 1, "steps": T,
+           "dtype": "bf16", "data": "synthetic",
+           "tokens_per_s": round(B * 1000 / ms, 1),
+           "config": {"workload": "sweep7b decoder blocks (d=4096, 32x128 MHA, SwiGLU 11008) [0,k), bf16 weights "
+                                  "N(0,0.02), KV cache from the prefix handoff", "k": k, "batch": B, "prefix_len": L},
+           "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                        "frac": round(achieved / PEAK_HBM_GBS, 4), "bytes_per_step": w_bytes + kv_bytes},
+           "kernels": kern}
+    ctx.vla_destroy()
+    print(json.dumps(out), flush=True)
+
+
 def gpu_stage_factory(ctx, pats, toks, enc_out, n_img, L_img, L, fid):
     """gpu_stage(i, k, boundary): the GPU stage of one frame (encoder +
     decoder blocks [0, k)) enqueued, with events around it on the compute
@@ -338,6 +418,10 @@ def main():
     ap.add_argument("--pipeline", action="store_true",
                     help="measure the partitioned model (GPU prefix + host suffix) instead of the GPU prefix")
     ap.add_argument("--pipeline-ks", default="16,24,28,31,32")
+    ap.add_argument("--decode", action="store_true",
+                    help="measure decode steps of blocks [0,k) over the prefix's KV cache instead")
+    ap.add_argument("--decode-steps", type=int, default=32)
+    ap.add_argument("--decode-batch", type=int, default=1)
     ap.add_argument("--pipeline-frames", type=int, default=4)
     ap.add_argument("--pipeline-threads", type=int, default=0, help="host suffix threads (0: all)")
     ap.add_argument("--pipeline-adaptive", type=int, default=20, metavar="FRAMES",
@@ -353,6 +437,9 @@ def main():
 
     if args.pipeline:
         pipeline_bench(args)
+        return
+    if args.decode:
+        decode_bench(args)
         return
 
     if args.copy_calibration:

@@ -166,6 +166,22 @@ vla_status vla_run_prefix(vla_ctx *ctx, uint64_t frame_id, const void *tokens, i
 vla_status vla_run_blocks(vla_ctx *ctx, uint64_t frame_id, const void *tokens, vla_dtype in_dtype, int B, int L,
                           int k_begin, int k_end, vla_boundary *out);
 
+/* One decode step across the boundary: decoder blocks [0, k) for one new
+ * token of each of B <= 4 sequences (bf16 stacks).  x[B][d] (host or device,
+ * bf16) are the tokens' inputs at position pos; each sequence attends over
+ * its cached keys and values [0, pos) plus its own, and appends its key
+ * (after RoPE) and value at pos.
+ * kv_cache: caller-owned DEVICE memory [k][2][B][n_kv_heads][L_cap][head_dim]
+ * bf16 (the layout of vla_boundary's kv with sequence stride L_cap instead of
+ * L), rows [0, pos) filled (for instance with a prefix's KV handoff copied
+ * in).  Needs pos < L_cap and, with RoPE, pos < max_tokens.
+ * out->hidden receives h^(k) of the new tokens [B][d] in out_dtype; out->kv
+ * must be NULL.  Frame ids, vla_wait_boundary and vla_frame_times work as for
+ * vla_run_prefix.  Enqueued; returns after launch.  VLA_ERR_SHAPE when the
+ * context's workspace (sized by max_tokens) cannot hold the step's scratch. */
+vla_status vla_decode_step(vla_ctx *ctx, uint64_t frame_id, const void *x, int B, int pos, int k, void *kv_cache,
+                           int L_cap, vla_boundary *out);
+
 /* Block the host until frame_id's handoff is complete (its host buffers are
  * then readable), or timeout_ms elapses (< 0: wait forever). */
 vla_status vla_wait_boundary(vla_ctx *ctx, uint64_t frame_id, int timeout_ms);

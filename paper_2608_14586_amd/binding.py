@@ -75,6 +75,7 @@ def lib():
             "vla_run_encoder": [c_void_p, c_uint64, c_void_p, c_int, c_int, c_void_p],
             "vla_run_prefix": [c_void_p, c_uint64, c_void_p, c_int, c_int, c_int, P(vla_boundary)],
             "vla_run_blocks": [c_void_p, c_uint64, c_void_p, c_int, c_int, c_int, c_int, c_int, P(vla_boundary)],
+            "vla_decode_step": [c_void_p, c_uint64, c_void_p, c_int, c_int, c_int, c_void_p, c_int, P(vla_boundary)],
             "vla_profile": [c_void_p, c_int],
             "vla_profile_read": [c_void_p, c_int, c_int, P(ctypes.c_double), P(c_int)],
             "vla_wait_boundary": [c_void_p, c_uint64, c_int],
@@ -228,6 +229,10 @@ class Context:
                        out: Boundary):
         _check(lib().vla_run_blocks(self.h, frame_id, _ptr(tokens), in_dtype, B, L, k_begin, k_end,
                                     ctypes.byref(out.c)), self.h)
+
+    def vla_decode_step(self, frame_id: int, x, B: int, pos: int, k: int, kv_cache, L_cap: int, out: Boundary):
+        _check(lib().vla_decode_step(self.h, frame_id, _ptr(x), B, pos, k, _ptr(kv_cache), L_cap, ctypes.byref(out.c)),
+               self.h)
 
     def vla_profile(self, enable: bool):
         _check(lib().vla_profile(self.h, int(enable)), self.h)

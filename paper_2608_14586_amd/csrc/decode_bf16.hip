@@ -1,0 +1,419 @@
+// One decode step of the decoder blocks on the GPU: B <= 4 sequences, one
+// new token each, attending over the KV cache the prefix handed over.
+//
+// With one token per sequence every projection is a skinny product whose
+// cost is streaming the block's weights from HBM once, so the kernels are
+// built around that stream:
+//  * gemv_kernel: each workgroup owns 16 output rows (8 when 16-row tiles
+//    would leave fewer than two workgroups per CU) and streams their weights
+//    over all of K from the packed slab-major layout (the rows' 128 bytes are
+//    contiguous per 64-k slab), 16 loads of 16 bytes in flight per lane
+//    per K chunk, products and accumulation in fp32.  The activation
+//    row is built in LDS while staging: RMSNorm is fused there (QKV,
+//    gate/up; each workgroup recomputes the row's scale, d floats per row);
+//    the split-key attention combine and SwiGLU run once in small kernels
+//    whose bf16 rows the O and down projections stage as they are.
+//    Epilogues: raw fp32 store or fp32 residual add.
+//  * attn_decode_kernel: one workgroup per (sequence, head, 256-key split);
+//    applies RoPE to q and to the new key at the token's position, appends the
+//    new key and value to the cache, and writes (max, sum, unnormalised
+//    output) partials that the O projection's staging combines.
+// Rounding points follow the prefill: normed activations, q and K/V after
+// RoPE, the attention output and the gated activation are bf16.
+
+#include "kernels.h"
+
+namespace vla {
+namespace {
+
+constexpr int GV_KCH = 2048;       // K elements staged per chunk
+constexpr int GV_MB = 4;           // largest batch
+constexpr int ATT_KC = 256;        // keys per attention split
+
+__device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// 8 bf16 products accumulated in fp32 (plain FMAs: the loop is bound by the
+// weight stream, not by VALU issue)
+__device__ __forceinline__ float dot8(const u32x4& w, const u32x4& x, float acc) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    acc = fmaf(bf_lo(w[i]), bf_lo(x[i]), acc);
+    acc = fmaf(bf_hi(w[i]), bf_hi(x[i]), acc);
+  }
+  return acc;
+}
+
+// ---------------------------------------------------------------- staging
+// Each stage fills xs[b][0..n) (bf16) with columns [k0, k0 + n) of the
+// product's input row b; prepare() runs once before the K loop.
+
+// x = bf16(h * rsqrt(mean(h^2) + eps) * g), h fp32 [B][K]
+struct StageNorm {
+  const float* h;
+  const float* g;
+  float eps;
+  __device__ void prepare(float* sc, int B, int K, int tid, float* red) const {
+    for (int b = 0; b < B; ++b) {
+      float s = 0.f;
+      for (int i = tid; i < K; i += 256) {
+        const float v = h[(size_t)b * K + i];
+        s += v * v;
+      }
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+      if ((tid & 63) == 0) red[tid >> 6] = s;
+      __syncthreads();
+      if (tid == 0) sc[b] = 1.f / sqrtf((red[0] + red[1] + red[2] + red[3]) / (float)K + eps);
+      __syncthreads();
+    }
+  }
+  __device__ void fill(bf16_t* xs, const float* sc, int B, int K, int k0, int n, int tid) const {
+    for (int b = 0; b < B; ++b)
+      for (int i = tid; i < n; i += 256) xs[b * GV_KCH + i] = f2bf(h[(size_t)b * K + k0 + i] * sc[b] * g[k0 + i]);
+  }
+};
+
+// x = a bf16 row already in global memory, a[B][K]
+struct StageCopy {
+  const bf16_t* a;
+  __device__ void prepare(float*, int, int, int, float*) const {}
+  __device__ void fill(bf16_t* xs, const float*, int B, int K, int k0, int n, int tid) const {
+    for (int b = 0; b < B; ++b)
+      for (int i = tid * 8; i < n; i += 256 * 8)
+        *(u32x4*)(xs + b * GV_KCH + i) = *(const u32x4*)(a + (size_t)b * K + k0 + i);
+  }
+};
+
+// o[b][h*dh + d] = bf16(sum_s 2^(m_s - m) o_s[d] / sum_s 2^(m_s - m) l_s) from
+// the split-key partials part[B][H][nsplit][2 + dh]; one thread per output
+__global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ part, int nsplit, int H, int dh, int B,
+                                                      bf16_t* __restrict__ o) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= B * H * dh) return;
+  const int d = i % dh, bh = i / dh;
+  const int stride = 2 + dh;
+  const float* p = part + (size_t)bh * nsplit * stride;
+  float m = -INFINITY;
+  for (int s = 0; s < nsplit; ++s) m = fmaxf(m, p[s * stride]);
+  float l = 0.f, acc = 0.f;
+  for (int s = 0; s < nsplit; ++s) {
+    const float w = exp2f(p[s * stride] - m);
+    l += w * p[s * stride + 1];
+    acc += w * p[s * stride + 2 + d];
+  }
+  o[i] = f2bf(acc / l);
+}
+
+// a[b][f] = bf16(silu(gate) * up) from the raw gate/up product gu[B][2*fpad]
+// in the packed row order (each group of 64 rows: 32 gate rows, then their 32
+// up rows); columns [F, fpad) are zero
+__global__ __launch_bounds__(256) void swiglu_kernel(const float* __restrict__ gu, int F, int fpad, int B,
+                                                     bf16_t* __restrict__ a) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= B * fpad) return;
+  const int b = i / fpad, f = i % fpad;
+  float v = 0.f;
+  if (f < F) {
+    const float* r = gu + (size_t)b * 2 * fpad + (f / 32) * 64 + f % 32;
+    const float g = r[0];
+    v = g / (1.f + __expf(-g)) * r[32];
+  }
+  a[i] = f2bf(v);
+}
+
+// ---------------------------------------------------------------- epilogues
+
+struct EpiRaw {  // out[b][n] = acc
+  float* out;
+  int ld;
+  __device__ void operator()(int b, int n, float v) const { out[(size_t)b * ld + n] = v; }
+};
+
+struct EpiAdd {  // h[b][n] += acc
+  float* h;
+  int ld;
+  __device__ void operator()(int b, int n, float v) const { h[(size_t)b * ld + n] += v; }
+};
+
+// out[b][n] for n in [blockIdx.x*ROWS, +ROWS), b < B: the dot of row n of
+// the packed W [K/64][nblk][128][64] with the staged input row b.
+template <int ROWS, class Stage, class Epi>
+__global__ __launch_bounds__(256) void gemv_kernel(Stage sg, const bf16_t* __restrict__ W, int nblk, int N, int K,
+                                                   int B, Epi epi) {
+  constexpr int GV_ROWS = ROWS, J = ROWS / 8;  // rows per workgroup, 8-row groups per lane
+  __shared__ __attribute__((aligned(16))) bf16_t xs[GV_MB * GV_KCH];
+  __shared__ float red[4 * GV_ROWS * GV_MB];
+  __shared__ float sc[GV_MB];
+  __shared__ float tmp[4];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n0 = blockIdx.x * GV_ROWS;
+  const int r8 = lane >> 3, c8 = lane & 7;
+  // rows n0 + r8 + 8 j lie in the same 128-row block (ROWS | 128)
+  const int blk = n0 / SLAB_N, ra = n0 % SLAB_N + r8;
+  sg.prepare(sc, B, K, tid, tmp);
+  float acc[J][GV_MB];
+#pragma unroll
+  for (int j = 0; j < J; ++j)
+#pragma unroll
+    for (int b = 0; b < GV_MB; ++b) acc[j][b] = 0.f;
+  for (int k0 = 0; k0 < K; k0 += GV_KCH) {
+    const int n = min(GV_KCH, K - k0);
+    __syncthreads();  // the previous chunk's reads of xs are done
+    sg.fill(xs, sc, B, K, k0, n, tid);
+    __syncthreads();
+    const int s0 = k0 / 64, ns = n / 64;
+    // this wave's slabs of the chunk: s0 + wave, s0 + wave + 4, ...; all
+    // weight loads first (up to 16 per lane), then the products
+    constexpr int U = GV_KCH / 64 / 4;
+    u32x4 wv[U][J];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int sl = wave + 4 * u;
+      if (sl < ns) {
+        const bf16_t* base = W + (((size_t)(s0 + sl) * nblk + blk) * SLAB_N) * 64;
+#pragma unroll
+        for (int j = 0; j < J; ++j) wv[u][j] = *(const u32x4*)(base + (size_t)(ra + 8 * j) * 64 + c8 * 8);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int sl = wave + 4 * u;
+      if (sl < ns) {
+#pragma unroll
+        for (int b = 0; b < GV_MB; ++b)
+          if (b < B) {
+            const u32x4 xv = *(const u32x4*)(xs + b * GV_KCH + sl * 64 + c8 * 8);
+#pragma unroll
+            for (int j = 0; j < J; ++j) acc[j][b] = dot8(wv[u][j], xv, acc[j][b]);
+          }
+      }
+    }
+  }
+  // reduce over the 8 lanes of a row, then over the 4 waves
+#pragma unroll
+  for (int j = 0; j < J; ++j)
+#pragma unroll
+    for (int b = 0; b < GV_MB; ++b) {
+      float v = acc[j][b];
+      v += __shfl_xor(v, 1);
+      v += __shfl_xor(v, 2);
+      v += __shfl_xor(v, 4);
+      acc[j][b] = v;
+    }
+  if (c8 == 0)
+#pragma unroll
+    for (int j = 0; j < J; ++j)
+#pragma unroll
+      for (int b = 0; b < GV_MB; ++b) red[(wave * GV_ROWS + r8 + 8 * j) * GV_MB + b] = acc[j][b];
+  __syncthreads();
+  if (tid < GV_ROWS * GV_MB) {
+    const int row = tid / GV_MB, b = tid % GV_MB;
+    const int nn = n0 + row;
+    if (b < B && nn < N) {
+      float v = 0.f;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) v += red[(w * GV_ROWS + row) * GV_MB + b];
+      epi(b, nn, v);
+    }
+  }
+}
+
+template <class Stage, class Epi>
+hipError_t gemv(const Stage& sg, const WOperand& W, int N, int K, int B, const Epi& epi, hipStream_t s) {
+  if (B <= 0 || B > GV_MB || K % 64 || N <= 0 || W.nblk * SLAB_N < (N + 15) / 16 * 16) return hipErrorInvalidValue;
+  if ((N + 15) / 16 >= 512)
+    hipLaunchKernelGGL((gemv_kernel<16, Stage, Epi>), dim3((N + 15) / 16), dim3(256), 0, s, sg, W.p, W.nblk, N, K, B,
+                       epi);
+  else
+    hipLaunchKernelGGL((gemv_kernel<8, Stage, Epi>), dim3((N + 7) / 8), dim3(256), 0, s, sg, W.p, W.nblk, N, K, B, epi);
+  return hipGetLastError();
+}
+
+// packed QKV row of true dimension d of a head (the packing keeps every
+// rotary pair (d, d + dh/2) in one 64-row group, 32 rows apart)
+__device__ __forceinline__ int packed_row_of_dim(int d, int dh) {
+  const int half = dh / 2;
+  return d < half ? (d / 32) * 64 + d % 32 : ((d - half) / 32) * 64 + 32 + (d - half) % 32;
+}
+
+// One (b, h, split): keys [split*ATT_KC, min(pos+1, (split+1)*ATT_KC)).
+// qkv [B][qkv_n] fp32 in the packed row order; caches [B][Hkv][L_cap][DH].
+template <int DH>
+__global__ __launch_bounds__(256) void attn_decode_kernel(const float* __restrict__ qkv, int qkv_n,
+                                                          const float* __restrict__ rope_cos,
+                                                          const float* __restrict__ rope_sin, bf16_t* kc, bf16_t* vc,
+                                                          int L_cap, int pos, int B, int H, int Hkv, float scale_log2,
+                                                          int nsplit, float* __restrict__ part) {
+  constexpr int DL = DH / 8;  // dims per lane (8 lanes per key)
+  __shared__ float sq[DH];
+  __shared__ bf16_t knew[DH], vnew[DH];
+  __shared__ float wm[4], wl[4];
+  __shared__ float wo[4][DH];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int split = blockIdx.x % nsplit, bh = blockIdx.x / nsplit, h = bh % H, b = bh / H;
+  const int hk = h / (H / Hkv);
+  const int half = DH / 2;
+  const float* row = qkv + (size_t)b * qkv_n;
+  const bool last = (split + 1) * ATT_KC > pos;
+  // q (and for the split holding pos, the new key and value) after RoPE, bf16-rounded as the prefill stores them
+  if (tid < DH) {
+    const int d = tid;
+    const float* qh = row + (size_t)h * DH;
+    const float* kh = row + (size_t)(H + hk) * DH;
+    const float* vh = row + (size_t)(H + Hkv + hk) * DH;
+    const int dp = d < half ? d + half : d - half;
+    float qv = qh[packed_row_of_dim(d, DH)], kv = kh[packed_row_of_dim(d, DH)];
+    if (rope_cos) {
+      const int i = d < half ? d : d - half;
+      const float c = rope_cos[(size_t)pos * half + i], s = rope_sin[(size_t)pos * half + i];
+      const float qp = qh[packed_row_of_dim(dp, DH)], kp = kh[packed_row_of_dim(dp, DH)];
+      qv = d < half ? qv * c - qp * s : qv * c + qp * s;
+      kv = d < half ? kv * c - kp * s : kv * c + kp * s;
+    }
+    sq[d] = bf2f(f2bf(qv)) * scale_log2;
+    if (last) {
+      knew[d] = f2bf(kv);
+      vnew[d] = f2bf(vh[packed_row_of_dim(d, DH)]);
+      // one writer per KV head appends the token to the cache
+      if (h % (H / Hkv) == 0) {
+        kc[(((size_t)b * Hkv + hk) * L_cap + pos) * DH + d] = knew[d];
+        vc[(((size_t)b * Hkv + hk) * L_cap + pos) * DH + d] = vnew[d];
+      }
+    }
+  }
+  __syncthreads();
+  const int g = lane >> 3, i8 = lane & 7;
+  float q[DL];
+#pragma unroll
+  for (int e = 0; e < DL; ++e) q[e] = sq[i8 * DL + e];
+  float m = -INFINITY, l = 0.f, o[DL];
+#pragma unroll
+  for (int e = 0; e < DL; ++e) o[e] = 0.f;
+  const int kbeg = split * ATT_KC, kend = min(pos + 1, kbeg + ATT_KC);
+  const bf16_t* kb = kc + ((size_t)b * Hkv + hk) * L_cap * DH;
+  const bf16_t* vb = vc + ((size_t)b * Hkv + hk) * L_cap * DH;
+  for (int j = kbeg + wave * 8 + g; j < kend; j += 32) {
+    float kk[DL], vv[DL];
+    if (j == pos) {
+#pragma unroll
+      for (int e = 0; e < DL; ++e) {
+        kk[e] = bf2f(knew[i8 * DL + e]);
+        vv[e] = bf2f(vnew[i8 * DL + e]);
+      }
+    } else {
+#pragma unroll
+      for (int c = 0; c < DL / 8; ++c) {
+        const u32x4 kw = *(const u32x4*)(kb + (size_t)j * DH + i8 * DL + c * 8);
+        const u32x4 vw = *(const u32x4*)(vb + (size_t)j * DH + i8 * DL + c * 8);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          kk[c * 8 + 2 * t] = bf_lo(kw[t]);
+          kk[c * 8 + 2 * t + 1] = bf_hi(kw[t]);
+          vv[c * 8 + 2 * t] = bf_lo(vw[t]);
+          vv[c * 8 + 2 * t + 1] = bf_hi(vw[t]);
+        }
+      }
+    }
+    float sdot = 0.f;
+#pragma unroll
+    for (int e = 0; e < DL; ++e) sdot += q[e] * kk[e];
+    sdot += __shfl_xor(sdot, 1);
+    sdot += __shfl_xor(sdot, 2);
+    sdot += __shfl_xor(sdot, 4);
+    const float mn = fmaxf(m, sdot);
+    const float a = exp2f(m - mn), p = exp2f(sdot - mn);
+    l = l * a + p;
+#pragma unroll
+    for (int e = 0; e < DL; ++e) o[e] = o[e] * a + p * vv[e];
+    m = mn;
+  }
+  // combine the 8 key groups of the wave (lanes 8 apart share dims)
+#pragma unroll
+  for (int off = 8; off < 64; off <<= 1) {
+    const float mo = __shfl_xor(m, off), lo = __shfl_xor(l, off);
+    const float mn = fmaxf(m, mo);
+    const float a = (m == -INFINITY) ? 0.f : exp2f(m - mn), ao = (mo == -INFINITY) ? 0.f : exp2f(mo - mn);
+    l = l * a + lo * ao;
+#pragma unroll
+    for (int e = 0; e < DL; ++e) o[e] = o[e] * a + __shfl_xor(o[e], off) * ao;
+    m = mn;
+  }
+  if (lane < 8) {
+#pragma unroll
+    for (int e = 0; e < DL; ++e) wo[wave][i8 * DL + e] = o[e];
+    if (lane == 0) {
+      wm[wave] = m;
+      wl[wave] = l;
+    }
+  }
+  __syncthreads();
+  float* out = part + (((size_t)b * H + h) * nsplit + split) * (2 + DH);
+  if (tid < DH) {
+    float mx = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) mx = fmaxf(mx, wm[w]);
+    float lsum = 0.f, osum = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float a = wm[w] == -INFINITY ? 0.f : exp2f(wm[w] - mx);
+      lsum += a * wl[w];
+      osum += a * wo[w][tid];
+    }
+    out[2 + tid] = osum;
+    if (tid == 0) {
+      out[0] = mx;
+      out[1] = lsum;
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t decode_qkv(const float* h, const float* g, float eps, const WOperand& W, float* raw, int B, int N, int K,
+                      hipStream_t s) {
+  return gemv(StageNorm{h, g, eps}, W, N, K, B, EpiRaw{raw, N}, s);
+}
+
+hipError_t decode_attention(const float* qkv, int qkv_n, const float* rope_cos, const float* rope_sin, bf16_t* kc,
+                            bf16_t* vc, int L_cap, int pos, int B, int H, int Hkv, int dh, float* part, int* nsplit,
+                            hipStream_t s) {
+  if (B <= 0 || H % Hkv || pos < 0 || pos >= L_cap) return hipErrorInvalidValue;
+  const int ns = pos / ATT_KC + 1;
+  *nsplit = ns;
+  const float scale_log2 = 1.4426950408889634f / sqrtf((float)dh);
+  if (dh == 128)
+    hipLaunchKernelGGL((attn_decode_kernel<128>), dim3(B * H * ns), dim3(256), 0, s, qkv, qkv_n, rope_cos, rope_sin,
+                       kc, vc, L_cap, pos, B, H, Hkv, scale_log2, ns, part);
+  else if (dh == 64)
+    hipLaunchKernelGGL((attn_decode_kernel<64>), dim3(B * H * ns), dim3(256), 0, s, qkv, qkv_n, rope_cos, rope_sin,
+                       kc, vc, L_cap, pos, B, H, Hkv, scale_log2, ns, part);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t decode_oproj(const float* part, int nsplit, int H, int dh, const WOperand& W, float* h, bf16_t* o, int B,
+                        int N, hipStream_t s) {
+  const int n = B * H * dh;
+  hipLaunchKernelGGL(combine_kernel, dim3((n + 255) / 256), dim3(256), 0, s, part, nsplit, H, dh, B, o);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return gemv(StageCopy{o}, W, N, H * dh, B, EpiAdd{h, N}, s);
+}
+
+hipError_t decode_up(const float* h, const float* g, float eps, const WOperand& W, float* gu, int B, int N, int K,
+                     hipStream_t s) {
+  return gemv(StageNorm{h, g, eps}, W, N, K, B, EpiRaw{gu, N}, s);
+}
+
+hipError_t decode_down(const float* gu, int F, int fpad, const WOperand& W, float* h, bf16_t* a, int B, int N,
+                       hipStream_t s) {
+  const int n = B * fpad;
+  hipLaunchKernelGGL(swiglu_kernel, dim3((n + 255) / 256), dim3(256), 0, s, gu, F, fpad, B, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return gemv(StageCopy{a}, W, N, fpad, B, EpiAdd{h, N}, s);
+}
+
+}  // namespace vla

@@ -72,6 +72,29 @@ hipError_t gemm_bf16_qkv(const bf16_t* A, int lda, const WOperand& W, const QkvA
 hipError_t attention_bf16(const bf16_t* q, const bf16_t* k, const bf16_t* vt, int ldvt, bf16_t* o, int B, int H,
                           int Hkv, int L, int dh, bool causal, hipStream_t s);
 
+// ------------------------------------------------------------ bf16 decode step
+// One new token for each of B <= 4 sequences (decode_bf16.hip).  W operands
+// are the packed resident weights; fp32 rows [B][...] throughout.
+// QKV (and gate/up): raw[b][n] = (RMSNorm(h[b]) g) . W[n], packed row order.
+hipError_t decode_qkv(const float* h, const float* g, float eps, const WOperand& W, float* raw, int B, int N, int K,
+                      hipStream_t s);
+// Attention of the token at position pos over cache rows [0, pos] of
+// kc/vc [B][Hkv][L_cap][dh]: RoPE on q and the new key, the new key and value
+// appended at pos, split-key partials part[B][H][nsplit][2 + dh] (max in log2
+// units, sum, unnormalised output); *nsplit = pos / 256 + 1.
+hipError_t decode_attention(const float* qkv, int qkv_n, const float* rope_cos, const float* rope_sin, bf16_t* kc,
+                            bf16_t* vc, int L_cap, int pos, int B, int H, int Hkv, int dh, float* part, int* nsplit,
+                            hipStream_t s);
+// o[b] = combine(part)[b] (bf16 scratch [B][H*dh]); h[b] += o[b] . W^T
+hipError_t decode_oproj(const float* part, int nsplit, int H, int dh, const WOperand& W, float* h, bf16_t* o, int B,
+                        int N, hipStream_t s);
+hipError_t decode_up(const float* h, const float* g, float eps, const WOperand& W, float* gu, int B, int N, int K,
+                     hipStream_t s);
+// a[b] = swiglu(gu[b]) (bf16 scratch [B][fpad]); h[b] += a[b] . W^T (the
+// down projection over the padded width fpad)
+hipError_t decode_down(const float* gu, int F, int fpad, const WOperand& W, float* h, bf16_t* a, int B, int N,
+                       hipStream_t s);
+
 // ----------------------------------------------------- norms and elementwise
 // y[M][d] = norm(x[M][d]) (fp32 in); RMSNorm when beta == NULL and !layernorm.
 hipError_t rmsnorm_bf16(const float* x, const float* g, float eps, bf16_t* y, int M, int d, hipStream_t s);

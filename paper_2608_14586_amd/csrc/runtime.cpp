@@ -703,6 +703,84 @@ Status run_blocks(vla_ctx* c, uint64_t frame_id, const void* tokens, vla_dtype i
   return OK;
 }
 
+// One decode step of decoder blocks [0, k): B sequences, one token each at
+// position pos, over the caller's device KV cache [k][2][B][Hkv][L_cap][dh].
+Status decode_step(vla_ctx* c, uint64_t frame_id, const void* x, int B, int pos, int k, void* kv_cache, int L_cap,
+                   vla_boundary* out) {
+  if (!c->llm.present) return fail(VLA_ERR_INVALID_ARG, "context has no decoder stack");
+  const Stack& s = c->llm;
+  const vla_stack_cfg& cf = s.c;
+  if (!x || !out || !out->hidden || !kv_cache) return fail(VLA_ERR_INVALID_ARG, "NULL token / boundary / cache");
+  if (!s.bf16()) return fail(VLA_ERR_UNSUPPORTED, "decode steps run on bf16 stacks");
+  if (out->out_dtype != VLA_BF16 && out->out_dtype != VLA_F32) return fail(VLA_ERR_INVALID_ARG, "bad out_dtype");
+  if (out->kv) return fail(VLA_ERR_INVALID_ARG, "a decode step appends to the device cache; boundary kv must be NULL");
+  if (k < 0 || k > cf.n_blocks) return fail(VLA_ERR_SHAPE, "k=%d outside [0, %d]", k, cf.n_blocks);
+  if (B <= 0 || B > 4 || B > cf.max_batch) return fail(VLA_ERR_SHAPE, "decode batch %d outside [1, min(4, max_batch)]", B);
+  if (pos < 0 || pos >= L_cap) return fail(VLA_ERR_SHAPE, "position %d outside the cache [0, %d)", pos, L_cap);
+  if (cf.use_rope && pos >= cf.max_tokens)
+    return fail(VLA_ERR_SHAPE, "position %d beyond the rotary tables (max_tokens %d)", pos, cf.max_tokens);
+  for (int l = 0; l < k; ++l)
+    if (!s.blocks[l].loaded) return fail(VLA_ERR_NOT_LOADED, "decoder block %d has no weights", l);
+  if (!is_device(kv_cache)) return fail(VLA_ERR_INVALID_ARG, "the KV cache must be device memory");
+  const int d = cf.d_model, H = cf.n_heads, Hkv = cf.n_kv_heads, dh = cf.head_dim;
+  const size_t n = (size_t)B * d;
+  const size_t hid_bytes = n * dtype_size(out->out_dtype);
+  if (out->hidden_bytes < hid_bytes) return fail(VLA_ERR_SHAPE, "hidden buffer %zu bytes < %zu", out->hidden_bytes, hid_bytes);
+  if (!is_pinned_host(out->hidden)) return fail(VLA_ERR_NOT_PINNED, "hidden buffer is not pinned host memory");
+  // scratch borrowed from the prefill workspace
+  Workspace& ws = c->ws[VLA_STACK_LLM];
+  const size_t M = s.m_max;
+  const int nsplit = pos / 256 + 1;
+  if ((size_t)B * s.qkv_n * 4 > M * s.hd * 2 || (size_t)B * H * nsplit * (2 + dh) * 4 > M * s.hd * 2 ||
+      (size_t)B * 2 * s.f_pad * 4 > M * s.f_pad * 2 || (size_t)B * s.hd > M * d || (size_t)B * s.f_pad > M * d)
+    return fail(VLA_ERR_SHAPE, "workspace too small for a decode step at position %d (raise max_tokens)", pos);
+  for (auto& sl : c->slots)
+    if (sl.used && sl.frame_id == frame_id)
+      return fail(VLA_ERR_INVALID_ARG, "frame %llu is already in flight", (unsigned long long)frame_id);
+
+  Slot& sl = c->slots[c->next_slot];
+  c->next_slot = (c->next_slot + 1) % NSLOT;
+  Status st = retire_slot(c, sl);
+  if (st.code) return st;
+  c->history.erase(frame_id);
+  sl.frame_id = frame_id;
+  sl.used = true;
+  out->frame_id = frame_id;
+  hipStream_t cs = c->compute;
+  HIPTRY(hipEventRecord(sl.ev_start, cs));
+  if ((st = intake(c, VLA_STACK_LLM, VLA_BF16, x, n)).code) return st;
+  float* h = ws.h;
+  float* raw = (float*)ws.q;
+  float* part = (float*)ws.o;
+  float* gu = (float*)ws.act;
+  bf16_t* obuf = (bf16_t*)ws.x;    // combined attention output [B][H*dh]
+  bf16_t* abuf = (bf16_t*)ws.tok;  // gated activation [B][f_pad] (the intake is done with it)
+  const size_t layer = (size_t)B * Hkv * L_cap * dh;
+  for (int l = 0; l < k; ++l) {
+    const Stack::Block& w = s.blocks[l];
+    bf16_t* kc = (bf16_t*)kv_cache + (size_t)l * 2 * layer;
+    bf16_t* vc = kc + layer;
+    int ns = 0;
+    PLAUNCH(c, VLA_STACK_LLM, VLA_K_QKV, vla::decode_qkv(h, w.n1g, cf.norm_eps, Stack::packed(w.w_qkv, s.qkv_n), raw, B, s.qkv_n, d, cs));
+    PLAUNCH(c, VLA_STACK_LLM, VLA_K_ATTN, vla::decode_attention(raw, s.qkv_n, cf.use_rope ? c->rope_cos : nullptr,
+                                                             cf.use_rope ? c->rope_sin : nullptr, kc, vc, L_cap, pos, B,
+                                                             H, Hkv, dh, part, &ns, cs));
+    PLAUNCH(c, VLA_STACK_LLM, VLA_K_OPROJ, vla::decode_oproj(part, ns, H, dh, Stack::packed(w.w_o, d), h, obuf, B, d, cs));
+    PLAUNCH(c, VLA_STACK_LLM, VLA_K_MLP_UP, vla::decode_up(h, w.n2g, cf.norm_eps, Stack::packed(w.w_up, 2 * s.f_pad), gu, B, 2 * s.f_pad, d, cs));
+    PLAUNCH(c, VLA_STACK_LLM, VLA_K_MLP_DOWN, vla::decode_down(gu, cf.d_ff, s.f_pad, Stack::packed(w.w_down, d), h, abuf, B, d, cs));
+  }
+  if (out->out_dtype == VLA_BF16)
+    PLAUNCH(c, VLA_STACK_LLM, VLA_K_OTHER, vla::f32_to_bf16(h, (bf16_t*)sl.hid, n, cs));
+  else
+    HIPTRY(hipMemcpyAsync(sl.hid, h, n * 4, hipMemcpyDeviceToDevice, cs));
+  HIPTRY(hipEventRecord(sl.ev_done, cs));
+  HIPTRY(hipStreamWaitEvent(c->copy, sl.ev_done, 0));
+  HIPTRY(hipEventRecord(sl.ev_hid, c->copy));
+  HIPTRY(hipMemcpyAsync(out->hidden, sl.hid, hid_bytes, hipMemcpyDeviceToHost, c->copy));
+  HIPTRY(hipEventRecord(sl.ev_copied, c->copy));
+  return OK;
+}
+
 Status run_encoder(vla_ctx* c, const void* patches, int n_img, int L, void* out_dev) {
   if (!c->enc.present) return fail(VLA_ERR_INVALID_ARG, "context has no encoder stack");
   const Stack& s = c->enc;
@@ -919,6 +997,17 @@ vla_status vla_run_blocks(vla_ctx* ctx, uint64_t frame_id, const void* tokens, v
   try {
     if (hipSetDevice(ctx->device) != hipSuccess) return finish(ctx, fail(VLA_ERR_HIP, "hipSetDevice failed"));
     return finish(ctx, run_blocks(ctx, frame_id, tokens, in_dtype, B, L, k_begin, k_end, out));
+  } catch (...) {
+    return finish(ctx, fail(VLA_ERR_INVALID_ARG, "internal error"));
+  }
+}
+
+vla_status vla_decode_step(vla_ctx* ctx, uint64_t frame_id, const void* x, int B, int pos, int k, void* kv_cache,
+                           int L_cap, vla_boundary* out) {
+  if (!ctx) return finish(nullptr, fail(VLA_ERR_INVALID_ARG, "NULL context"));
+  try {
+    if (hipSetDevice(ctx->device) != hipSuccess) return finish(ctx, fail(VLA_ERR_HIP, "hipSetDevice failed"));
+    return finish(ctx, decode_step(ctx, frame_id, x, B, pos, k, kv_cache, L_cap, out));
   } catch (...) {
     return finish(ctx, fail(VLA_ERR_INVALID_ARG, "internal error"));
   }

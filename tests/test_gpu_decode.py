@@ -1,0 +1,133 @@
+"""Decode steps across the boundary (vla_decode_step): decoder blocks [0, k) for
+one new token per sequence over the KV cache a prefix handed over.
+
+Pin: by causality, the step at position p equals row p of a prefill over the
+p + 1 tokens, so the oracle is its own prefill of the longer sequence."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from synth.configs import llama_like, Workload
+
+from paper_2608_14586_amd import binding as vb
+from prefix_cases import log, rel_l2
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(shape, B, L, k, steps, name, out_dtype="f32"):
+    import torch
+    wl = Workload(name, "bf16", shape, None)
+    W = [synth.llm_block_weights(wl, l, perturbed=True) for l in range(k)]
+    d, Hkv, dh = shape.d_model, shape.n_kv_heads, shape.head_dim
+    L_cap = L + steps + 5
+    ctx = vb.Context(llm=vb.stack_cfg(shape, "bf16", max_tokens=L_cap, max_batch=B, n_blocks=k))
+    for l in range(k):
+        ctx.vla_load_block_weights(vb.VLA_STACK_LLM, l, W[l])
+    toks = synth.normal_bf16(synth.seed_of(name, "tok"), (B, L + steps, d))
+    bnd = vb.Boundary(B, L, d, k, Hkv, dh)
+    ctx.vla_run_prefix(1, np.ascontiguousarray(toks[:, :L]), B, L, k, bnd)
+    ctx.vla_wait_boundary(1, 60000)
+    cache = torch.zeros((k, 2, B, Hkv, L_cap, dh), dtype=torch.bfloat16, device="cuda")
+    cache[:, :, :, :, :L] = bnd.kv.cuda()
+    outs = []
+    for t in range(steps):
+        ob = vb.Boundary(B, 1, d, 0, Hkv, dh, out_dtype=out_dtype, with_kv=False)
+        ctx.vla_decode_step(10 + t, np.ascontiguousarray(toks[:, L + t]), B, L + t, k, cache, L_cap, ob)
+        ctx.vla_wait_boundary(10 + t, 60000)
+        outs.append(ob.hidden.float().numpy().reshape(B, d))
+    return wl, W, toks, outs, cache, ctx
+
+
+def _oracle_rows(wl, W, toks, L, steps, k):
+    Wf = [{n: synth.as_f32(a).astype(np.float64) for n, a in w.items()} for w in W]
+    x = synth.as_f32(toks).astype(np.float64)
+    h, _ = oracle.run_prefix(x, lambda l: Wf[l], wl.llm, k, dtype=np.float64, keep_kv=False)
+    return x[:, L:L + steps], h[:, L:L + steps]
+
+
+@pytest.mark.parametrize("name,shape,B,L,k", [
+    ("dec_gqa", llama_like(2, 256, 4, 2, 64, 704), 2, 77, 2),
+    ("dec_dh128", llama_like(2, 256, 2, 1, 128, 512), 1, 130, 2),
+    ("dec_split", llama_like(1, 192, 3, 3, 64, 448), 2, 300, 1),   # keys cross a 256-key split
+    ("dec_short", llama_like(3, 128, 2, 2, 64, 320), 1, 1, 3),     # a one-token prefix
+])
+def test_decode_steps_match_oracle(name, shape, B, L, k):
+    steps = 3
+    wl, W, toks, outs, _, _ = _run(shape, B, L, k, steps, name)
+    x, ref = _oracle_rows(wl, W, toks, L, steps, k)
+    for t in range(steps):
+        for b in range(B):
+            # the blocks' update of the residual, at the prefix's 1e-2 bar
+            e = rel_l2(outs[t][b] - x[b, t], ref[b, t] - x[b, t])
+            log("%s step %d seq %d: update rel L2 %.2e" % (name, t, b, e))
+            assert e < 1e-2, (name, t, b, e)
+
+
+def test_decode_appends_the_prefill_keys():
+    # the cache rows a decode step appends agree with what a prefill over the
+    # longer sequence writes (bf16 rounding of nearly equal inputs apart)
+    import torch
+    shape = llama_like(2, 256, 4, 2, 64, 704)
+    B, L, k, steps = 1, 40, 2, 2
+    wl, W, toks, outs, cache, ctx = _run(shape, B, L, k, steps, "dec_keys")
+    bnd = vb.Boundary(B, L + steps, shape.d_model, k, shape.n_kv_heads, shape.head_dim)
+    ctx.vla_run_prefix(50, np.ascontiguousarray(toks), B, L + steps, k, bnd)
+    ctx.vla_wait_boundary(50, 60000)
+    got = cache[:, :, :, :, L:L + steps].float().cpu().numpy()
+    want = bnd.kv[:, :, :, :, L:L + steps].float().numpy()
+    assert rel_l2(got, want) < 1e-2
+    # rows before the new positions are untouched
+    assert torch.equal(cache[:, :, :, :, :L].cpu(), bnd.kv[:, :, :, :, :L])
+
+
+def test_decode_k0_returns_input_and_rejects_bad_calls():
+    import torch
+    shape = llama_like(1, 128, 2, 2, 64, 320)
+    wl = Workload("dec_err", "bf16", shape, None)
+    ctx = vb.Context(llm=vb.stack_cfg(shape, "bf16", max_tokens=64, max_batch=4, n_blocks=1))
+    ctx.vla_load_block_weights(vb.VLA_STACK_LLM, 0, synth.llm_block_weights(wl, 0))
+    cache = torch.zeros((1, 2, 4, 2, 64, 64), dtype=torch.bfloat16, device="cuda")
+    x = synth.normal_bf16(synth.seed_of("dec_err_x"), (2, 128))
+    ob = vb.Boundary(2, 1, 128, 0, 2, 64, out_dtype="bf16", with_kv=False)
+    ctx.vla_decode_step(1, x, 2, 5, 0, cache, 64, ob)
+    ctx.vla_wait_boundary(1, 60000)
+    assert np.array_equal(ob.hidden.view(torch.int16).numpy().view(np.uint16).reshape(2, 128), x)
+    bad = [((1, x, 2, 64, 1, cache, 64, ob), "VLA_ERR_SHAPE"),          # pos == L_cap
+           ((2, x, 5, 3, 1, cache, 64, ob), "VLA_ERR_SHAPE"),           # batch above 4
+           ((3, x, 2, 3, 2, cache, 64, ob), "VLA_ERR_SHAPE"),           # k above the resident blocks
+           ((4, x, 2, 3, 1, cache.cpu(), 64, ob), "VLA_ERR_INVALID_ARG"),  # host cache
+           ((5, x, 2, 3, 1, cache, 64, vb.Boundary(2, 1, 128, 1, 2, 64)), "VLA_ERR_INVALID_ARG")]  # kv given
+    for args, code in bad:
+        with pytest.raises(vb.VlaError) as e:
+            ctx.vla_decode_step(*args)
+        assert e.value.name == code, (args[0], e.value.name)
+
+
+def test_decode_full_size_against_gpu_prefill():
+    # 7B-shaped blocks at the bench length: the step at L against row L of the
+    # GPU's own prefill over L + 1 tokens
+    import torch
+    wl = synth.CONFIGS["sweep7b"]
+    s = wl.llm
+    L, k, B = 2048, 2, 1
+    W = [synth.llm_block_weights(wl, l) for l in range(k)]
+    ctx = vb.Context(llm=vb.stack_cfg(s, "bf16", max_tokens=L + 8, max_batch=B, n_blocks=k))
+    for l in range(k):
+        ctx.vla_load_block_weights(vb.VLA_STACK_LLM, l, W[l])
+    toks = synth.tokens(wl, frame=7, B=B, L=L + 1)
+    full = vb.Boundary(B, L + 1, s.d_model, k, s.n_kv_heads, s.head_dim, out_dtype="f32")
+    ctx.vla_run_prefix(1, toks, B, L + 1, k, full)
+    ctx.vla_wait_boundary(1, 120000)
+    cache = torch.zeros((k, 2, B, s.n_kv_heads, L + 8, s.head_dim), dtype=torch.bfloat16, device="cuda")
+    cache[:, :, :, :, :L] = full.kv[:, :, :, :, :L].cuda()
+    ob = vb.Boundary(B, 1, s.d_model, 0, s.n_kv_heads, s.head_dim, out_dtype="f32", with_kv=False)
+    ctx.vla_decode_step(2, np.ascontiguousarray(toks[:, L]), B, L, k, cache, L + 8, ob)
+    ctx.vla_wait_boundary(2, 120000)
+    x = synth.as_f32(toks[:, L])
+    got = ob.hidden.numpy().reshape(B, s.d_model)
+    want = full.hidden.numpy()[:, L]
+    e = rel_l2(got - x, want - x)
+    log("7B-shaped decode at position %d: update rel L2 vs the prefill's row %.2e" % (L, e))
+    assert e < 1e-2
