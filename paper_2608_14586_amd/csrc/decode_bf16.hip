@@ -11,13 +11,16 @@
 //    per K chunk, products and accumulation in fp32.  The activation
 //    row is built in LDS while staging: RMSNorm is fused there (QKV,
 //    gate/up; each workgroup recomputes the row's scale, d floats per row);
-//    the split-key attention combine and SwiGLU run once in small kernels
-//    whose bf16 rows the O and down projections stage as they are.
+//    SwiGLU runs once in a small kernel whose bf16 rows the down projection
+//    stages as they are, like the attention output for the O projection.
 //    Epilogues: raw fp32 store or fp32 residual add.
 //  * attn_decode_kernel: one workgroup per (sequence, head, 256-key split);
 //    applies RoPE to q and to the new key at the token's position, appends the
 //    new key and value to the cache, and writes (max, sum, unnormalised
-//    output) partials that the O projection's staging combines.
+//    output) partials that a small kernel combines into the bf16 attention
+//    output.  (Combining in the last workgroup of each head, found with a
+//    device-scope counter, needs an L2 write-back per workgroup on this
+//    multi-XCD part and measured 3x slower than the extra launch.)
 // Rounding points follow the prefill: normed activations, q and K/V after
 // RoPE, the attention output and the gated activation are bf16.
 
@@ -85,26 +88,6 @@ struct StageCopy {
   }
 };
 
-// o[b][h*dh + d] = bf16(sum_s 2^(m_s - m) o_s[d] / sum_s 2^(m_s - m) l_s) from
-// the split-key partials part[B][H][nsplit][2 + dh]; one thread per output
-__global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ part, int nsplit, int H, int dh, int B,
-                                                      bf16_t* __restrict__ o) {
-  const int i = blockIdx.x * 256 + threadIdx.x;
-  if (i >= B * H * dh) return;
-  const int d = i % dh, bh = i / dh;
-  const int stride = 2 + dh;
-  const float* p = part + (size_t)bh * nsplit * stride;
-  float m = -INFINITY;
-  for (int s = 0; s < nsplit; ++s) m = fmaxf(m, p[s * stride]);
-  float l = 0.f, acc = 0.f;
-  for (int s = 0; s < nsplit; ++s) {
-    const float w = exp2f(p[s * stride] - m);
-    l += w * p[s * stride + 1];
-    acc += w * p[s * stride + 2 + d];
-  }
-  o[i] = f2bf(acc / l);
-}
-
 // a[b][f] = bf16(silu(gate) * up) from the raw gate/up product gu[B][2*fpad]
 // in the packed row order (each group of 64 rows: 32 gate rows, then their 32
 // up rows); columns [F, fpad) are zero
@@ -151,22 +134,18 @@ __global__ __launch_bounds__(256) void gemv_kernel(Stage sg, const bf16_t* __res
   const int r8 = lane >> 3, c8 = lane & 7;
   // rows n0 + r8 + 8 j lie in the same 128-row block (ROWS | 128)
   const int blk = n0 / SLAB_N, ra = n0 % SLAB_N + r8;
-  sg.prepare(sc, B, K, tid, tmp);
   float acc[J][GV_MB];
 #pragma unroll
   for (int j = 0; j < J; ++j)
 #pragma unroll
     for (int b = 0; b < GV_MB; ++b) acc[j][b] = 0.f;
-  for (int k0 = 0; k0 < K; k0 += GV_KCH) {
-    const int n = min(GV_KCH, K - k0);
-    __syncthreads();  // the previous chunk's reads of xs are done
-    sg.fill(xs, sc, B, K, k0, n, tid);
-    __syncthreads();
-    const int s0 = k0 / 64, ns = n / 64;
-    // this wave's slabs of the chunk: s0 + wave, s0 + wave + 4, ...; all
-    // weight loads first (up to 16 per lane), then the products
-    constexpr int U = GV_KCH / 64 / 4;
-    u32x4 wv[U][J];
+  // this wave's slabs of a chunk: wave, wave + 4, ...; a chunk's weight
+  // loads (up to 16 per lane) are issued before the staging work they do not
+  // depend on, so the HBM fetch overlaps it
+  constexpr int U = GV_KCH / 64 / 4;
+  u32x4 wv[U][J];
+  auto load = [&](int k0) {
+    const int s0 = k0 / 64, ns = min(GV_KCH, K - k0) / 64;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int sl = wave + 4 * u;
@@ -176,6 +155,14 @@ __global__ __launch_bounds__(256) void gemv_kernel(Stage sg, const bf16_t* __res
         for (int j = 0; j < J; ++j) wv[u][j] = *(const u32x4*)(base + (size_t)(ra + 8 * j) * 64 + c8 * 8);
       }
     }
+  };
+  load(0);
+  sg.prepare(sc, B, K, tid, tmp);
+  for (int k0 = 0; k0 < K; k0 += GV_KCH) {
+    const int n = min(GV_KCH, K - k0), ns = n / 64;
+    __syncthreads();  // the previous chunk's reads of xs are done
+    sg.fill(xs, sc, B, K, k0, n, tid);
+    __syncthreads();
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int sl = wave + 4 * u;
@@ -189,6 +176,7 @@ __global__ __launch_bounds__(256) void gemv_kernel(Stage sg, const bf16_t* __res
           }
       }
     }
+    if (k0 + GV_KCH < K) load(k0 + GV_KCH);
   }
   // reduce over the 8 lanes of a row, then over the 4 waves
 #pragma unroll
@@ -368,6 +356,46 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const float* __restric
   }
 }
 
+// o[b][h*dh + d] = bf16(sum_s 2^(m_s - m) o_s[d] / sum_s 2^(m_s - m) l_s) over
+// the split-key partials part[B][H][nsplit][2 + dh]: one workgroup per
+// (b, h), one thread per dimension; every split's values are loaded before
+// they are combined (independent loads, not a dependent chain)
+template <int DH>
+__global__ __launch_bounds__(DH) void combine_kernel(const float* __restrict__ part, int nsplit,
+                                                     bf16_t* __restrict__ o) {
+  constexpr int MAXS = 32;
+  const int bh = blockIdx.x, d = threadIdx.x, stride = 2 + DH;
+  const float* p = part + (size_t)bh * nsplit * stride;
+  float m = -INFINITY, l = 0.f, acc = 0.f;
+  for (int s0 = 0; s0 < nsplit; s0 += MAXS) {
+    const int n = min(MAXS, nsplit - s0);
+    float ms[MAXS], ls[MAXS], os[MAXS];
+#pragma unroll
+    for (int s = 0; s < MAXS; ++s)
+      if (s < n) {
+        ms[s] = p[(s0 + s) * stride];
+        ls[s] = p[(s0 + s) * stride + 1];
+        os[s] = p[(s0 + s) * stride + 2 + d];
+      }
+    float mn = m;
+#pragma unroll
+    for (int s = 0; s < MAXS; ++s)
+      if (s < n) mn = fmaxf(mn, ms[s]);
+    const float r = m == -INFINITY ? 0.f : exp2f(m - mn);
+    l *= r;
+    acc *= r;
+#pragma unroll
+    for (int s = 0; s < MAXS; ++s)
+      if (s < n) {
+        const float w = exp2f(ms[s] - mn);
+        l += w * ls[s];
+        acc += w * os[s];
+      }
+    m = mn;
+  }
+  o[(size_t)bh * DH + d] = f2bf(acc / l);
+}
+
 }  // namespace
 
 hipError_t decode_qkv(const float* h, const float* g, float eps, const WOperand& W, float* raw, int B, int N, int K,
@@ -376,11 +404,10 @@ hipError_t decode_qkv(const float* h, const float* g, float eps, const WOperand&
 }
 
 hipError_t decode_attention(const float* qkv, int qkv_n, const float* rope_cos, const float* rope_sin, bf16_t* kc,
-                            bf16_t* vc, int L_cap, int pos, int B, int H, int Hkv, int dh, float* part, int* nsplit,
+                            bf16_t* vc, int L_cap, int pos, int B, int H, int Hkv, int dh, float* part, bf16_t* o,
                             hipStream_t s) {
   if (B <= 0 || H % Hkv || pos < 0 || pos >= L_cap) return hipErrorInvalidValue;
   const int ns = pos / ATT_KC + 1;
-  *nsplit = ns;
   const float scale_log2 = 1.4426950408889634f / sqrtf((float)dh);
   if (dh == 128)
     hipLaunchKernelGGL((attn_decode_kernel<128>), dim3(B * H * ns), dim3(256), 0, s, qkv, qkv_n, rope_cos, rope_sin,
@@ -390,16 +417,17 @@ hipError_t decode_attention(const float* qkv, int qkv_n, const float* rope_cos, 
                        kc, vc, L_cap, pos, B, H, Hkv, scale_log2, ns, part);
   else
     return hipErrorInvalidValue;
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (dh == 128)
+    hipLaunchKernelGGL((combine_kernel<128>), dim3(B * H), dim3(128), 0, s, part, ns, o);
+  else
+    hipLaunchKernelGGL((combine_kernel<64>), dim3(B * H), dim3(64), 0, s, part, ns, o);
   return hipGetLastError();
 }
 
-hipError_t decode_oproj(const float* part, int nsplit, int H, int dh, const WOperand& W, float* h, bf16_t* o, int B,
-                        int N, hipStream_t s) {
-  const int n = B * H * dh;
-  hipLaunchKernelGGL(combine_kernel, dim3((n + 255) / 256), dim3(256), 0, s, part, nsplit, H, dh, B, o);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  return gemv(StageCopy{o}, W, N, H * dh, B, EpiAdd{h, N}, s);
+hipError_t decode_oproj(const bf16_t* o, int K, const WOperand& W, float* h, int B, int N, hipStream_t s) {
+  return gemv(StageCopy{o}, W, N, K, B, EpiAdd{h, N}, s);
 }
 
 hipError_t decode_up(const float* h, const float* g, float eps, const WOperand& W, float* gu, int B, int N, int K,

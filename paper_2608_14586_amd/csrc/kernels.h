@@ -80,14 +80,13 @@ hipError_t decode_qkv(const float* h, const float* g, float eps, const WOperand&
                       hipStream_t s);
 // Attention of the token at position pos over cache rows [0, pos] of
 // kc/vc [B][Hkv][L_cap][dh]: RoPE on q and the new key, the new key and value
-// appended at pos, split-key partials part[B][H][nsplit][2 + dh] (max in log2
-// units, sum, unnormalised output); *nsplit = pos / 256 + 1.
+// appended at pos, o[B][H*dh] (bf16).  Scratch: split-key partials
+// part[B][H][pos / 256 + 1][2 + dh].
 hipError_t decode_attention(const float* qkv, int qkv_n, const float* rope_cos, const float* rope_sin, bf16_t* kc,
-                            bf16_t* vc, int L_cap, int pos, int B, int H, int Hkv, int dh, float* part, int* nsplit,
+                            bf16_t* vc, int L_cap, int pos, int B, int H, int Hkv, int dh, float* part, bf16_t* o,
                             hipStream_t s);
-// o[b] = combine(part)[b] (bf16 scratch [B][H*dh]); h[b] += o[b] . W^T
-hipError_t decode_oproj(const float* part, int nsplit, int H, int dh, const WOperand& W, float* h, bf16_t* o, int B,
-                        int N, hipStream_t s);
+// h[b] += o[b] . W^T (the O projection, o [B][K] bf16)
+hipError_t decode_oproj(const bf16_t* o, int K, const WOperand& W, float* h, int B, int N, hipStream_t s);
 hipError_t decode_up(const float* h, const float* g, float eps, const WOperand& W, float* gu, int B, int N, int K,
                      hipStream_t s);
 // a[b] = swiglu(gu[b]) (bf16 scratch [B][fpad]); h[b] += a[b] . W^T (the

@@ -760,12 +760,11 @@ Status decode_step(vla_ctx* c, uint64_t frame_id, const void* x, int B, int pos,
     const Stack::Block& w = s.blocks[l];
     bf16_t* kc = (bf16_t*)kv_cache + (size_t)l * 2 * layer;
     bf16_t* vc = kc + layer;
-    int ns = 0;
     PLAUNCH(c, VLA_STACK_LLM, VLA_K_QKV, vla::decode_qkv(h, w.n1g, cf.norm_eps, Stack::packed(w.w_qkv, s.qkv_n), raw, B, s.qkv_n, d, cs));
     PLAUNCH(c, VLA_STACK_LLM, VLA_K_ATTN, vla::decode_attention(raw, s.qkv_n, cf.use_rope ? c->rope_cos : nullptr,
                                                              cf.use_rope ? c->rope_sin : nullptr, kc, vc, L_cap, pos, B,
-                                                             H, Hkv, dh, part, &ns, cs));
-    PLAUNCH(c, VLA_STACK_LLM, VLA_K_OPROJ, vla::decode_oproj(part, ns, H, dh, Stack::packed(w.w_o, d), h, obuf, B, d, cs));
+                                                             H, Hkv, dh, part, obuf, cs));
+    PLAUNCH(c, VLA_STACK_LLM, VLA_K_OPROJ, vla::decode_oproj(obuf, s.hd, Stack::packed(w.w_o, d), h, B, d, cs));
     PLAUNCH(c, VLA_STACK_LLM, VLA_K_MLP_UP, vla::decode_up(h, w.n2g, cf.norm_eps, Stack::packed(w.w_up, 2 * s.f_pad), gu, B, 2 * s.f_pad, d, cs));
     PLAUNCH(c, VLA_STACK_LLM, VLA_K_MLP_DOWN, vla::decode_down(gu, cf.d_ff, s.f_pad, Stack::packed(w.w_down, d), h, abuf, B, d, cs));
   }
