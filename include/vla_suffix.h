@@ -59,6 +59,23 @@ vla_status vla_suffix_run(vla_suffix *s, const void *h, vla_dtype in_dtype, int 
  * inside the dynamic zone).  k == k_end copies the boundary through. */
 vla_status vla_suffix_run_from(vla_suffix *s, int k, const void *h, vla_dtype in_dtype, int B, int L, float *out);
 
+/* Host KV caches for decode steps: capacity L_cap positions for B sequences
+ * on each of the executor's blocks (B = 0 or L_cap = 0 frees them).  While
+ * set, a vla_suffix_run / _run_from over B sequences of L <= L_cap tokens
+ * records the keys (after RoPE) and values of the blocks it runs at
+ * positions [0, L). */
+vla_status vla_suffix_set_cache(vla_suffix *s, int B, int L_cap);
+
+/* One decode step on the host: blocks [k, k_end) (k_begin <= k <= k_end) for
+ * one new token of each of the cache's B sequences at position pos
+ * (pos < L_cap), attending over cache rows [0, pos] and appending its own key
+ * and value.  h[B][d] is the boundary state of the new tokens (bf16 or f32,
+ * for instance the hidden output of vla_decode_step); out[B][d] f32 receives
+ * the state after block k_end - 1.  VLA_ERR_SHAPE when B differs from the
+ * cache's or pos is outside it. */
+vla_status vla_suffix_decode_step(vla_suffix *s, int k, const void *h, vla_dtype in_dtype, int B, int pos,
+                                  float *out);
+
 /* Threads the executor uses. */
 vla_status vla_suffix_threads(const vla_suffix *s, int *n);
 

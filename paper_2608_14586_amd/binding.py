@@ -90,6 +90,8 @@ def lib():
             "vla_suffix_run": [c_void_p, c_void_p, c_int, c_int, c_int, c_void_p],
             "vla_suffix_run_from": [c_void_p, c_int, c_void_p, c_int, c_int, c_int, c_void_p],
             "vla_suffix_threads": [c_void_p, P(c_int)],
+            "vla_suffix_set_cache": [c_void_p, c_int, c_int],
+            "vla_suffix_decode_step": [c_void_p, c_int, c_void_p, c_int, c_int, c_int, c_void_p],
             "vla_pipeline_create": [c_void_p, c_void_p, c_int, P(c_void_p)],
             "vla_pipeline_push": [c_void_p, c_uint64, P(vla_boundary), c_int, c_int, c_int, c_void_p],
             "vla_pipeline_pop": [c_void_p, P(c_uint64), P(c_float), P(c_float), c_int],
@@ -306,6 +308,12 @@ class Suffix:
 
     def vla_suffix_run_from(self, k: int, h, in_dtype: int, B: int, L: int, out):
         _check(lib().vla_suffix_run_from(self.h, k, _ptr(h), in_dtype, B, L, _ptr(out)))
+
+    def vla_suffix_set_cache(self, B: int, L_cap: int):
+        _check(lib().vla_suffix_set_cache(self.h, B, L_cap))
+
+    def vla_suffix_decode_step(self, k: int, h, in_dtype: int, B: int, pos: int, out):
+        _check(lib().vla_suffix_decode_step(self.h, k, _ptr(h), in_dtype, B, pos, _ptr(out)))
 
     def vla_suffix_threads(self) -> int:
         n = c_int()

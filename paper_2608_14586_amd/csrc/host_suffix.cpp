@@ -271,6 +271,9 @@ struct Suffix {
   std::vector<uint16_t> x, q, kk, vv, o, act;
   std::vector<float> rope_cos, rope_sin;
   int rope_L = 0;
+  // KV caches of the blocks for decode steps: [block][B][Hkv][cache_L][dh] bf16
+  int cache_B = 0, cache_L = 0;
+  std::vector<std::vector<uint16_t>> kc, vc;
 };
 
 Suffix* create(const Cfg& c, int k_begin, int k_end, int n_threads) {
@@ -350,7 +353,7 @@ static void rms_rows(Pool& pool, const float* h, uint16_t* y, int ldy, int M, in
 }
 
 static void rope_tables(Suffix* s, int L) {
-  if (s->rope_L == L) return;
+  if (s->rope_L >= L) return;
   const int half = s->c.dh / 2;
   s->rope_cos.resize((size_t)L * half);
   s->rope_sin.resize((size_t)L * half);
@@ -422,30 +425,28 @@ static void attn_block(const Cfg& c, const uint16_t* q, int ldq, const Packed& K
   }
 }
 
-static void block_fwd(Suffix* s, const Block& w, int B, int L) {
+// q, k, v of rows m = b * L + r at positions pos0 + r, RoPE applied, to
+// [B][heads][L][dh] bf16 (q, kk, vv workspaces)
+static void qkv_rope(Suffix* s, const Block& w, int B, int L, int pos0) {
   const Cfg& c = s->c;
   Pool& pool = *s->pool;
   const int M = B * L, d = c.d, H = c.H, Hkv = c.Hkv, dh = c.dh, hd = H * dh, kvd = Hkv * dh;
-  const int dpad = (d + 1) / 2 * 2, hdpad = (hd + 1) / 2 * 2;
-  const int Fp = (c.F + 63) / 64 * 64;
+  const int dpad = (d + 1) / 2 * 2;
   const int half = dh / 2;
   float* h = s->h.data();
   uint16_t* x = s->x.data();
-
-  // --- attention half
   rms_rows(pool, h, x, dpad, M, d, w.g1.data(), c.eps);
-  // QKV with RoPE on q and k, scattered to [B][heads][L][dh] bf16
   uint16_t *q = s->q.data(), *kk = s->kk.data(), *vv = s->vv.data();
   const float* cs = s->rope_cos.data();
   const float* sn = s->rope_sin.data();
   gemm(pool, x, dpad, w.wqkv, M, [&](int m, int n0, const float* v, int nv) {
-    const int b = m / L, p = m % L;
+    const int b = m / L, r = m % L, p = pos0 + r;
     // a 64-column tile never straddles a head (dh is 64 or a multiple of 64)
     const int kind = n0 < hd ? 0 : (n0 < hd + kvd ? 1 : 2);
     const int base = kind == 0 ? 0 : (kind == 1 ? hd : hd + kvd);
     const int head = (n0 - base) / dh, d0 = (n0 - base) % dh;
     const int nh = kind == 0 ? H : Hkv;
-    uint16_t* dst = (kind == 0 ? q : (kind == 1 ? kk : vv)) + (((size_t)b * nh + head) * L + p) * dh + d0;
+    uint16_t* dst = (kind == 0 ? q : (kind == 1 ? kk : vv)) + (((size_t)b * nh + head) * L + r) * dh + d0;
     if (kind < 2 && c.use_rope) {
       // rotate-half pairs (i, i + dh/2) live in the same head; handle a
       // 64-column tile by reading its partner from the tile when dh == 64,
@@ -468,48 +469,42 @@ static void block_fwd(Suffix* s, const Block& w, int B, int L) {
   });
   if (c.use_rope && dh > 64) {
     pool.run(M, [&](int m) {
-      const int b = m / L, p = m % L;
+      const int b = m / L, r = m % L, p = pos0 + r;
       const float* raw = s->qkv.data() + (size_t)m * (hd + 2 * kvd);
       for (int head = 0; head < H + Hkv; ++head) {
         const bool isq = head < H;
-        const float* r = raw + (isq ? head * dh : hd + (head - H) * dh);
-        uint16_t* dst = isq ? q + (((size_t)b * H + head) * L + p) * dh : kk + (((size_t)b * Hkv + head - H) * L + p) * dh;
+        const float* rr = raw + (isq ? head * dh : hd + (head - H) * dh);
+        uint16_t* dst = isq ? q + (((size_t)b * H + head) * L + r) * dh : kk + (((size_t)b * Hkv + head - H) * L + r) * dh;
         for (int i = 0; i < half; ++i) {
           const float c0 = cs[(size_t)p * half + i], s0 = sn[(size_t)p * half + i];
-          const float a = r[i], bb = r[i + half];
+          const float a = rr[i], bb = rr[i + half];
           dst[i] = f2bf(a * c0 - bb * s0);
           dst[i + half] = f2bf(bb * c0 + a * s0);
         }
       }
     });
   }
-  // pack K and V^T per (batch, KV head)
-  std::vector<Packed> Kp(B * Hkv), Vp(B * Hkv);
-  pool.run(B * Hkv, [&](int t) {
-    const uint16_t* kh = kk + (size_t)t * L * dh;
-    const uint16_t* vh = vv + (size_t)t * L * dh;
-    pack_rows(Kp[t], L, dh, [&](int n, int k) { return kh[(size_t)n * dh + k]; });
-    pack_rows(Vp[t], dh, L, [&](int n, int k) { return vh[(size_t)k * dh + n]; });
-  });
-  const int nqb = (L + 63) / 64;
-  const float scale = 1.f / std::sqrt((float)dh);
-  uint16_t* o = s->o.data();
-  // heaviest query blocks first
-  pool.run(B * H * nqb, [&](int t) {
-    thread_local std::vector<float> S;
-    thread_local std::vector<uint16_t> P;
-    const int qb = nqb - 1 - t / (B * H), bh = t % (B * H), b = bh / H, head = bh % H;
-    const int kvh = head / (H / Hkv);
-    attn_block(c, q + ((size_t)b * H + head) * L * dh, dh, Kp[b * Hkv + kvh], Vp[b * Hkv + kvh], L, qb * 64,
-               o + (size_t)b * L * hdpad + head * dh, hdpad, scale, S, P);
-  });
-  // h += o Wo^T
-  gemm(pool, o, hdpad, w.wo, M, [&](int m, int n0, const float* v, int nv) {
+}
+
+// h += o Wo^T over M rows
+static void oproj(Suffix* s, const Block& w, int M) {
+  const Cfg& c = s->c;
+  const int d = c.d, hdpad = (c.H * c.dh + 1) / 2 * 2;
+  float* h = s->h.data();
+  gemm(*s->pool, s->o.data(), hdpad, w.wo, M, [&](int m, int n0, const float* v, int nv) {
     float* hr = h + (size_t)m * d + n0;
     for (int i = 0; i < nv; ++i) hr[i] += v[i];
   });
+}
 
-  // --- MLP half
+// h += swiglu(RMSNorm(h) Wgu^T) Wd^T over M rows
+static void mlp_half(Suffix* s, const Block& w, int M) {
+  const Cfg& c = s->c;
+  Pool& pool = *s->pool;
+  const int d = c.d, dpad = (d + 1) / 2 * 2;
+  const int Fp = (c.F + 63) / 64 * 64;
+  float* h = s->h.data();
+  uint16_t* x = s->x.data();
   rms_rows(pool, h, x, dpad, M, d, w.g2.data(), c.eps);
   uint16_t* act = s->act.data();
   const int ldact = (Fp + 1) / 2 * 2;
@@ -532,14 +527,153 @@ static void block_fwd(Suffix* s, const Block& w, int B, int L) {
       }
     }
   });
-  // h += act Wd^T
   gemm(pool, act, ldact, w.wd, M, [&](int m, int n0, const float* v, int nv) {
     float* hr = h + (size_t)m * d + n0;
     for (int i = 0; i < nv; ++i) hr[i] += v[i];
   });
 }
 
-bool run(Suffix* s, int k, const void* in, bool in_f32, int B, int L, float* out) {
+static void block_fwd(Suffix* s, int bi, int B, int L) {
+  const Block& w = s->blocks[bi];
+  const Cfg& c = s->c;
+  Pool& pool = *s->pool;
+  const int M = B * L, H = c.H, Hkv = c.Hkv, dh = c.dh, hd = H * dh;
+  const int hdpad = (hd + 1) / 2 * 2;
+  qkv_rope(s, w, B, L, 0);
+  uint16_t *q = s->q.data(), *kk = s->kk.data(), *vv = s->vv.data();
+  // keep this block's keys and values for later decode steps
+  if (s->cache_B == B && s->cache_L >= L) {
+    pool.run(B * Hkv, [&](int t) {
+      std::memcpy(s->kc[bi].data() + (size_t)t * s->cache_L * dh, kk + (size_t)t * L * dh, sizeof(uint16_t) * L * dh);
+      std::memcpy(s->vc[bi].data() + (size_t)t * s->cache_L * dh, vv + (size_t)t * L * dh, sizeof(uint16_t) * L * dh);
+    });
+  }
+  // pack K and V^T per (batch, KV head)
+  std::vector<Packed> Kp(B * Hkv), Vp(B * Hkv);
+  pool.run(B * Hkv, [&](int t) {
+    const uint16_t* kh = kk + (size_t)t * L * dh;
+    const uint16_t* vh = vv + (size_t)t * L * dh;
+    pack_rows(Kp[t], L, dh, [&](int n, int k) { return kh[(size_t)n * dh + k]; });
+    pack_rows(Vp[t], dh, L, [&](int n, int k) { return vh[(size_t)k * dh + n]; });
+  });
+  const int nqb = (L + 63) / 64;
+  const float scale = 1.f / std::sqrt((float)dh);
+  uint16_t* o = s->o.data();
+  // heaviest query blocks first
+  pool.run(B * H * nqb, [&](int t) {
+    thread_local std::vector<float> S;
+    thread_local std::vector<uint16_t> P;
+    const int qb = nqb - 1 - t / (B * H), bh = t % (B * H), b = bh / H, head = bh % H;
+    const int kvh = head / (H / Hkv);
+    attn_block(c, q + ((size_t)b * H + head) * L * dh, dh, Kp[b * Hkv + kvh], Vp[b * Hkv + kvh], L, qb * 64,
+               o + (size_t)b * L * hdpad + head * dh, hdpad, scale, S, P);
+  });
+  oproj(s, w, M);
+  mlp_half(s, w, M);
+}
+
+// Attention of one new token per sequence at position pos over cache rows
+// [0, pos] (the token's own key and value already appended): fp32 scores,
+// softmax and accumulation, bf16 output.
+static void decode_attention(Suffix* s, int bi, int B, int pos) {
+  const Cfg& c = s->c;
+  const int H = c.H, Hkv = c.Hkv, dh = c.dh, hdpad = (H * dh + 1) / 2 * 2;
+  const float scale = 1.f / std::sqrt((float)dh);
+  const uint16_t* q = s->q.data();
+  uint16_t* o = s->o.data();
+  s->pool->run(B * H, [&](int t) {
+    thread_local std::vector<float> sc;
+    sc.resize(pos + 1 + 16);
+    const int b = t / H, head = t % H, kvh = head / (H / Hkv);
+    const uint16_t* kb = s->kc[bi].data() + ((size_t)b * Hkv + kvh) * s->cache_L * dh;
+    const uint16_t* vb = s->vc[bi].data() + ((size_t)b * Hkv + kvh) * s->cache_L * dh;
+    const uint16_t* qh = q + ((size_t)b * H + head) * dh;
+    // q in fp32 vectors (dh is a multiple of 64)
+    __m512 qv[8];
+    for (int i = 0; i < dh / 16; ++i)
+      qv[i] = _mm512_mul_ps(_mm512_castsi512_ps(_mm512_slli_epi32(
+                                _mm512_cvtepu16_epi32(_mm256_loadu_si256((const __m256i*)(qh + 16 * i))), 16)),
+                            _mm512_set1_ps(scale));
+    float mx = -INFINITY;
+    for (int j = 0; j <= pos; ++j) {
+      const uint16_t* kr = kb + (size_t)j * dh;
+      __m512 acc = _mm512_setzero_ps();
+      for (int i = 0; i < dh / 16; ++i) {
+        const __m512 kf = _mm512_castsi512_ps(
+            _mm512_slli_epi32(_mm512_cvtepu16_epi32(_mm256_loadu_si256((const __m256i*)(kr + 16 * i))), 16));
+        acc = _mm512_fmadd_ps(qv[i], kf, acc);
+      }
+      sc[j] = _mm512_reduce_add_ps(acc);
+      mx = std::max(mx, sc[j]);
+    }
+    float sum = 0.f;
+    int j = 0;
+    const __m512 vm = _mm512_set1_ps(mx);
+    for (; j + 16 <= pos + 1; j += 16) {
+      const __m512 e = exp512(_mm512_sub_ps(_mm512_loadu_ps(&sc[j]), vm));
+      _mm512_storeu_ps(&sc[j], e);
+      sum += _mm512_reduce_add_ps(e);
+    }
+    for (; j <= pos; ++j) {
+      const __m512 e = exp512(_mm512_set1_ps(sc[j] - mx));
+      sc[j] = _mm_cvtss_f32(_mm512_castps512_ps128(e));
+      sum += sc[j];
+    }
+    __m512 ov[8];
+    for (int i = 0; i < dh / 16; ++i) ov[i] = _mm512_setzero_ps();
+    for (int jj = 0; jj <= pos; ++jj) {
+      const uint16_t* vr = vb + (size_t)jj * dh;
+      const __m512 pj = _mm512_set1_ps(sc[jj]);
+      for (int i = 0; i < dh / 16; ++i) {
+        const __m512 vf = _mm512_castsi512_ps(
+            _mm512_slli_epi32(_mm512_cvtepu16_epi32(_mm256_loadu_si256((const __m256i*)(vr + 16 * i))), 16));
+        ov[i] = _mm512_fmadd_ps(pj, vf, ov[i]);
+      }
+    }
+    uint16_t* orow = o + (size_t)b * hdpad + head * dh;
+    const __m512 inv = _mm512_set1_ps(1.f / sum);
+    for (int i = 0; i < dh / 16; ++i) _mm256_storeu_si256((__m256i*)(orow + 16 * i), cvt16(_mm512_mul_ps(ov[i], inv)));
+  });
+}
+
+static void block_decode(Suffix* s, int bi, int B, int pos) {
+  const Block& w = s->blocks[bi];
+  const Cfg& c = s->c;
+  const int Hkv = c.Hkv, dh = c.dh;
+  qkv_rope(s, w, B, 1, pos);
+  // append the token's key and value at pos
+  for (int t = 0; t < B * Hkv; ++t) {
+    std::memcpy(s->kc[bi].data() + ((size_t)t * s->cache_L + pos) * dh, s->kk.data() + (size_t)t * dh,
+                sizeof(uint16_t) * dh);
+    std::memcpy(s->vc[bi].data() + ((size_t)t * s->cache_L + pos) * dh, s->vv.data() + (size_t)t * dh,
+                sizeof(uint16_t) * dh);
+  }
+  decode_attention(s, bi, B, pos);
+  oproj(s, w, B);
+  mlp_half(s, w, B);
+}
+
+void set_cache(Suffix* s, int B, int L_cap) {
+  const size_t n = (size_t)B * s->c.Hkv * L_cap * s->c.dh;
+  s->cache_B = B;
+  s->cache_L = L_cap;
+  s->kc.assign(s->blocks.size(), std::vector<uint16_t>());
+  s->vc.assign(s->blocks.size(), std::vector<uint16_t>());
+  if (B <= 0 || L_cap <= 0) {
+    s->cache_B = s->cache_L = 0;
+    return;
+  }
+  for (size_t i = 0; i < s->blocks.size(); ++i) {
+    s->kc[i].assign(n, 0);
+    s->vc[i].assign(n, 0);
+  }
+}
+
+int cache_batch(const Suffix* s) { return s->cache_B; }
+int cache_len(const Suffix* s) { return s->cache_L; }
+
+// workspaces for M rows of B sequences of L tokens
+static void reserve(Suffix* s, int B, int L) {
   const Cfg& c = s->c;
   const int M = B * L, d = c.d, hd = c.H * c.dh, kvd = c.Hkv * c.dh;
   const int dpad = (d + 1) / 2 * 2, hdpad = (hd + 1) / 2 * 2;
@@ -553,15 +687,34 @@ bool run(Suffix* s, int k, const void* in, bool in_f32, int B, int L, float* out
   s->act.assign((size_t)M * ((Fp + 1) / 2 * 2), 0);
   s->gu.resize((size_t)M * 2 * Fp);
   if (c.use_rope && c.dh > 64) s->qkv.resize((size_t)M * (hd + 2 * kvd));
-  rope_tables(s, L);
+}
+
+static void load_input(Suffix* s, const void* in, bool in_f32, size_t n) {
   if (in_f32) {
-    std::memcpy(s->h.data(), in, sizeof(float) * (size_t)M * d);
+    std::memcpy(s->h.data(), in, sizeof(float) * n);
   } else {
     const uint16_t* hb = (const uint16_t*)in;
-    for (size_t i = 0; i < (size_t)M * d; ++i) s->h[i] = bf2f(hb[i]);
+    for (size_t i = 0; i < n; ++i) s->h[i] = bf2f(hb[i]);
   }
-  for (int l = k; l < s->k_end; ++l) block_fwd(s, s->blocks[l - s->k_begin], B, L);
-  std::memcpy(out, s->h.data(), sizeof(float) * (size_t)M * d);
+}
+
+bool decode(Suffix* s, int k, const void* in, bool in_f32, int B, int pos, float* out) {
+  const size_t n = (size_t)B * s->c.d;
+  reserve(s, B, 1);
+  rope_tables(s, std::max(pos + 1, s->cache_L));
+  load_input(s, in, in_f32, n);
+  for (int l = k; l < s->k_end; ++l) block_decode(s, l - s->k_begin, B, pos);
+  std::memcpy(out, s->h.data(), sizeof(float) * n);
+  return true;
+}
+
+bool run(Suffix* s, int k, const void* in, bool in_f32, int B, int L, float* out) {
+  const size_t n = (size_t)B * L * s->c.d;
+  reserve(s, B, L);
+  rope_tables(s, std::max(L, s->cache_L));
+  load_input(s, in, in_f32, n);
+  for (int l = k; l < s->k_end; ++l) block_fwd(s, l - s->k_begin, B, L);
+  std::memcpy(out, s->h.data(), sizeof(float) * n);
   return true;
 }
 

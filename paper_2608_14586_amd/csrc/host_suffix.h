@@ -28,6 +28,14 @@ bool all_loaded(const Suffix* s);
 // blocks [k, k_end) over h (bf16, or f32 when in_f32) [B][L][d] -> out f32 [B][L][d];
 // k_begin <= k <= k_end
 bool run(Suffix* s, int k, const void* in, bool in_f32, int B, int L, float* out);
+// host KV caches for decode steps ([block][B][Hkv][L_cap][dh]); a later run()
+// with this B and L <= L_cap records its keys and values; B or L_cap <= 0 frees
+void set_cache(Suffix* s, int B, int L_cap);
+int cache_batch(const Suffix* s);
+int cache_len(const Suffix* s);
+// one new token per sequence at position pos through blocks [k, k_end) over
+// the caches (rows [0, pos) filled), appending its keys and values
+bool decode(Suffix* s, int k, const void* in, bool in_f32, int B, int pos, float* out);
 
 }  // namespace host
 }  // namespace vla

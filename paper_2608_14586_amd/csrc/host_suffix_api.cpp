@@ -100,6 +100,32 @@ vla_status vla_suffix_run(vla_suffix* s, const void* h, vla_dtype in_dtype, int 
   return vla_suffix_run_from(s, s->k_begin, h, in_dtype, B, L, out);
 }
 
+vla_status vla_suffix_set_cache(vla_suffix* s, int B, int L_cap) {
+  if (!s || B < 0 || L_cap < 0) return VLA_ERR_INVALID_ARG;
+  try {
+    vla::host::set_cache(s->impl, B, L_cap);
+    return VLA_OK;
+  } catch (...) {
+    vla::host::set_cache(s->impl, 0, 0);
+    return VLA_ERR_OOM;
+  }
+}
+
+vla_status vla_suffix_decode_step(vla_suffix* s, int k, const void* h, vla_dtype in_dtype, int B, int pos,
+                                  float* out) {
+  if (!s || !h || !out || B <= 0) return VLA_ERR_INVALID_ARG;
+  if (in_dtype != VLA_BF16 && in_dtype != VLA_F32) return VLA_ERR_INVALID_ARG;
+  if (k < s->k_begin || k > s->k_end) return VLA_ERR_INVALID_ARG;
+  if (B != vla::host::cache_batch(s->impl) || pos < 0 || pos >= vla::host::cache_len(s->impl)) return VLA_ERR_SHAPE;
+  if (!vla::host::all_loaded(s->impl)) return VLA_ERR_NOT_LOADED;
+  try {
+    vla::host::decode(s->impl, k, h, in_dtype == VLA_F32, B, pos, out);
+    return VLA_OK;
+  } catch (...) {
+    return VLA_ERR_OOM;
+  }
+}
+
 vla_status vla_suffix_threads(const vla_suffix* s, int* n) {
   if (!s || !n) return VLA_ERR_INVALID_ARG;
   *n = vla::host::threads(s->impl);

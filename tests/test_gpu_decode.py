@@ -131,3 +131,45 @@ def test_decode_full_size_against_gpu_prefill():
     e = rel_l2(got - x, want - x)
     log("7B-shaped decode at position %d: update rel L2 vs the prefill's row %.2e" % (L, e))
     assert e < 1e-2
+
+
+def test_decode_across_the_boundary():
+    # the whole partitioned decode (Eq. (6) per token): blocks [0, 2) on the
+    # GPU from the prefix's KV cache, the boundary to pinned host memory,
+    # blocks [2, 4) on the host from its own cache; against the oracle's
+    # prefill over all four blocks
+    import torch
+    shape = llama_like(4, 256, 4, 2, 64, 704)
+    wl = Workload("dec_across", "bf16", shape, None)
+    W = [synth.llm_block_weights(wl, l, perturbed=True) for l in range(4)]
+    B, L, K, N, steps = 1, 60, 2, 4, 3
+    d, Hkv, dh = shape.d_model, shape.n_kv_heads, shape.head_dim
+    L_cap = L + steps + 4
+    ctx = vb.Context(llm=vb.stack_cfg(shape, "bf16", max_tokens=L_cap, max_batch=B, n_blocks=K))
+    for l in range(K):
+        ctx.vla_load_block_weights(vb.VLA_STACK_LLM, l, W[l])
+    sfx = vb.Suffix(vb.stack_cfg(shape, "bf16", max_tokens=L_cap), K, N)
+    for l in range(K, N):
+        sfx.vla_suffix_load_block_weights(l, W[l])
+    sfx.vla_suffix_set_cache(B, L_cap)
+    toks = synth.normal_bf16(synth.seed_of("dec_across_tok"), (B, L + steps, d))
+    # prefill: GPU prefix with its KV handoff, then the host suffix recording its own cache
+    bnd = vb.Boundary(B, L, d, K, Hkv, dh, out_dtype="f32")
+    ctx.vla_run_prefix(1, np.ascontiguousarray(toks[:, :L]), B, L, K, bnd)
+    ctx.vla_wait_boundary(1, 60000)
+    out = np.empty((B, L, d), np.float32)
+    sfx.vla_suffix_run(bnd.hidden.numpy(), vb.VLA_F32, B, L, out)
+    cache = torch.zeros((K, 2, B, Hkv, L_cap, dh), dtype=torch.bfloat16, device="cuda")
+    cache[:, :, :, :, :L] = bnd.kv.cuda()
+    Wf = [{n: synth.as_f32(a).astype(np.float64) for n, a in w.items()} for w in W]
+    x = synth.as_f32(toks).astype(np.float64)
+    ref, _ = oracle.run_prefix(x, lambda l: Wf[l], shape, N, dtype=np.float64, keep_kv=False)
+    for t in range(steps):
+        ob = vb.Boundary(B, 1, d, 0, Hkv, dh, out_dtype="f32", with_kv=False)
+        ctx.vla_decode_step(10 + t, np.ascontiguousarray(toks[:, L + t]), B, L + t, K, cache, L_cap, ob)
+        ctx.vla_wait_boundary(10 + t, 60000)
+        o = np.empty((B, d), np.float32)
+        sfx.vla_suffix_decode_step(K, ob.hidden.numpy().reshape(B, d), vb.VLA_F32, B, L + t, o)
+        e = rel_l2(o[0] - x[0, L + t], ref[0, L + t] - x[0, L + t])
+        log("decode across the boundary, step %d: update rel L2 %.2e" % (t, e))
+        assert e < 1e-2, (t, e)

@@ -142,3 +142,44 @@ def test_suffix_errors():
     with pytest.raises(vb.VlaError) as e:
         s.vla_suffix_run(h, vb.VLA_BF16, 1, 8, out)
     assert e.value.name == "VLA_ERR_NOT_LOADED"
+
+
+@pytest.mark.parametrize("n_blocks,d,H,Hkv,dh,F,B,L,k0,steps", [
+    (3, 256, 4, 2, 64, 704, 2, 77, 1, 3),    # GQA, two sequences
+    (2, 256, 2, 1, 128, 512, 1, 40, 0, 2),   # dh = 128 (RoPE in the second pass)
+    (2, 128, 2, 2, 64, 320, 1, 1, 0, 3),     # a one-token prefix
+])
+def test_suffix_decode_steps_match_oracle(n_blocks, d, H, Hkv, dh, F, B, L, k0, steps):
+    # the prefill records its keys and values; each decode step at position p
+    # must equal row p of a prefill over the p + 1 boundary states
+    wl, W = _case("sfx_dec_%d_%d" % (d, L), n_blocks, d, H, Hkv, dh, F)
+    seq = synth.f32_to_bf16(synth.normal_f32(synth.seed_of("sfx_dec_seq", d, L), (B, L + steps, d)))
+    s = _suffix(wl, W, k0, n_blocks)
+    s.vla_suffix_set_cache(B, L + steps + 2)
+    out = np.empty((B, L, d), np.float32)
+    s.vla_suffix_run(np.ascontiguousarray(seq[:, :L]), vb.VLA_BF16, B, L, out)
+    hf = synth.as_f32(seq)
+    ref = _oracle(wl, W, hf, k0, n_blocks)
+    for t in range(steps):
+        o = np.empty((B, d), np.float32)
+        s.vla_suffix_decode_step(k0, np.ascontiguousarray(seq[:, L + t]), vb.VLA_BF16, B, L + t, o)
+        for b in range(B):
+            e = _rel(o[b] - hf[b, L + t], ref[b, L + t] - hf[b, L + t])
+            assert e < 1e-2, (t, b, e)
+
+
+def test_suffix_decode_errors():
+    wl, W = _case("sfx_dec_err", 1, 128, 2, 2, 64, 320)
+    s = _suffix(wl, W, 0, 1)
+    h = np.zeros((1, 128), np.uint16)
+    o = np.empty((1, 128), np.float32)
+    with pytest.raises(vb.VlaError) as e:     # no cache
+        s.vla_suffix_decode_step(0, h, vb.VLA_BF16, 1, 0, o)
+    assert e.value.name == "VLA_ERR_SHAPE"
+    s.vla_suffix_set_cache(1, 8)
+    with pytest.raises(vb.VlaError) as e:     # past the cache
+        s.vla_suffix_decode_step(0, h, vb.VLA_BF16, 1, 8, o)
+    assert e.value.name == "VLA_ERR_SHAPE"
+    with pytest.raises(vb.VlaError) as e:     # batch differs from the cache's
+        s.vla_suffix_decode_step(0, np.zeros((2, 128), np.uint16), vb.VLA_BF16, 2, 3, np.empty((2, 128), np.float32))
+    assert e.value.name == "VLA_ERR_SHAPE"
