@@ -205,8 +205,58 @@ def decode_bench(args):
            "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                         "frac": round(achieved / PEAK_HBM_GBS, 4), "bytes_per_step": w_bytes + kv_bytes},
            "kernels": kern}
+    if args.decode_host_blocks > 0:
+        out["across"] = decode_across(args, ctx, wl, bnd, cache, xs, outs[0], L_cap)
     ctx.vla_destroy()
     print(json.dumps(out), flush=True)
+
+
+def decode_across(args, ctx, wl, bnd, cache, xs, ob, L_cap):
+    """One token through the whole partitioned model (Eq. (6) per token): the
+    GPU step over blocks [0, k), its boundary to pinned host memory, then the
+    host decode step over blocks [k, N) from the host's own KV cache, which
+    its prefill of the same prefix filled.  Tokens are serial (each needs the
+    previous one), so the stages add up: T_G + T_X + T_C per token."""
+    import torch
+    import synth
+    from paper_2608_14586_amd import binding as vb
+
+    s = wl.llm
+    L, k, B, T = wl.seq, args.k, args.decode_batch, len(xs)
+    N = k + args.decode_host_blocks
+    sfx = vb.Suffix(vb.stack_cfg(s, "bf16", max_tokens=L_cap), k, N, args.pipeline_threads)
+    for l in range(k, N):
+        sfx.vla_suffix_load_block_weights(l, synth.llm_block_weights(wl, l))
+    sfx.vla_suffix_set_cache(B, L_cap)
+    h = torch.empty((B, L, s.d_model), dtype=torch.float32)
+    t = time.perf_counter()
+    sfx.vla_suffix_run(bnd.hidden, vb.VLA_BF16, B, L, h)
+    prefill_ms = (time.perf_counter() - t) * 1000
+    o = torch.empty((B, s.d_model), dtype=torch.float32)
+    tg, tc = [], []
+    fid = 5000
+    for i in range(T):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        ctx.vla_decode_step(fid + i, xs[i], B, L + i, k, cache, L_cap, ob)
+        ctx.vla_wait_boundary(fid + i, 600000)
+        t1 = time.perf_counter()
+        sfx.vla_suffix_decode_step(k, ob.hidden, vb.VLA_BF16, B, L + i, o)
+        t2 = time.perf_counter()
+        tg.append((t1 - t0) * 1000)
+        tc.append((t2 - t1) * 1000)
+    tg, tc = sorted(tg[2:]), sorted(tc[2:])
+    mg, mc = tg[len(tg) // 2], tc[len(tc) // 2]
+    w_block = 2 * (s.d_model * (s.n_heads + 2 * s.n_kv_heads) * s.head_dim + s.n_heads * s.head_dim * s.d_model
+                   + 3 * s.d_model * s.d_ff)
+    kv_block = 2 * B * s.n_kv_heads * L * s.head_dim * 2
+    host_gbs = (N - k) * (w_block + kv_block) / (mc / 1000) / 1e9
+    r = {"n_blocks": N, "host_blocks": N - k, "host_threads": sfx.vla_suffix_threads(),
+         "gpu_step_ms": round(mg, 3), "host_step_ms": round(mc, 3), "token_ms": round(mg + mc, 3),
+         "host_ms_per_block": round(mc / (N - k), 3), "host_gbs": round(host_gbs, 1),
+         "host_prefill_ms": round(prefill_ms, 1), "steps": len(tc)}
+    sfx.vla_suffix_destroy()
+    return r
 
 
 def gpu_stage_factory(ctx, pats, toks, enc_out, n_img, L_img, L, fid):
@@ -422,6 +472,8 @@ def main():
                     help="measure decode steps of blocks [0,k) over the prefix's KV cache instead")
     ap.add_argument("--decode-steps", type=int, default=32)
     ap.add_argument("--decode-batch", type=int, default=1)
+    ap.add_argument("--decode-host-blocks", type=int, default=0,
+                    help="with --decode: also run blocks [k, k + n) on the host per token")
     ap.add_argument("--pipeline-frames", type=int, default=4)
     ap.add_argument("--pipeline-threads", type=int, default=0, help="host suffix threads (0: all)")
     ap.add_argument("--pipeline-adaptive", type=int, default=20, metavar="FRAMES",
