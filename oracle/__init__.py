@@ -8,7 +8,8 @@ routes through it and shares no code with it.
 It is a plain, slow, obviously-correct numpy implementation of what the prefix
 computes: the boundary hidden state after the first p whole transformer blocks
 (the paper's Eq. (5), Sec. IV-B), the prefix KV cache those blocks write, and
-the visual-encoder blocks.  Default precision is float32 (the precision the
+the visual-encoder blocks, and the encoder's stem and connector that turn
+camera images into the backbone's input tokens.  Default precision is float32 (the precision the
 prefix's parity bar is stated in); every function also runs in float64, which
 the pins use.  Block internals follow the workload definitions (LLaMA-style
 pre-RMSNorm decoder with RoPE and SwiGLU; pre-LayerNorm ViT with GELU), since
@@ -36,3 +37,4 @@ from .reference import (  # noqa: F401
     vit_block,
     transfer_bytes,
 )
+from .vision import connector, merge_patches, patch_embed, run_vision  # noqa: F401

@@ -18,7 +18,7 @@ import subprocess
 
 import numpy as np
 
-from .configs import CONFIGS, StackShape, Workload  # noqa: F401
+from .configs import CONFIGS, StackShape, VisionShape, Workload  # noqa: F401
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SO = os.path.join(_HERE, "libsynth.so")
@@ -186,6 +186,41 @@ def patches(wl: "Workload", frame: int = 0, n_img: int = None, L_img: int = None
     L_img = wl.img_tokens if L_img is None else L_img
     return _draw(seed_of(wl.name, "patches", frame, n_img, L_img), (n_img, L_img, wl.enc.d_model),
                  1.0, wl.dtype)
+
+
+def vision_weights(wl: "Workload", perturbed: bool = False) -> dict:
+    """Stem, final encoder norm and connector weights: projections, biases and
+    the position embedding ~ N(0, 0.02); LayerNorm gain 1 / shift 0, or
+    U(0.5, 1.5) / N(0, 0.1) when ``perturbed``."""
+    v, e = wl.vision, wl.enc
+    dt = wl.dtype
+    tag = (wl.name, "vision")
+    d, kin = e.d_model, v.channels * v.patch * v.patch
+    return {
+        "w_patch": _draw(seed_of(*tag, "w_patch"), (d, kin), 0.02, dt),
+        "b_patch": _draw(seed_of(*tag, "b_patch"), (d,), 0.02, dt),
+        "pos": _draw(seed_of(*tag, "pos"), (v.L_img, d), 0.02, dt),
+        "post_g": _gain(seed_of(*tag, "post_g"), d, dt, perturbed),
+        "post_b": _shift(seed_of(*tag, "post_b"), d, dt, perturbed),
+        "w_c1": _draw(seed_of(*tag, "w_c1"), (v.d_hidden, v.merge * v.merge * d), 0.02, dt),
+        "b_c1": _draw(seed_of(*tag, "b_c1"), (v.d_hidden,), 0.02, dt),
+        "w_c2": _draw(seed_of(*tag, "w_c2"), (v.d_out, v.d_hidden), 0.02, dt),
+        "b_c2": _draw(seed_of(*tag, "b_c2"), (v.d_out,), 0.02, dt),
+    }
+
+
+def images(wl: "Workload", frame: int = 0, n_img: int = None) -> np.ndarray:
+    """Camera images [n_img, C, H, W] ~ N(0, 1) (pixels after the usual
+    per-channel normalisation) for ``frame``."""
+    v = wl.vision
+    n_img = wl.n_img if n_img is None else n_img
+    return _draw(seed_of(wl.name, "images", frame, n_img), (n_img, v.channels, v.img_h, v.img_w), 1.0, wl.dtype)
+
+
+def text(wl: "Workload", frame: int = 0, T: int = None) -> np.ndarray:
+    """Text token embeddings [T, d_llm] ~ N(0, 1) that follow the visual tokens."""
+    T = wl.text_tokens if T is None else T
+    return _draw(seed_of(wl.name, "text", frame, T), (T, wl.llm.d_model), 1.0, wl.dtype)
 
 
 def as_f32(a: np.ndarray) -> np.ndarray:
