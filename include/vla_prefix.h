@@ -148,6 +148,69 @@ vla_status vla_load_block_weights(vla_ctx *ctx, vla_stack which, int block, cons
 vla_status vla_run_encoder(vla_ctx *ctx, uint64_t frame_id, const void *patches, int n_img, int L_img,
                            void *out_dev);
 
+/*
+ * Front and back of the visual encoder: E(x_t) of Eq. (5) from the frame's
+ * camera images (Eq. (1)), the part of the GPU stage that Sec. IV-A puts
+ * before the backbone.  The paper does not describe either end; this library
+ * computes the common ViT patch embedding and a LLaVA-style projector:
+ *   images [n_img][channels][img_h][img_w] (stack dtype; normalised pixels)
+ *   -> per image, patch x patch squares in row-major grid order (gh x gw,
+ *      gh = img_h / patch, gw = img_w / patch), each flattened channel first,
+ *      then pixel row, then pixel column, times w_patch^T, + b_patch
+ *      + pos[grid index]                  (a stride-patch convolution)
+ *   -> every block of the encoder stack (each image attended on its own)
+ *   -> LayerNorm(post_g, post_b)
+ *   -> merge of merge x merge neighbouring patches into one token: token
+ *      (ty, tx) of an image, row-major over (gh/merge) x (gw/merge), holds the
+ *      features of patches (ty*merge + dy, tx*merge + dx), dy outer, dx
+ *      inner, side by side (merge*merge*d_enc wide)
+ *   -> GELU(m w_c1^T + b_c1) w_c2^T + b_c2  = the visual tokens, d_out wide.
+ * Needs: img_h, img_w multiples of patch; gh, gw multiples of merge;
+ * gh * gw <= the encoder's max_tokens; bf16: d_hidden, d_out multiples of 64;
+ * fp32: d_out a multiple of 4.
+ */
+typedef struct {
+  int channels, img_h, img_w, patch, merge;
+  int d_hidden; /* connector MLP width */
+  int d_out;    /* token width (the decoder's d_model) */
+  float norm_eps;
+} vla_vision_cfg;
+
+/* Host weights of the vision front, the encoder stack's dtype, all required:
+ * w_patch[d_enc][channels*patch*patch] b_patch[d_enc] pos[gh*gw][d_enc]
+ * post_g[d_enc] post_b[d_enc] w_c1[d_hidden][merge*merge*d_enc] b_c1[d_hidden]
+ * w_c2[d_out][d_hidden] b_c2[d_out].  Copied (and re-laid-out) on load. */
+typedef struct {
+  const void *w_patch, *b_patch, *pos, *post_g, *post_b, *w_c1, *b_c1, *w_c2, *b_c2;
+} vla_vision_weights;
+
+/* Device bytes vla_attach_vision needs for this encoder stack and vision
+ * front: weights plus scratch for max_batch images. */
+vla_status vla_query_vision_sizes(const vla_stack_cfg *enc, const vla_vision_cfg *vis, size_t *bytes);
+
+/* Give a context with an encoder stack a vision front, in caller-owned device
+ * memory dev_mem of `bytes` (>= vla_query_vision_sizes, 256-byte aligned;
+ * the library allocates nothing).  Waits for the context's work in flight;
+ * attaching again replaces the previous front (its weights must be loaded
+ * again).  The memory must outlive the context or the next attach. */
+vla_status vla_attach_vision(vla_ctx *ctx, const vla_vision_cfg *vis, void *dev_mem, size_t bytes);
+
+/* Copy the vision front's weights from host memory.  Synchronous. */
+vla_status vla_load_vision_weights(vla_ctx *ctx, const vla_vision_weights *w);
+
+/* One frame's backbone input, E(x_t): images[n_img][channels][img_h][img_w]
+ * (host or device, n_img <= the encoder's max_batch) through the stem, the
+ * encoder blocks and the connector into tokens_dev rows [0, V), V = n_img *
+ * (gh/merge) * (gw/merge), camera by camera; then text[L_text][d_out] (host
+ * or device, may be NULL when L_text = 0) into rows [V, V + L_text).
+ * tokens_dev: device memory, 16-byte aligned, tokens_bytes >= (V + L_text) *
+ * d_out * element size, in the encoder stack's dtype -- with a decoder stack
+ * of the same dtype and d_model = d_out it is vla_run_prefix's input as it
+ * is (B = 1, L = V + L_text).  Runs on the encoder stream and orders itself
+ * with the decoder as vla_run_encoder does.  Enqueued; returns after launch. */
+vla_status vla_run_vision(vla_ctx *ctx, uint64_t frame_id, const void *images, int n_img, const void *text,
+                          int L_text, void *tokens_dev, size_t tokens_bytes);
+
 /* Prefix: decoder blocks [0, k) over tokens[B][L][d] (host or device, stack
  * dtype) as one causal prefill; the boundary h^(k) and the KV cache of the k
  * blocks are copied to `out` on the copy stream, each layer's KV as soon as
@@ -203,7 +266,9 @@ typedef enum {
   VLA_K_MLP_UP = 4,   /* gate/up + SwiGLU, or fc1 + GELU */
   VLA_K_MLP_DOWN = 5, /* down / fc2 + residual */
   VLA_K_OTHER = 6,    /* intake, boundary cast (fp32 path: its extra kernels) */
-  VLA_K_COUNT = 7
+  VLA_K_STEM = 7,     /* vision front: patch rows + patch embedding GEMM */
+  VLA_K_CONNECTOR = 8, /* vision back: final norm + merge, connector MLP */
+  VLA_K_COUNT = 9
 } vla_kernel_class;
 
 /* Start (enable != 0, clearing previous totals) or stop timing every kernel

@@ -24,7 +24,7 @@ STATUS = {0: "VLA_OK", -1: "VLA_ERR_INVALID_ARG", -2: "VLA_ERR_SHAPE", -3: "VLA_
           -8: "VLA_ERR_UNSUPPORTED", -9: "VLA_ERR_UNKNOWN_FRAME"}
 VLA_BF16, VLA_F32 = 0, 1
 VLA_STACK_LLM, VLA_STACK_ENC = 0, 1
-KERNEL_CLASSES = ["norm", "qkv", "attn", "oproj", "mlp_up", "mlp_down", "other"]
+KERNEL_CLASSES = ["norm", "qkv", "attn", "oproj", "mlp_up", "mlp_down", "other", "stem", "connector"]
 
 
 class VlaError(RuntimeError):
@@ -54,6 +54,18 @@ class vla_boundary(ctypes.Structure):
                 ("out_dtype", c_int), ("frame_id", c_uint64)]
 
 
+class vla_vision_cfg(ctypes.Structure):
+    _fields_ = [("channels", c_int), ("img_h", c_int), ("img_w", c_int), ("patch", c_int), ("merge", c_int),
+                ("d_hidden", c_int), ("d_out", c_int), ("norm_eps", c_float)]
+
+
+_VISION_FIELDS = ["w_patch", "b_patch", "pos", "post_g", "post_b", "w_c1", "b_c1", "w_c2", "b_c2"]
+
+
+class vla_vision_weights(ctypes.Structure):
+    _fields_ = [(n, c_void_p) for n in _VISION_FIELDS]
+
+
 _lib = None
 
 
@@ -76,6 +88,10 @@ def lib():
             "vla_run_prefix": [c_void_p, c_uint64, c_void_p, c_int, c_int, c_int, P(vla_boundary)],
             "vla_run_blocks": [c_void_p, c_uint64, c_void_p, c_int, c_int, c_int, c_int, c_int, P(vla_boundary)],
             "vla_decode_step": [c_void_p, c_uint64, c_void_p, c_int, c_int, c_int, c_void_p, c_int, P(vla_boundary)],
+            "vla_query_vision_sizes": [P(vla_stack_cfg), P(vla_vision_cfg), P(c_size_t)],
+            "vla_attach_vision": [c_void_p, P(vla_vision_cfg), c_void_p, c_size_t],
+            "vla_load_vision_weights": [c_void_p, P(vla_vision_weights)],
+            "vla_run_vision": [c_void_p, c_uint64, c_void_p, c_int, c_void_p, c_int, c_void_p, c_size_t],
             "vla_profile": [c_void_p, c_int],
             "vla_profile_read": [c_void_p, c_int, c_int, P(ctypes.c_double), P(c_int)],
             "vla_wait_boundary": [c_void_p, c_uint64, c_int],
@@ -133,6 +149,19 @@ def stack_cfg(shape, dtype: str, max_tokens: int, max_batch: int = 1, n_blocks: 
         max_batch=max_batch, norm_is_layernorm=int(shape.norm_is_layernorm), mlp_is_gelu=int(shape.mlp_is_gelu),
         causal=int(shape.causal), use_rope=int(shape.use_rope), has_bias=int(shape.has_bias),
         norm_eps=shape.norm_eps, rope_base=shape.rope_base, dtype=VLA_BF16 if dtype == "bf16" else VLA_F32)
+
+
+def vision_cfg(vis) -> vla_vision_cfg:
+    """A vla_vision_cfg from any object with the VisionShape attributes."""
+    return vla_vision_cfg(channels=vis.channels, img_h=vis.img_h, img_w=vis.img_w, patch=vis.patch, merge=vis.merge,
+                          d_hidden=vis.d_hidden, d_out=vis.d_out, norm_eps=vis.norm_eps)
+
+
+def vla_query_vision_sizes(enc, vis) -> int:
+    n = c_size_t()
+    _check(lib().vla_query_vision_sizes(ctypes.byref(enc) if enc else None, ctypes.byref(vis) if vis else None,
+                                        ctypes.byref(n)))
+    return n.value
 
 
 def vla_query_sizes(llm, enc, B: int, L: int, k: int):
@@ -223,6 +252,33 @@ class Context:
 
     def vla_run_encoder(self, frame_id: int, patches, n_img: int, L_img: int, out_dev):
         _check(lib().vla_run_encoder(self.h, frame_id, _ptr(patches), n_img, L_img, _ptr(out_dev)), self.h)
+
+    def vla_attach_vision(self, vis: vla_vision_cfg):
+        """Allocate the vision block (torch device memory kept by this object)
+        and attach it."""
+        import torch
+        n = vla_query_vision_sizes(self.enc, vis)
+        with torch.cuda.device(self.device):
+            mem = torch.empty(max(n, 256), dtype=torch.uint8, device="cuda:%d" % self.device)
+        _check(lib().vla_attach_vision(self.h, ctypes.byref(vis), mem.data_ptr(), mem.numel()), self.h)
+        self.vision_mem = mem
+        self.vis = vis
+
+    def vla_load_vision_weights(self, weights: dict):
+        w = vla_vision_weights()
+        keep = []
+        for name, arr in weights.items():
+            if name not in _VISION_FIELDS:
+                raise KeyError(name)
+            arr = np.ascontiguousarray(arr)
+            keep.append(arr)
+            setattr(w, name, arr.ctypes.data)
+        _check(lib().vla_load_vision_weights(self.h, ctypes.byref(w)), self.h)
+
+    def vla_run_vision(self, frame_id: int, images, n_img: int, text, L_text: int, tokens_out):
+        nbytes = tokens_out.numel() * tokens_out.element_size()
+        _check(lib().vla_run_vision(self.h, frame_id, _ptr(images), n_img, _ptr(text), L_text, _ptr(tokens_out),
+                                    nbytes), self.h)
 
     def vla_run_prefix(self, frame_id: int, tokens, B: int, L: int, k: int, out: Boundary):
         _check(lib().vla_run_prefix(self.h, frame_id, _ptr(tokens), B, L, k, ctypes.byref(out.c)), self.h)

@@ -19,7 +19,8 @@ DEVICE_FLAGS = ["--offload-arch=" + ARCH, "-O3", "-fPIC", "-std=c++17", "-Xclang
                 "-packed-fp32-ops", "-Wno-unused-result"]
 HOST_FLAGS = ["-O2", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-result"]
 
-SOURCES = ["gemm_bf16.hip", "attention_bf16.hip", "decode_bf16.hip", "norm.hip", "fp32_path.hip", "runtime.cpp",
+SOURCES = ["gemm_bf16.hip", "attention_bf16.hip", "decode_bf16.hip", "norm.hip", "fp32_path.hip", "vision.hip",
+           "runtime.cpp",
            "ops.cpp",
            "host_suffix.cpp", "host_suffix_api.cpp", "sched.cpp"]
 # Attention keeps its score and output accumulators in VGPRs: the softmax

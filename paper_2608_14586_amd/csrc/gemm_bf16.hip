@@ -563,6 +563,12 @@ hipError_t gemm_bf16_gelu(const bf16_t* A, int lda, const WOperand& W, bf16_t* o
   return launch<true>(A, lda, W, M, N, K, EpiGelu{out, bias, ldo, M, N}, s);
 }
 
+hipError_t gemm_bf16_bias(const bf16_t* A, int lda, const WOperand& W, bf16_t* out, int ldo, const float* bias, int M,
+                          int N, int K, hipStream_t s) {
+  if (N % 8 || ldo % 8) return hipErrorInvalidValue;
+  return launch<true>(A, lda, W, M, N, K, EpiStoreBF16{out, bias, ldo, M, N}, s);
+}
+
 hipError_t gemm_bf16_qkv(const bf16_t* A, int lda, const WOperand& W, const QkvArgs& qa, int M, int N, int K,
                          hipStream_t s) {
   if (qa.dh % 64 != 0 || N % 64 != 0) return hipErrorInvalidValue;

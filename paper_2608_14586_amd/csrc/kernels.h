@@ -64,6 +64,20 @@ struct QkvArgs {
 hipError_t gemm_bf16_qkv(const bf16_t* A, int lda, const WOperand& W, const QkvArgs& qa, int M, int N, int K,
                          hipStream_t s);
 
+// out (bf16) = acc + bias (bias may be NULL); N % 8 == 0, ldo % 8 == 0
+hipError_t gemm_bf16_bias(const bf16_t* A, int lda, const WOperand& W, bf16_t* out, int ldo, const float* bias,
+                          int M, int N, int K, hipStream_t s);
+
+// ---------------------------------------------------------- vision stem
+// Patch rows of n_img images [C][H][W] cut into p x p patches (row-major
+// grid, gw = W / p across): A[i * L + l][k] for k < C*p*p is pixel
+// (c, y, x) = (k / (p*p), k / p % p, k % p) of patch l, zero up to Kp;
+// h[i * L + l][:] = pos[l][:] (fp32), the residual the stem GEMM adds to.
+hipError_t patchify_bf16(const bf16_t* img, int n_img, int C, int H, int W, int p, bf16_t* A, int Kp,
+                         const float* pos, float* h, int d, hipStream_t s);
+hipError_t patchify_f32(const float* img, int n_img, int C, int H, int W, int p, float* A, int Kp, const float* pos,
+                        float* h, int d, hipStream_t s);
+
 // ---------------------------------------------------------- bf16 attention
 // o[B][L][H*dh] = softmax(q k^T / sqrt(dh) [+ causal mask]) v per (b, head);
 // query head h reads KV head h / (H / Hkv).  q [B][H][L][dh], k [B][Hkv][L][dh],
@@ -102,6 +116,14 @@ hipError_t layernorm_bf16(const float* x, const float* g, const float* b, float 
 hipError_t rmsnorm_f32(const float* x, const float* g, float eps, float* y, int M, int d, hipStream_t s);
 hipError_t layernorm_f32(const float* x, const float* g, const float* b, float eps, float* y, int M, int d,
                          hipStream_t s);
+// LayerNorm of encoder rows, n_img images x gh*gw patches in row-major grid
+// order, each written into the connector's merged layout: patch (gy, gx) of
+// image i becomes feature block (gy % m) * m + gx % m (d wide) of token
+// i * (gh/m) * (gw/m) + (gy/m) * (gw/m) + gx/m (m*m*d wide).
+hipError_t layernorm_merge_bf16(const float* x, const float* g, const float* b, float eps, bf16_t* y, int n_img,
+                                int gh, int gw, int m, int d, hipStream_t s);
+hipError_t layernorm_merge_f32(const float* x, const float* g, const float* b, float eps, float* y, int n_img,
+                               int gh, int gw, int m, int d, hipStream_t s);
 hipError_t bf16_to_f32(const bf16_t* x, float* y, size_t n, hipStream_t s);
 hipError_t f32_to_bf16(const float* x, bf16_t* y, size_t n, hipStream_t s);
 

@@ -6,10 +6,29 @@
 namespace vla {
 namespace {
 
-template <int NCH, bool LAYERNORM, class OutT>
+// Where row r of the output starts: y + rows(r).
+struct RowsPlain {
+  int d;
+  __device__ __forceinline__ size_t operator()(int r) const { return (size_t)r * d; }
+};
+
+// Encoder rows (images x gh*gw patches, row-major grid) placed in the
+// connector's merged layout: patch (gy, gx) of image i is feature block
+// (gy % m) * m + gx % m of token i * (gh/m) * (gw/m) + (gy/m) * (gw/m) + gx/m,
+// a token being m*m*d wide.
+struct RowsMerged {
+  int d, gh, gw, m;
+  __device__ __forceinline__ size_t operator()(int r) const {
+    const int L = gh * gw, i = r / L, l = r % L, gy = l / gw, gx = l % gw, tw = gw / m;
+    const size_t tok = (size_t)i * (gh / m) * tw + (size_t)(gy / m) * tw + gx / m;
+    return tok * m * m * d + (size_t)((gy % m) * m + gx % m) * d;
+  }
+};
+
+template <int NCH, bool LAYERNORM, class OutT, class Rows>
 __global__ __launch_bounds__(256) void norm_kernel(const float* __restrict__ x, const float* __restrict__ g,
                                                    const float* __restrict__ bta, float eps, OutT* __restrict__ y,
-                                                   int M, int d) {
+                                                   int M, int d, Rows rows) {
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= M) return;
@@ -61,30 +80,40 @@ __global__ __launch_bounds__(256) void norm_kernel(const float* __restrict__ x, 
 #pragma unroll
       for (int e = 0; e < 4; ++e) o[e] += bb[e];
     }
+    const size_t at = rows(row) + (size_t)i * 4;
     if constexpr (sizeof(OutT) == 2) {
       u32x2 w = {pack_bf2(o[0], o[1]), pack_bf2(o[2], o[3])};
-      *(u32x2*)((bf16_t*)y + (size_t)row * d + i * 4) = w;
+      *(u32x2*)((bf16_t*)y + at) = w;
     } else {
-      *(f32x4*)((float*)y + (size_t)row * d + i * 4) = o;
+      *(f32x4*)((float*)y + at) = o;
     }
   }
 }
 
-template <bool LN, class OutT>
+template <bool LN, class OutT, class Rows>
 hipError_t launch_norm(const float* x, const float* g, const float* b, float eps, OutT* y, int M, int d,
-                       hipStream_t s) {
+                       Rows rows, hipStream_t s) {
   if (M <= 0) return hipSuccess;
   if (d % 4 != 0) return hipErrorInvalidValue;
   const int n4 = d / 4;
   dim3 grid((M + 3) / 4), block(256);
-  if (n4 <= 64) hipLaunchKernelGGL((norm_kernel<1, LN, OutT>), grid, block, 0, s, x, g, b, eps, y, M, d);
-  else if (n4 <= 128) hipLaunchKernelGGL((norm_kernel<2, LN, OutT>), grid, block, 0, s, x, g, b, eps, y, M, d);
-  else if (n4 <= 256) hipLaunchKernelGGL((norm_kernel<4, LN, OutT>), grid, block, 0, s, x, g, b, eps, y, M, d);
-  else if (n4 <= 512) hipLaunchKernelGGL((norm_kernel<8, LN, OutT>), grid, block, 0, s, x, g, b, eps, y, M, d);
-  else if (n4 <= 1024) hipLaunchKernelGGL((norm_kernel<16, LN, OutT>), grid, block, 0, s, x, g, b, eps, y, M, d);
-  else if (n4 <= 2048) hipLaunchKernelGGL((norm_kernel<32, LN, OutT>), grid, block, 0, s, x, g, b, eps, y, M, d);
+#define VLA_NORM(NCH) hipLaunchKernelGGL((norm_kernel<NCH, LN, OutT, Rows>), grid, block, 0, s, x, g, b, eps, y, M, d, rows)
+  if (n4 <= 64) VLA_NORM(1);
+  else if (n4 <= 128) VLA_NORM(2);
+  else if (n4 <= 256) VLA_NORM(4);
+  else if (n4 <= 512) VLA_NORM(8);
+  else if (n4 <= 1024) VLA_NORM(16);
+  else if (n4 <= 2048) VLA_NORM(32);
   else return hipErrorInvalidValue;
+#undef VLA_NORM
   return hipGetLastError();
+}
+
+template <class OutT>
+hipError_t launch_norm_merge(const float* x, const float* g, const float* b, float eps, OutT* y, int n_img, int gh,
+                             int gw, int m, int d, hipStream_t s) {
+  if (n_img <= 0 || gh <= 0 || gw <= 0 || m <= 0 || gh % m || gw % m) return hipErrorInvalidValue;
+  return launch_norm<true>(x, g, b, eps, y, n_img * gh * gw, d, RowsMerged{d, gh, gw, m}, s);
 }
 
 __global__ void bf16_to_f32_kernel(const bf16_t* __restrict__ x, float* __restrict__ y, size_t n) {
@@ -133,18 +162,27 @@ inline unsigned ew_grid(size_t n) {
 }  // namespace
 
 hipError_t rmsnorm_bf16(const float* x, const float* g, float eps, bf16_t* y, int M, int d, hipStream_t s) {
-  return launch_norm<false>(x, g, (const float*)nullptr, eps, y, M, d, s);
+  return launch_norm<false>(x, g, (const float*)nullptr, eps, y, M, d, RowsPlain{d}, s);
 }
 hipError_t layernorm_bf16(const float* x, const float* g, const float* b, float eps, bf16_t* y, int M, int d,
                           hipStream_t s) {
-  return launch_norm<true>(x, g, b, eps, y, M, d, s);
+  return launch_norm<true>(x, g, b, eps, y, M, d, RowsPlain{d}, s);
 }
 hipError_t rmsnorm_f32(const float* x, const float* g, float eps, float* y, int M, int d, hipStream_t s) {
-  return launch_norm<false>(x, g, (const float*)nullptr, eps, y, M, d, s);
+  return launch_norm<false>(x, g, (const float*)nullptr, eps, y, M, d, RowsPlain{d}, s);
 }
 hipError_t layernorm_f32(const float* x, const float* g, const float* b, float eps, float* y, int M, int d,
                          hipStream_t s) {
-  return launch_norm<true>(x, g, b, eps, y, M, d, s);
+  return launch_norm<true>(x, g, b, eps, y, M, d, RowsPlain{d}, s);
+}
+
+hipError_t layernorm_merge_bf16(const float* x, const float* g, const float* b, float eps, bf16_t* y, int n_img,
+                                int gh, int gw, int m, int d, hipStream_t s) {
+  return launch_norm_merge(x, g, b, eps, y, n_img, gh, gw, m, d, s);
+}
+hipError_t layernorm_merge_f32(const float* x, const float* g, const float* b, float eps, float* y, int n_img,
+                               int gh, int gw, int m, int d, hipStream_t s) {
+  return launch_norm_merge(x, g, b, eps, y, n_img, gh, gw, m, d, s);
 }
 
 hipError_t bf16_to_f32(const bf16_t* x, float* y, size_t n, hipStream_t s) {

@@ -123,6 +123,60 @@ Status validate_stack(const vla_stack_cfg* c, bool is_llm, Stack* s) {
   return OK;
 }
 
+// Stem and connector around the encoder stack (vla_attach_vision): weights
+// and scratch in a device block the caller hands over.
+struct Vision {
+  bool present = false, loaded = false, bf16 = true;
+  vla_vision_cfg c{};
+  size_t esz = 2;
+  int d = 0, gh = 0, gw = 0, L_img = 0, tpi = 0, K = 0, Kp = 0, md = 0, max_img = 0;
+  void *w_patch = nullptr, *w_c1 = nullptr, *w_c2 = nullptr;
+  float *b_patch = nullptr, *pos = nullptr, *post_g = nullptr, *post_b = nullptr, *b_c1 = nullptr, *b_c2 = nullptr;
+  void *img = nullptr, *A = nullptr, *merged = nullptr, *hid = nullptr;
+  size_t bytes = 0;
+};
+
+Status validate_vision(const Stack& enc, const vla_vision_cfg* v, Vision* out) {
+  if (!v) return fail(VLA_ERR_INVALID_ARG, "NULL vision config");
+  if (!enc.present) return fail(VLA_ERR_INVALID_ARG, "the vision front needs an encoder stack");
+  if (v->channels <= 0 || v->img_h <= 0 || v->img_w <= 0 || v->patch <= 0 || v->merge <= 0 || v->d_hidden <= 0 ||
+      v->d_out <= 0)
+    return fail(VLA_ERR_INVALID_ARG, "vision: non-positive dimension");
+  if (!(v->norm_eps >= 0.f)) return fail(VLA_ERR_INVALID_ARG, "vision: norm_eps < 0");
+  if (v->img_h % v->patch || v->img_w % v->patch)
+    return fail(VLA_ERR_UNSUPPORTED, "vision: image sides must be multiples of the patch");
+  const int gh = v->img_h / v->patch, gw = v->img_w / v->patch;
+  if (gh % v->merge || gw % v->merge)
+    return fail(VLA_ERR_UNSUPPORTED, "vision: patch grid %dx%d is not a multiple of merge %d", gh, gw, v->merge);
+  if (gh * gw > enc.c.max_tokens)
+    return fail(VLA_ERR_SHAPE, "vision: %d patches per image exceed the encoder's max_tokens %d", gh * gw,
+                enc.c.max_tokens);
+  const bool b = enc.bf16();
+  if (b && (v->d_hidden % 64 || v->d_out % 64))
+    return fail(VLA_ERR_UNSUPPORTED, "vision: bf16 path needs d_hidden and d_out multiples of 64");
+  if (!b && v->d_out % 4) return fail(VLA_ERR_UNSUPPORTED, "vision: d_out must be a multiple of 4");
+  const long K = (long)v->channels * v->patch * v->patch;
+  if (K > (1 << 20) || (long)v->merge * v->merge * enc.c.d_model > (1 << 20) || v->d_hidden > (1 << 20) ||
+      v->d_out > (1 << 20))
+    return fail(VLA_ERR_UNSUPPORTED, "vision: dimension above 2^20");
+  Vision& o = *out;
+  o = Vision{};
+  o.present = true;
+  o.bf16 = b;
+  o.c = *v;
+  o.esz = enc.esz;
+  o.d = enc.c.d_model;
+  o.gh = gh;
+  o.gw = gw;
+  o.L_img = gh * gw;
+  o.tpi = (gh / v->merge) * (gw / v->merge);
+  o.K = (int)K;
+  o.Kp = b ? round_up((int)K, 64) : (int)K;
+  o.md = v->merge * v->merge * o.d;
+  o.max_img = enc.c.max_batch;
+  return OK;
+}
+
 struct Slot {
   uint64_t frame_id = 0;
   bool used = false;
@@ -165,6 +219,7 @@ struct vla_ctx {
   std::string last_error;
 
   Workspace ws[2];  // by vla_stack
+  Vision vis;
   float *rope_cos = nullptr, *rope_sin = nullptr;
   // cross-stream order: a prefix waits for the latest encoder run (whose
   // output it may read); an encoder's output write waits for the latest
@@ -266,6 +321,30 @@ void layout(vla_ctx* c, Bump& a) {
   a.off = align_up(a.off, ALIGN);
 }
 
+// The vision block: weights (packed like the blocks' for bf16), then the
+// image staging, patch rows, merged rows and the connector's hidden rows.
+void layout_vision(Vision& v, Bump& a) {
+  const auto wbytes = [&](int N, int K) {
+    return v.bf16 ? (size_t)vla::slab_blocks(N) * vla::SLAB_N * K * 2 : (size_t)N * K * 4;
+  };
+  const vla_vision_cfg& c = v.c;
+  v.w_patch = a.take(wbytes(v.d, v.Kp));
+  v.b_patch = (float*)a.take((size_t)v.d * 4);
+  v.pos = (float*)a.take((size_t)v.L_img * v.d * 4);
+  v.post_g = (float*)a.take((size_t)v.d * 4);
+  v.post_b = (float*)a.take((size_t)v.d * 4);
+  v.w_c1 = a.take(wbytes(c.d_hidden, v.md));
+  v.b_c1 = (float*)a.take((size_t)c.d_hidden * 4);
+  v.w_c2 = a.take(wbytes(c.d_out, c.d_hidden));
+  v.b_c2 = (float*)a.take((size_t)c.d_out * 4);
+  const size_t rows = (size_t)v.max_img * v.L_img;
+  v.img = a.take((size_t)v.max_img * c.channels * c.img_h * c.img_w * v.esz);
+  v.A = a.take(rows * v.Kp * v.esz);
+  v.merged = a.take(rows * v.d * v.esz);
+  v.hid = a.take((size_t)v.max_img * v.tpi * c.d_hidden * v.esz);
+  a.off = align_up(a.off, ALIGN);
+}
+
 // ------------------------------------------------------------ weight packing
 
 // bf16 QKV rows: per head, 64-row groups [32 first-half dims | their 32
@@ -296,8 +375,8 @@ Status copy_h2d(void* dst, const void* src, size_t bytes) {
 
 // Row-major weight rows [N][K] -> the arena: packed slab-major for bf16
 // stacks (the layout the GEMMs read, kernels.h), as-is for fp32 stacks.
-Status put_weight(const Stack& s, void* dst, const void* rm, int N, int K) {
-  if (!s.bf16()) return copy_h2d(dst, rm, (size_t)N * K * s.esz);
+Status put_matrix(bool bf16, void* dst, const void* rm, int N, int K) {
+  if (!bf16) return copy_h2d(dst, rm, (size_t)N * K * 4);
   const int nblk = vla::slab_blocks(N), SN = vla::SLAB_N;
   std::vector<uint16_t> t((size_t)nblk * SN * K, 0);
   const uint16_t* src = (const uint16_t*)rm;
@@ -305,6 +384,36 @@ Status put_weight(const Stack& s, void* dst, const void* rm, int N, int K) {
     for (int n = 0; n < N; ++n)
       memcpy(&t[(((size_t)kt * nblk + n / SN) * SN + n % SN) * 64], src + (size_t)n * K + (size_t)kt * 64, 128);
   return copy_h2d(dst, t.data(), t.size() * 2);
+}
+
+Status put_weight(const Stack& s, void* dst, const void* rm, int N, int K) { return put_matrix(s.bf16(), dst, rm, N, K); }
+
+Status load_vision(Vision& v, vla_dtype dt, const vla_vision_weights* w) {
+  if (!w->w_patch || !w->b_patch || !w->pos || !w->post_g || !w->post_b || !w->w_c1 || !w->b_c1 || !w->w_c2 ||
+      !w->b_c2)
+    return fail(VLA_ERR_INVALID_ARG, "vision weights: every field is required");
+  v.loaded = false;
+  const vla_vision_cfg& c = v.c;
+  // stem rows [d][K], zero columns up to Kp
+  std::vector<char> buf((size_t)v.d * v.Kp * v.esz, 0);
+  for (int r = 0; r < v.d; ++r)
+    memcpy(&buf[(size_t)r * v.Kp * v.esz], (const char*)w->w_patch + (size_t)r * v.K * v.esz, (size_t)v.K * v.esz);
+  Status st = put_matrix(v.bf16, v.w_patch, buf.data(), v.d, v.Kp);
+  if (st.code) return st;
+  if ((st = put_matrix(v.bf16, v.w_c1, w->w_c1, c.d_hidden, v.md)).code) return st;
+  if ((st = put_matrix(v.bf16, v.w_c2, w->w_c2, c.d_out, c.d_hidden)).code) return st;
+  auto put = [&](float* dst, const void* src, size_t n) -> Status {
+    std::vector<float> f = vec_f32(src, n, dt);
+    return copy_h2d(dst, f.data(), n * 4);
+  };
+  if ((st = put(v.b_patch, w->b_patch, v.d)).code) return st;
+  if ((st = put(v.pos, w->pos, (size_t)v.L_img * v.d)).code) return st;
+  if ((st = put(v.post_g, w->post_g, v.d)).code) return st;
+  if ((st = put(v.post_b, w->post_b, v.d)).code) return st;
+  if ((st = put(v.b_c1, w->b_c1, c.d_hidden)).code) return st;
+  if ((st = put(v.b_c2, w->b_c2, c.d_out)).code) return st;
+  v.loaded = true;
+  return OK;
 }
 
 Status load_block(vla_ctx* c, Stack& s, int bi, const vla_block_weights* w) {
@@ -811,6 +920,102 @@ Status run_encoder(vla_ctx* c, const void* patches, int n_img, int L, void* out_
   return OK;
 }
 
+// images -> stem -> encoder blocks -> final norm + merge -> connector MLP ->
+// tokens[0, V); text -> tokens[V, V + L_text)
+Status run_vision(vla_ctx* c, const void* images, int n_img, const void* text, int L_text, void* tokens,
+                  size_t tokens_bytes) {
+  if (!c->enc.present) return fail(VLA_ERR_INVALID_ARG, "context has no encoder stack");
+  Vision& v = c->vis;
+  if (!v.present) return fail(VLA_ERR_INVALID_ARG, "no vision front attached (vla_attach_vision)");
+  if (!v.loaded) return fail(VLA_ERR_NOT_LOADED, "vision weights not loaded");
+  const Stack& s = c->enc;
+  for (int l = 0; l < s.c.n_blocks; ++l)
+    if (!s.blocks[l].loaded) return fail(VLA_ERR_NOT_LOADED, "encoder block %d has no weights", l);
+  if (!images || !tokens) return fail(VLA_ERR_INVALID_ARG, "NULL images / tokens");
+  if (n_img <= 0 || n_img > v.max_img)
+    return fail(VLA_ERR_SHAPE, "n_img=%d outside [1, %d]", n_img, v.max_img);
+  if (L_text < 0) return fail(VLA_ERR_SHAPE, "negative L_text");
+  if (L_text > 0 && !text) return fail(VLA_ERR_INVALID_ARG, "NULL text with L_text > 0");
+  const vla_vision_cfg& vc = v.c;
+  const int nv = n_img * v.tpi, M = n_img * v.L_img, d = v.d;
+  const size_t need = ((size_t)nv + L_text) * vc.d_out * v.esz;
+  if (tokens_bytes < need) return fail(VLA_ERR_SHAPE, "tokens buffer of %zu bytes < %zu", tokens_bytes, need);
+  if (!is_device(tokens)) return fail(VLA_ERR_INVALID_ARG, "tokens must be device memory");
+  if ((uintptr_t)tokens % 16) return fail(VLA_ERR_INVALID_ARG, "tokens must be 16-byte aligned");
+  hipStream_t st = c->encs;
+  Workspace& ws = c->ws[VLA_STACK_ENC];
+  const void* img = images;
+  if (!is_device(images)) {
+    HIPTRY(hipMemcpyAsync(v.img, images, (size_t)n_img * vc.channels * vc.img_h * vc.img_w * v.esz,
+                          hipMemcpyHostToDevice, st));
+    img = v.img;
+  }
+  const int C = vc.channels, H = vc.img_h, W = vc.img_w, p = vc.patch, m = vc.merge, dh = vc.d_hidden;
+  if (v.bf16) {
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_STEM, vla::patchify_bf16((const bf16_t*)img, n_img, C, H, W, p, (bf16_t*)v.A,
+                                                             v.Kp, v.pos, ws.h, d, st));
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_STEM, vla::gemm_bf16_residual((const bf16_t*)v.A, v.Kp, Stack::packed(v.w_patch, d),
+                                                                  ws.h, d, v.b_patch, M, d, v.Kp, st));
+  } else {
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_STEM, vla::patchify_f32((const float*)img, n_img, C, H, W, p, (float*)v.A, v.Kp,
+                                                            v.pos, ws.h, d, st));
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_STEM, vla::gemm_f32((const float*)v.A, v.K, (const float*)v.w_patch, v.K, ws.h, d,
+                                                        v.b_patch, 1, M, d, v.K, st));
+  }
+  Status rs;
+  for (int l = 0; l < s.c.n_blocks; ++l)
+    if ((rs = enc_block(c, s.blocks[l], n_img, v.L_img)).code) return rs;
+  // tokens may still be the input of the latest prefix
+  const bool split = c->encs != c->compute;
+  if (split && c->intake_recorded) HIPTRY(hipStreamWaitEvent(st, c->ev_intake, 0));
+  if (v.bf16) {
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_CONNECTOR, vla::layernorm_merge_bf16(ws.h, v.post_g, v.post_b, vc.norm_eps,
+                                                                         (bf16_t*)v.merged, n_img, v.gh, v.gw, m, d, st));
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_CONNECTOR, vla::gemm_bf16_gelu((const bf16_t*)v.merged, v.md, Stack::packed(v.w_c1, dh),
+                                                                   (bf16_t*)v.hid, dh, v.b_c1, nv, dh, v.md, st));
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_CONNECTOR, vla::gemm_bf16_bias((const bf16_t*)v.hid, dh, Stack::packed(v.w_c2, vc.d_out),
+                                                                   (bf16_t*)tokens, vc.d_out, v.b_c2, nv, vc.d_out, dh, st));
+  } else {
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_CONNECTOR, vla::layernorm_merge_f32(ws.h, v.post_g, v.post_b, vc.norm_eps,
+                                                                        (float*)v.merged, n_img, v.gh, v.gw, m, d, st));
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_CONNECTOR, vla::gemm_f32((const float*)v.merged, v.md, (const float*)v.w_c1, v.md,
+                                                             (float*)v.hid, dh, v.b_c1, 0, nv, dh, v.md, st));
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_CONNECTOR, vla::gelu_f32((float*)v.hid, (size_t)nv * dh, st));
+    PLAUNCH(c, VLA_STACK_ENC, VLA_K_CONNECTOR, vla::gemm_f32((const float*)v.hid, dh, (const float*)v.w_c2, dh,
+                                                             (float*)tokens, vc.d_out, v.b_c2, 0, nv, vc.d_out, dh, st));
+  }
+  if (L_text > 0)
+    HIPTRY(hipMemcpyAsync((char*)tokens + (size_t)nv * vc.d_out * v.esz, text, (size_t)L_text * vc.d_out * v.esz,
+                          hipMemcpyDefault, st));
+  if (split) {
+    HIPTRY(hipEventRecord(c->ev_enc_done, st));
+    c->enc_recorded = true;
+  }
+  return OK;
+}
+
+Status attach_vision(vla_ctx* c, const vla_vision_cfg* vc, void* mem, size_t bytes) {
+  Vision v;
+  Status st = validate_vision(c->enc, vc, &v);
+  if (st.code) return st;
+  Bump dry{nullptr};
+  layout_vision(v, dry);
+  if (!mem) return fail(VLA_ERR_INVALID_ARG, "NULL vision memory");
+  if (dry.off > bytes) return fail(VLA_ERR_OOM, "vision block of %zu bytes < %zu required", bytes, dry.off);
+  if (((uintptr_t)mem) % ALIGN) return fail(VLA_ERR_INVALID_ARG, "vision memory must be %zu-byte aligned", ALIGN);
+  if (!is_device(mem)) return fail(VLA_ERR_INVALID_ARG, "vision memory is not device memory");
+  // a previous block may still be read by work in flight
+  HIPTRY(hipStreamSynchronize(c->compute));
+  HIPTRY(hipStreamSynchronize(c->encs));
+  Bump real{(char*)mem};
+  layout_vision(v, real);
+  v.bytes = real.off;
+  // weight padding (pad rows and the stem's pad columns) must be zero
+  HIPTRY(hipMemset(mem, 0, real.off));
+  c->vis = v;
+  return OK;
+}
+
 vla_status finish(vla_ctx* c, const Status& st) {
   if (c) c->last_error = st.msg;
   if (st.code != VLA_OK) g_last_error = st.msg;
@@ -985,6 +1190,61 @@ vla_status vla_run_encoder(vla_ctx* ctx, uint64_t frame_id, const void* patches,
   try {
     if (hipSetDevice(ctx->device) != hipSuccess) return finish(ctx, fail(VLA_ERR_HIP, "hipSetDevice failed"));
     return finish(ctx, run_encoder(ctx, patches, n_img, L_img, out_dev));
+  } catch (...) {
+    return finish(ctx, fail(VLA_ERR_INVALID_ARG, "internal error"));
+  }
+}
+
+vla_status vla_query_vision_sizes(const vla_stack_cfg* enc, const vla_vision_cfg* vis, size_t* bytes) {
+  try {
+    vla_ctx tmp;
+    Status st = validate_stack(enc, false, &tmp.enc);
+    if (!st.code && !enc) st = fail(VLA_ERR_INVALID_ARG, "NULL encoder config");
+    Vision v;
+    if (!st.code) st = validate_vision(tmp.enc, vis, &v);
+    if (st.code) return finish(nullptr, st);
+    Bump dry{nullptr};
+    layout_vision(v, dry);
+    if (bytes) *bytes = dry.off;
+    return VLA_OK;
+  } catch (...) {
+    return finish(nullptr, fail(VLA_ERR_INVALID_ARG, "internal error"));
+  }
+}
+
+vla_status vla_attach_vision(vla_ctx* ctx, const vla_vision_cfg* vis, void* dev_mem, size_t bytes) {
+  if (!ctx) return finish(nullptr, fail(VLA_ERR_INVALID_ARG, "NULL context"));
+  try {
+    if (hipSetDevice(ctx->device) != hipSuccess) return finish(ctx, fail(VLA_ERR_HIP, "hipSetDevice failed"));
+    return finish(ctx, attach_vision(ctx, vis, dev_mem, bytes));
+  } catch (...) {
+    return finish(ctx, fail(VLA_ERR_INVALID_ARG, "internal error"));
+  }
+}
+
+vla_status vla_load_vision_weights(vla_ctx* ctx, const vla_vision_weights* w) {
+  if (!ctx) return finish(nullptr, fail(VLA_ERR_INVALID_ARG, "NULL context"));
+  try {
+    if (!w) return finish(ctx, fail(VLA_ERR_INVALID_ARG, "NULL weights"));
+    if (!ctx->vis.present) return finish(ctx, fail(VLA_ERR_INVALID_ARG, "no vision front attached"));
+    if (hipSetDevice(ctx->device) != hipSuccess) return finish(ctx, fail(VLA_ERR_HIP, "hipSetDevice failed"));
+    if (hipStreamSynchronize(ctx->compute) != hipSuccess || hipStreamSynchronize(ctx->encs) != hipSuccess)
+      return finish(ctx, fail(VLA_ERR_HIP, "hipStreamSynchronize failed"));
+    return finish(ctx, load_vision(ctx->vis, ctx->enc.c.dtype, w));
+  } catch (const std::bad_alloc&) {
+    return finish(ctx, fail(VLA_ERR_OOM, "host allocation failed"));
+  } catch (...) {
+    return finish(ctx, fail(VLA_ERR_INVALID_ARG, "internal error"));
+  }
+}
+
+vla_status vla_run_vision(vla_ctx* ctx, uint64_t frame_id, const void* images, int n_img, const void* text,
+                          int L_text, void* tokens_dev, size_t tokens_bytes) {
+  if (!ctx) return finish(nullptr, fail(VLA_ERR_INVALID_ARG, "NULL context"));
+  (void)frame_id;
+  try {
+    if (hipSetDevice(ctx->device) != hipSuccess) return finish(ctx, fail(VLA_ERR_HIP, "hipSetDevice failed"));
+    return finish(ctx, run_vision(ctx, images, n_img, text, L_text, tokens_dev, tokens_bytes));
   } catch (...) {
     return finish(ctx, fail(VLA_ERR_INVALID_ARG, "internal error"));
   }

@@ -218,9 +218,10 @@ def images(wl: "Workload", frame: int = 0, n_img: int = None) -> np.ndarray:
 
 
 def text(wl: "Workload", frame: int = 0, T: int = None) -> np.ndarray:
-    """Text token embeddings [T, d_llm] ~ N(0, 1) that follow the visual tokens."""
+    """Text token embeddings [T, d_out] ~ N(0, 1) that follow the visual tokens
+    (d_out is the decoder's d_model)."""
     T = wl.text_tokens if T is None else T
-    return _draw(seed_of(wl.name, "text", frame, T), (T, wl.llm.d_model), 1.0, wl.dtype)
+    return _draw(seed_of(wl.name, "text", frame, T), (T, wl.vision.d_out), 1.0, wl.dtype)
 
 
 def as_f32(a: np.ndarray) -> np.ndarray:

@@ -113,3 +113,46 @@ def test_encoder_stack_validation():
     bad.causal = 1
     with pytest.raises(vb.VlaError):
         vb.vla_query_sizes(None, bad, 0, 0, 0)
+
+
+def _vis_case(dtype="bf16"):
+    from synth.configs import VisionShape, vit_like
+    enc = vb.stack_cfg(vit_like(2, 128, 2, 64, 256), dtype, max_tokens=64, max_batch=3)
+    return enc, VisionShape(3, 56, 84, 14, 2, 128, 192)
+
+
+def test_vision_sizes_grow_with_images():
+    enc, vis = _vis_case()
+    n3 = vb.vla_query_vision_sizes(enc, vb.vision_cfg(vis))
+    enc.max_batch = 6
+    n6 = vb.vla_query_vision_sizes(enc, vb.vision_cfg(vis))
+    # per image: staging 3*56*84 bf16, 24 patch rows of 640 (588 padded), 24 merged rows of 128, 6 x 128 hidden
+    per_img = 3 * 56 * 84 * 2 + 24 * 640 * 2 + 24 * 128 * 2 + 6 * 128 * 2
+    assert n6 - n3 >= 3 * per_img and n6 - n3 < 3 * per_img + 4 * 256
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("img_h", 60, "VLA_ERR_UNSUPPORTED"),      # not a multiple of the patch
+    ("merge", 4, "VLA_ERR_UNSUPPORTED"),       # 4 x 6 grid not a multiple of 4
+    ("d_hidden", 96, "VLA_ERR_UNSUPPORTED"),   # bf16 needs multiples of 64
+    ("d_out", 100, "VLA_ERR_UNSUPPORTED"),
+    ("patch", 7, "VLA_ERR_SHAPE"),             # 8 x 12 = 96 patches > max_tokens 64
+    ("channels", 0, "VLA_ERR_INVALID_ARG"),
+])
+def test_vision_validation(field, value, code):
+    enc, vis = _vis_case()
+    v = vb.vision_cfg(vis)
+    setattr(v, field, value)
+    with pytest.raises(vb.VlaError) as e:
+        vb.vla_query_vision_sizes(enc, v)
+    assert e.value.name == code
+
+
+def test_vision_needs_an_encoder_and_f32_relaxes_widths():
+    enc, vis = _vis_case("f32")
+    v = vb.vision_cfg(vis)
+    v.d_hidden, v.d_out = 96, 100
+    assert vb.vla_query_vision_sizes(enc, v) > 0
+    with pytest.raises(vb.VlaError) as e:
+        vb.vla_query_vision_sizes(None, v)
+    assert e.value.name == "VLA_ERR_INVALID_ARG"
