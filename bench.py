@@ -39,9 +39,15 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-def class_work(wl, kind, k):
-    """Algorithmic FLOPs (GEMM / attention classes) or HBM bytes (norm) per
-    launch of each kernel class of one stack, from the stack shapes."""
+# kernel classes launched once per block; the others once per frame
+PER_BLOCK = ("qkv", "attn", "oproj", "mlp_up", "mlp_down", "norm")
+
+
+def class_work(wl, kind, k, images=False):
+    """Algorithmic FLOPs (GEMM / attention classes) or HBM bytes (norm) of
+    each kernel class of one stack, from the stack shapes:
+    {class: (unit, work, launches)}, the work of `launches` consecutive
+    launches (one block's, or the vision front's per frame)."""
     if kind == "llm":
         s, B, L = wl.llm, wl.batch, wl.seq
         M = B * L
@@ -52,14 +58,22 @@ def class_work(wl, kind, k):
         pairs = B * L * L
     d, H, Hkv, dh, F = s.d_model, s.n_heads, s.n_kv_heads, s.head_dim, s.d_ff
     up_rows = 2 * F if kind == "llm" else F
-    return {
-        "qkv": ("flop", 2.0 * M * d * (H + 2 * Hkv) * dh),
-        "attn": ("flop", 4.0 * pairs * dh * H),
-        "oproj": ("flop", 2.0 * M * H * dh * d),
-        "mlp_up": ("flop", 2.0 * M * d * up_rows),
-        "mlp_down": ("flop", 2.0 * M * F * d),
-        "norm": ("byte", M * d * 4.0 + M * d * 2.0 + d * 4.0 * (2 if s.norm_is_layernorm else 1)),
+    w = {
+        "qkv": ("flop", 2.0 * M * d * (H + 2 * Hkv) * dh, 1),
+        "attn": ("flop", 4.0 * pairs * dh * H, 1),
+        "oproj": ("flop", 2.0 * M * H * dh * d, 1),
+        "mlp_up": ("flop", 2.0 * M * d * up_rows, 1),
+        "mlp_down": ("flop", 2.0 * M * F * d, 1),
+        "norm": ("byte", M * d * 4.0 + M * d * 2.0 + d * 4.0 * (2 if s.norm_is_layernorm else 1), 1),
     }
+    if kind == "enc" and images:
+        v = wl.vision
+        V = wl.n_img * v.tokens_per_image
+        # patch rows + the stem GEMM (K = channels * patch^2, unpadded)
+        w["stem"] = ("flop", 2.0 * M * d * v.channels * v.patch * v.patch, 2)
+        # final norm + merge, then the two connector GEMMs
+        w["connector"] = ("flop", 2.0 * V * v.merge * v.merge * d * v.d_hidden + 2.0 * V * v.d_hidden * v.d_out, 3)
+    return w
 
 
 def profiled_traffic(kernel_class):
@@ -86,11 +100,12 @@ def profiled_traffic(kernel_class):
     return None
 
 
-def frame_flops(wl, k):
+def frame_flops(wl, k, images=False):
     tot = 0.0
     for kind, n in (("llm", k), ("enc", wl.enc.n_blocks)):
-        w = class_work(wl, kind, k)
-        tot += n * sum(v for c, (u, v) in w.items() if u == "flop")
+        for c, (u, v, _) in class_work(wl, kind, k, images).items():
+            if u == "flop":
+                tot += v * (n if c in PER_BLOCK else 1)
     return tot
 
 
@@ -257,6 +272,110 @@ def decode_across(args, ctx, wl, bnd, cache, xs, ob, L_cap):
          "host_prefill_ms": round(prefill_ms, 1), "steps": len(tc)}
     sfx.vla_suffix_destroy()
     return r
+
+
+def dual_bench(args):
+    """The dual-stack workload: camera images through the stem, the ViT-L
+    encoder and the connector into 1536 visual + 512 text tokens, then two
+    24-block 0.5B-class decoder stacks over the same tokens (a dual-expert
+    backbone), each to partition point k on the GPU; the host suffix runs
+    blocks [k, 24) of both.  k = 0 leaves only the encoder on the GPU."""
+    import numpy as np
+    import torch
+    import synth
+    from paper_2608_14586_amd import binding as vb
+
+    wl = synth.CONFIGS["dual05b"]
+    s, e, vis = wl.llm, wl.enc, wl.vision
+    n_img, T = wl.n_img, wl.text_tokens
+    L = n_img * vis.tokens_per_image + T
+    N = s.n_blocks
+    ks = sorted(set(int(x) for x in args.dual_ks.split(",")))
+    assert all(0 <= k <= N for k in ks)
+    lcfg = vb.stack_cfg(s, "bf16", max_tokens=L, max_batch=1, n_blocks=N)
+    ctx = [vb.Context(llm=lcfg, enc=vb.stack_cfg(e, "bf16", max_tokens=vis.L_img, max_batch=n_img))]
+    ctx.append(vb.Context(llm=lcfg, compute_stream=ctx[0].compute_stream))
+    t0 = time.time()
+    for l in range(e.n_blocks):
+        ctx[0].vla_load_block_weights(vb.VLA_STACK_ENC, l, synth.vit_block_weights(wl, l))
+    ctx[0].vla_attach_vision(vb.vision_cfg(vis))
+    ctx[0].vla_load_vision_weights(synth.vision_weights(wl))
+    # stack j holds blocks j*N .. j*N + N-1 of the workload's weight sequence
+    for j in range(2):
+        for l in range(N):
+            ctx[j].vla_load_block_weights(vb.VLA_STACK_LLM, l, synth.llm_block_weights(wl, j * N + l))
+    dev = torch.device("cuda:0")
+    imgs = [torch.from_numpy(synth.images(wl, frame=f).view(np.int16)).to(dev) for f in range(2)]
+    texts = [torch.from_numpy(synth.text(wl, frame=f).view(np.int16)).to(dev) for f in range(2)]
+    tok = torch.empty((L, s.d_model), dtype=torch.bfloat16, device=dev)
+    torch.cuda.synchronize()
+    log("dual stack resident (%.0fs)" % (time.time() - t0))
+    fid = [1]
+    table = {}
+    last = {}
+    for k in ks:
+        bnds = [[vb.Boundary(1, L, s.d_model, k, s.n_kv_heads, s.head_dim) for _ in range(3)] for _ in range(2)]
+
+        def frames(n):
+            ids = []
+            ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            torch.cuda.synchronize()
+            t = time.perf_counter()
+            for i in range(n):
+                f = fid[0]
+                fid[0] += 1
+                if i == 0:
+                    ev[0].record(ctx[0].compute_stream)
+                ctx[0].vla_run_vision(f, imgs[i % 2], n_img, texts[i % 2], T, tok)
+                if i == 0:
+                    ev[1].record(ctx[0].compute_stream)
+                for j in range(2):
+                    ctx[j].vla_run_prefix(f, tok, 1, L, k, bnds[j][i % 3])
+                ids.append((f, i % 3))
+            for f, _ in ids[-3:]:
+                for j in range(2):
+                    ctx[j].vla_wait_boundary(f, 120000)
+            torch.cuda.synchronize()
+            return (time.perf_counter() - t) * 1000 / n, ev[0].elapsed_time(ev[1]), ids[-1][1]
+
+        frames(args.warmup)
+        ms, vis_ms, slot = frames(args.steps)
+        table[k] = {"t_gpu_ms": round(ms, 3), "t_vision_ms": round(vis_ms, 3),
+                    "handoff_mib": round(2 * (L * s.d_model * 2 + k * 2 * s.n_kv_heads * L * s.head_dim * 2) / 2 ** 20, 1)}
+        last[k] = [bnds[j][slot] for j in range(2)]
+        log("dual k=%d: %s" % (k, json.dumps(table[k])))
+    # the host suffix of both stacks on the last frame's boundaries
+    for k in [k for k in ks if k < N and k in args.dual_host_ks]:
+        t_c = 0.0
+        for j in range(2):
+            sfx = vb.Suffix(vb.stack_cfg(s, "bf16", max_tokens=L), k, N, args.pipeline_threads)
+            for l in range(k, N):
+                sfx.vla_suffix_load_block_weights(l, synth.llm_block_weights(wl, j * N + l))
+            out = np.empty((1, L, s.d_model), np.float32)
+            sfx.vla_suffix_run(last[k][j].hidden, vb.VLA_BF16, 1, L, out)   # first touch of the packed weights
+            t = time.perf_counter()
+            sfx.vla_suffix_run(last[k][j].hidden, vb.VLA_BF16, 1, L, out)
+            t_c += (time.perf_counter() - t) * 1000
+            threads = sfx.vla_suffix_threads()
+            sfx.vla_suffix_destroy()
+        r = table[k]
+        r["t_host_ms"] = round(t_c, 1)
+        r["host_threads"] = threads
+        r["host_ms_per_block"] = round(t_c / (2 * (N - k)), 2)
+        r["frame_by_frame_ms"] = round(r["t_gpu_ms"] + t_c, 1)            # Eq. (12) without T_X
+        r["pipelined_interval_ms"] = round(max(r["t_gpu_ms"], t_c), 1)     # Eq. (13) without T_X
+        log("dual k=%d host: %.1f ms over %d blocks" % (k, t_c, 2 * (N - k)))
+    out = {"metric": "dual-stack frame: GPU stage (images -> stem + ViT-L + connector -> two 0.5B-class stacks "
+                     "[0,k) over 2048 tokens) per partition point k, and the host suffix of both stacks",
+           "unit": "ms", "higher_is_better": False, "n_gpus": 1, "steps": args.steps, "dtype": "bf16",
+           "data": "synthetic",
+           "config": {"workload": "dual05b: 6 cameras 448x448, 14x14 patches, ViT-L 24 blocks, 2x2 merge, "
+                                  "connector 4096->896->896; 2 x 24 decoder blocks d=896 14x64 GQA 2 KV SwiGLU "
+                                  "4864; 1536 visual + 512 text tokens", "ks": ks},
+           "per_k": {str(k): v for k, v in table.items()}}
+    for c in ctx[::-1]:
+        c.vla_destroy()
+    print(json.dumps(out), flush=True)
 
 
 def gpu_stage_factory(ctx, pats, toks, enc_out, n_img, L_img, L, fid):
@@ -463,6 +582,9 @@ def main():
     ap.add_argument("--k", type=int, default=16)
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--frame", choices=("embeddings", "images"), default="embeddings",
+                    help="encoder input: synthetic patch embeddings, or camera images through the stem, with the "
+                         "connector's tokens as the decoder's input")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (HBM counter calibration)")
     ap.add_argument("--pipeline", action="store_true",
@@ -474,6 +596,11 @@ def main():
     ap.add_argument("--decode-batch", type=int, default=1)
     ap.add_argument("--decode-host-blocks", type=int, default=0,
                     help="with --decode: also run blocks [k, k + n) on the host per token")
+    ap.add_argument("--dual", action="store_true",
+                    help="the dual 0.5B-stack workload from camera images (GPU stage per k, host suffix)")
+    ap.add_argument("--dual-ks", default="0,6,12,18,24")
+    ap.add_argument("--dual-host-ks", type=lambda x: [int(v) for v in x.split(",") if v], default=[0, 12, 18],
+                    help="partition points whose host suffix is timed")
     ap.add_argument("--pipeline-frames", type=int, default=4)
     ap.add_argument("--pipeline-threads", type=int, default=0, help="host suffix threads (0: all)")
     ap.add_argument("--pipeline-adaptive", type=int, default=20, metavar="FRAMES",
@@ -492,6 +619,9 @@ def main():
         return
     if args.decode:
         decode_bench(args)
+        return
+    if args.dual:
+        dual_bench(args)
         return
 
     if args.copy_calibration:
@@ -527,6 +657,16 @@ def main():
     toks = [torch.from_numpy(synth.tokens(wl, frame=f).view(np.int16)).to(dev) for f in range(2)]
     pats = [torch.from_numpy(synth.patches(wl, frame=f).view(np.int16)).to(dev) for f in range(2)]
     enc_out = torch.empty((n_img, L_img, e.d_model), dtype=torch.bfloat16, device=dev)
+    images = args.frame == "images"
+    if images:
+        # E(x_t) from camera images: stem, encoder, connector; the prefix reads its tokens
+        vis = wl.vision
+        assert n_img * vis.tokens_per_image + wl.text_tokens == L
+        ctx.vla_attach_vision(vb.vision_cfg(vis))
+        ctx.vla_load_vision_weights(synth.vision_weights(wl))
+        imgs = [torch.from_numpy(synth.images(wl, frame=f).view(np.int16)).to(dev) for f in range(2)]
+        texts = [torch.from_numpy(synth.text(wl, frame=f).view(np.int16)).to(dev) for f in range(2)]
+        frame_tok = torch.empty((L, s.d_model), dtype=torch.bfloat16, device=dev)
     torch.cuda.synchronize()
     log("weights and inputs resident (%.0fs)" % (time.time() - t0))
 
@@ -548,10 +688,13 @@ def main():
             st = ctx.encoder_stream
             if i == 0:
                 ev0.record(st)
-            ctx.vla_run_encoder(f, pats[i % 2], n_img, L_img, enc_out)
+            if images:
+                ctx.vla_run_vision(f, imgs[i % 2], n_img, texts[i % 2], wl.text_tokens, frame_tok)
+            else:
+                ctx.vla_run_encoder(f, pats[i % 2], n_img, L_img, enc_out)
             if i == 0:
                 ev1.record(st)
-            ctx.vla_run_prefix(f, toks[i % 2], 1, L, k, bnds[i % 3])
+            ctx.vla_run_prefix(f, frame_tok if images else toks[i % 2], 1, L, k, bnds[i % 3])
             ids.append(f)
         for f in ids[-3:]:
             ctx.vla_wait_boundary(f, 120000)
@@ -579,22 +722,23 @@ def main():
              "t_boundary_copy_ms": round(float(np.mean([t[1] for t in times])), 4),
              "t_prefix_plus_handoff_ms": round(float(np.mean([t[2] for t in times])), 3),
              "t_encoder_ms": round(enc_ms, 3),
-             "frame_tflops": round(frame_flops(wl, k) / 1e12, 3),
-             "mfma_frac_of_bf16_peak": round(frame_flops(wl, k) / (ms / 1000.0) / 1e12 / PEAK_BF16_TFLOPS, 4),
+             "frame_tflops": round(frame_flops(wl, k, images) / 1e12, 3),
+             "mfma_frac_of_bf16_peak": round(frame_flops(wl, k, images) / (ms / 1000.0) / 1e12 / PEAK_BF16_TFLOPS,
+                                             4),
              "hbm_footprint_gib": round(foot[0] / 2 ** 30, 3),
              "handoff_bytes": foot[1] + foot[2]}
         if prof:
             classes = {}
             for kind, stk, nl in (("llm", vb.VLA_STACK_LLM, k), ("enc", vb.VLA_STACK_ENC, e.n_blocks)):
-                work = class_work(wl, kind, k)
+                work = class_work(wl, kind, k, images)
                 for ci, cname in enumerate(vb.KERNEL_CLASSES):
                     tot, cnt = ctx.vla_profile_read(stk, ci)
                     if cnt == 0:
                         continue
                     ent = {"ms_total": round(tot, 4), "launches": cnt, "avg_us": round(tot / cnt * 1000, 2)}
                     if cname in work:
-                        unit, per = work[cname]
-                        avg_s = tot / cnt / 1000.0
+                        unit, per, group = work[cname]
+                        avg_s = tot / cnt * group / 1000.0   # time of the launches the work covers
                         if unit == "flop":
                             ent["tflops"] = round(per / avg_s / 1e12, 1)
                             ent["frac"] = round(per / avg_s / 1e12 / PEAK_BF16_TFLOPS, 4)
@@ -616,16 +760,19 @@ def main():
                 "unit": "TFLOP/s" if "tflops" in dom else "GB/s", "frac": dom["frac"],
                 "traffic": profiled_traffic(dom_name),
                 "per_launch": dom["per_launch"], "avg_launch_us": dom["avg_us"]}
+    front = ("6 camera images 448x448 -> patch stem + ViT-L encoder + 2x2-merge MLP connector -> 1536 visual + "
+             "512 text tokens" if images else "ViT-L encoder 6x1024")
     out = {
-        "metric": "GPU-prefix tokens/s at boundary k=%d (frame: ViT-L encoder 6x1024 + 7B-shaped decoder blocks "
-                  "[0,k) over 2048 tokens + boundary/KV handoff to pinned host)" % args.k,
+        "metric": "GPU-prefix tokens/s at boundary k=%d (frame: %s + 7B-shaped decoder blocks "
+                  "[0,k) over 2048 tokens + boundary/KV handoff to pinned host)" % (args.k, front),
         "value": head["prefix_tokens_per_s"], "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": head["ms_per_frame"], "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": "sweep7b: encoder 24x ViT-L block (d=1024, 16x64, GELU 4096) over 6 images x 1024 "
                                "patches; decoder 7B-shaped blocks (d=4096, 32x128 MHA, SwiGLU 11008, RoPE) [0,k) "
                                "over 1x2048 tokens; bf16 weights N(0,0.02), inputs N(0,1)",
-                   "k": args.k, "seq_len": L, "batch": 1, "n_img": n_img, "img_tokens": L_img},
+                   "k": args.k, "seq_len": L, "batch": 1, "n_img": n_img, "img_tokens": L_img,
+                   "frame_input": args.frame},
         "mfma_frac_of_bf16_peak": head["mfma_frac_of_bf16_peak"],
         "roofline": roofline,
         "kernels": kern,
