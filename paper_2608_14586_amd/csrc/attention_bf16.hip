@@ -1,9 +1,14 @@
 // Flash-style attention for gfx950 (bf16 MFMA, fp32 online softmax).
 //
 // One workgroup = 4 waves = 128 queries of one (batch, head); each wave owns
-// 32 queries.  Keys advance in tiles of 64 staged in LDS (double buffered):
-// K as [key][dh] and V transposed as [dh][key], so every MFMA operand is a
-// contiguous LDS read.
+// 32 queries.  Keys advance in tiles of 64 staged in LDS: K as [key][dh] and
+// V transposed as [dh][key], so every MFMA operand is a contiguous LDS read.
+// The tiles move global -> LDS with buffer_load ... lds (no VGPRs, no
+// ds_write) into a ring of stages, the 16-byte chunks of each row
+// XOR-swizzled so that fragment reads hit every bank once per 16-lane phase;
+// a barrier waits only for the tile about to be read (vmcnt(N)), so later
+// tiles stay in flight across it.  Key rows past L read as zero through the
+// buffer resource; V^T columns past L are zeroed in LDS in the last tile.
 //
 // The scores are formed transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16
 // (A = K tile from LDS, B = the wave's Q held in registers).  In the 32x32
@@ -28,22 +33,35 @@
 namespace vla {
 namespace {
 
-constexpr int BQ = 128, BKV = 64, PADK = 8, PADV = 8;
+constexpr int BQ = 128, BKV = 64;
 
 // key index <-> stored V^T column: bits 2 and 3 swapped (an involution)
 __device__ __forceinline__ int swap23(int t) { return (t & ~12) | ((t & 4) << 1) | ((t & 8) >> 1); }
 
-template <int DH, bool CAUSAL>
+__device__ __forceinline__ void lds_dma16(__amdgpu_buffer_rsrc_t r, void* lds, unsigned voff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, voff, 0, 0, 0);
+}
+// wait until at most N of this wave's global->LDS loads are outstanding and
+// every LDS access has completed, then barrier (no vmcnt(0) drain)
+template <int N>
+__device__ __forceinline__ void wait_barrier() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0070);
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+template <int DH, bool CAUSAL, int NS>
 __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
-                                                        const bf16_t* __restrict__ vt, int ldvt,
-                                                        bf16_t* __restrict__ o, int B, int H, int Hkv, int L,
-                                                        float scale_log2) {
-  constexpr int LDK = DH + PADK, LDV = BKV + PADV;
-  constexpr int KCH = BKV * DH / 8 / 256;  // 16-byte chunks per thread, K tile
-  constexpr int VCH = DH * BKV / 8 / 256;  // V^T tile
+                                                       const bf16_t* __restrict__ vt, int ldvt,
+                                                       bf16_t* __restrict__ o, int B, int H, int Hkv, int L,
+                                                       float scale_log2) {
+  constexpr int KROWB = DH * 2;                  // bytes per K row
+  constexpr int KT = BKV * KROWB, VT = DH * BKV * 2;   // bytes per K / V^T tile
+  constexpr int STAGE = KT + VT;
+  constexpr int KI = KT / 1024 / 4, VI = VT / 1024 / 4;  // 1 KB loads per wave per tile
   constexpr int ND = DH / 32;
-  __shared__ __attribute__((aligned(16))) bf16_t sK[2][BKV * LDK];
-  __shared__ __attribute__((aligned(16))) bf16_t sV[2][DH * LDV];
+  __shared__ __attribute__((aligned(1024))) char smem[NS * STAGE];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, li = lane & 31;
@@ -51,23 +69,21 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict
   const int id = blockIdx.x;
   const int rest = id % (H * B);
   const int qb_r = id / (H * B);
-  // causal: the first half of the grid takes the heavy query blocks in
-  // descending order, the second half the light ones ascending, so the two
-  // workgroups that share a CU (ids i and i + half the grid) sum to the same
-  // number of key tiles
   const int heavy = (nqb + 1) / 2;
   const int qb = !CAUSAL ? qb_r : (qb_r < heavy ? nqb - 1 - qb_r : qb_r - heavy);
   const int h = rest % H, b = rest / H;
   const int hk = h / (H / Hkv);
   const int q0 = qb * BQ;
   const int qw0 = q0 + wave * 32;
-  const int qi = qw0 + li;  // this lane's query
+  const int qi = qw0 + li;
 
   const bf16_t* qh = q + ((size_t)b * H + h) * L * DH;
   const bf16_t* kh = k + ((size_t)b * Hkv + hk) * L * DH;
   const bf16_t* vh = vt + ((size_t)b * Hkv + hk) * DH * (size_t)ldvt;
+  // rows past L read as zero
+  const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc((void*)kh, (short)0, L * DH * 2, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc((void*)vh, (short)0, DH * ldvt * 2, 0x00020000);
 
-  // Q fragments (B operand of S^T): query qi, dims ks*16 + half*8 .. +8
   bf16x8 fq[DH / 16];
 #pragma unroll
   for (int ks = 0; ks < DH / 16; ++ks) {
@@ -80,49 +96,26 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict
   const int kend = CAUSAL ? min(L, q0 + BQ) : L;
   const int ntiles = (kend + BKV - 1) / BKV;
 
-  u32x4 rk[KCH], rv[VCH];
-  auto gload = [&](int kb) {
+  // K row r of a tile: 16-byte chunk c stored at chunk c ^ ksw(r); V^T row d: chunk c at c ^ ((d >> 1) & 7)
+  auto ksw = [](int r) { return DH == 128 ? (r & 15) : ((r >> 1) & 7); };
+  auto issue = [&](int t) {
+    char* st = smem + (t % NS) * STAGE;
+    const int kb = t * BKV;
 #pragma unroll
-    for (int c = 0; c < KCH; ++c) {
-      int idx = tid + c * 256;
-      int row = idx / (DH / 8), cc = idx % (DH / 8);
-      int key = kb + row;
-      rk[c] = key < L ? *(const u32x4*)(kh + (size_t)key * DH + cc * 8) : u32x4{0, 0, 0, 0};
+    for (int j = 0; j < KI; ++j) {
+      const int blk = wave * KI + j;
+      constexpr int RPK = 1024 / KROWB;        // rows per 1 KB
+      constexpr int CPR = KROWB / 16;          // chunks per row
+      const int r = blk * RPK + lane / CPR, cs = lane % CPR;
+      const int c = cs ^ ksw(r);
+      lds_dma16(rk, st + blk * 1024, (unsigned)(((kb + r) * DH + c * 8) * 2));
     }
 #pragma unroll
-    for (int c = 0; c < VCH; ++c) {
-      int idx = tid + c * 256;
-      int d = idx / (BKV / 8), cc = idx % (BKV / 8);
-      int pos = kb + cc * 8;  // stored column; it holds key pos ^ swap23
-      const bf16_t* src = vh + (size_t)d * ldvt + pos;
-      if ((pos & ~15) + 16 <= L) {
-        rv[c] = *(const u32x4*)src;
-      } else {
-        // columns of keys >= L are zero (their probabilities are zero too)
-        uint32_t w[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int k0 = swap23(pos + 2 * e), k1 = swap23(pos + 2 * e + 1);
-          uint32_t lo = k0 < L ? src[2 * e] : 0u;
-          uint32_t hi = k1 < L ? src[2 * e + 1] : 0u;
-          w[e] = lo | (hi << 16);
-        }
-        rv[c] = u32x4{w[0], w[1], w[2], w[3]};
-      }
-    }
-  };
-  auto lstore = [&](int buf) {
-#pragma unroll
-    for (int c = 0; c < KCH; ++c) {
-      int idx = tid + c * 256;
-      int row = idx / (DH / 8), cc = idx % (DH / 8);
-      *(u32x4*)(&sK[buf][row * LDK + cc * 8]) = rk[c];
-    }
-#pragma unroll
-    for (int c = 0; c < VCH; ++c) {
-      int idx = tid + c * 256;
-      int d = idx / (BKV / 8), cc = idx % (BKV / 8);
-      *(u32x4*)(&sV[buf][d * LDV + cc * 8]) = rv[c];
+    for (int j = 0; j < VI; ++j) {
+      const int blk = wave * VI + j;
+      const int d = blk * 8 + lane / 8, cs = lane % 8;
+      const int c = cs ^ ((d >> 1) & 7);
+      lds_dma16(rv, st + KT + blk * 1024, (unsigned)((d * ldvt + kb + c * 8) * 2));
     }
   };
 
@@ -133,30 +126,42 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict
     for (int r = 0; r < 16; ++r) acc_o[t][r] = 0.f;
   float m_run = -INFINITY, l_part = 0.f;
 
-  gload(0);
-  lstore(0);
-  __syncthreads();
+  constexpr int PER = KI + VI;   // loads per wave per tile
+#pragma unroll
+  for (int t = 0; t < NS - 1; ++t)
+    if (t < ntiles) issue(t);
 
   for (int it = 0; it < ntiles; ++it) {
-    const int buf = it & 1;
+    // tile it landed (for every wave), and every wave is done with the stage the next issue overwrites
+    if (it + NS - 2 < ntiles) wait_barrier<(NS - 2) * PER>(); else wait_barrier<0>();
     const int kb = it * BKV;
-    if (it + 1 < ntiles) gload(kb + BKV);
+    char* st = smem + (it % NS) * STAGE;
+    if (kb + BKV > L) {
+      // ragged last tile: V^T columns of keys >= L hold whatever lies past the
+      // keys; zero them (their probabilities are zero, but 0 * NaN is not)
+      for (int e = tid; e < DH * BKV; e += 256) {
+        const int d = e / BKV, s = e % BKV;
+        const int key = kb + swap23(s);
+        if (key >= L) *(bf16_t*)(st + KT + d * 128 + (((s / 8) ^ ((d >> 1) & 7)) * 16) + (s % 8) * 2) = 0;
+      }
+      wait_barrier<0>();
+    }
+    if (it + NS - 1 < ntiles) issue(it + NS - 1);
     const bool active = !CAUSAL || kb <= qw0 + 31;
     if (active && qw0 < L) {
-      // S^T for two 32-key tiles (the first k-step starts from a zero accumulator)
       f32x16 s[2];
       const f32x16 zero = {};
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
-        const bf16_t* kbase = &sK[buf][(t * 32 + li) * LDK + half * 8];
+        const int r = t * 32 + li;
+        const char* krow = st + r * KROWB;
 #pragma unroll
         for (int ks = 0; ks < DH / 16; ++ks) {
-          bf16x8 fk = *(const bf16x8*)(kbase + ks * 16);
+          const int c = ks * 2 + half;
+          bf16x8 fk = *(const bf16x8*)(krow + ((c ^ ksw(r)) * 16));
           s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fk, fq[ks], ks == 0 ? zero : s[t], 0, 0, 0);
         }
       }
-      // tile max of the raw scores (the scale is positive, so it commutes
-      // with the max); masked entries become -inf
       const bool need_mask = (kb + BKV > L) || (CAUSAL && kb + BKV - 1 > qw0);
       if (need_mask) {
 #pragma unroll
@@ -174,10 +179,6 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict
 #pragma unroll
         for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[t][r]);
       mt = fmaxf(mt, __shfl_xor(mt, 32, 64)) * scale_log2;
-      // Lazy rescaling: the running max m_run only moves (and O, l are only
-      // rescaled) when some query of the wave sees its max grow by more than
-      // 2^8; otherwise the probabilities are taken against the stale max and
-      // stay below 256, exactly representable in the same relative precision.
       if (__any((mt > m_run + 8.f) ? 1 : 0)) {
         const float m_new = fmaxf(m_run, mt);
         const float alpha = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
@@ -194,14 +195,11 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          // p = 2^(s * scale - m), one FMA and one v_exp_f32 per score
-          // (results below 2^-126 flush to zero, which a softmax can ignore)
           float p = __builtin_amdgcn_exp2f(fmaf(s[t][r], scale_log2, -m_use));
           s[t][r] = p;
           psum += p;
         }
       l_part += psum;
-      // O^T += V^T P^T over 4 k-steps of 16 keys
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
@@ -218,17 +216,15 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict
             cv.u[3] = pack_bf2(s[t][(2 * ih + 1) * 4 + 2], s[t][(2 * ih + 1) * 4 + 3]);
             fp = cv.v;
           }
-          // stored columns 16 (2t + ih) + 8 half .. + 7 hold this lane's 8 keys
-          const int col = t * 32 + ih * 16 + half * 8;
+          const int c = t * 4 + ih * 2 + half;
 #pragma unroll
           for (int dt = 0; dt < ND; ++dt) {
-            const bf16x8 fv = *(const bf16x8*)&sV[buf][(dt * 32 + li) * LDV + col];
+            const int d = dt * 32 + li;
+            const bf16x8 fv = *(const bf16x8*)(st + KT + d * 128 + ((c ^ ((d >> 1) & 7)) * 16));
             acc_o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fv, fp, acc_o[dt], 0, 0, 0);
           }
         }
     }
-    if (it + 1 < ntiles) lstore(buf ^ 1);
-    __syncthreads();
   }
 
   const float l_tot = l_part + __shfl_xor(l_part, 32, 64);
@@ -252,8 +248,11 @@ hipError_t launch_attn(const bf16_t* q, const bf16_t* k, const bf16_t* vt, int l
                        int L, hipStream_t s) {
   const int nqb = (L + BQ - 1) / BQ;
   const float scale_log2 = 1.4426950408889634f / sqrtf((float)DH);
-  hipLaunchKernelGGL((attn_bf16_kernel<DH, CAUSAL>), dim3(nqb * H * B), dim3(256), 0, s, q, k, vt, ldvt, o, B, H, Hkv,
-                     L, scale_log2);
+  // three stages of 16 KB for dh = 64 (three workgroups per CU), two of 32 KB
+  // for dh = 128 (a third would leave one workgroup per CU)
+  constexpr int NS = DH == 64 ? 3 : 2;
+  hipLaunchKernelGGL((attn_bf16_kernel<DH, CAUSAL, NS>), dim3(nqb * H * B), dim3(256), 0, s, q, k, vt, ldvt, o, B, H,
+                     Hkv, L, scale_log2);
   return hipGetLastError();
 }
 
