@@ -4,17 +4,26 @@
 // With one token per sequence every projection is a skinny product whose
 // cost is streaming the block's weights from HBM once, so the kernels are
 // built around that stream:
-//  * gemv_kernel: each workgroup owns 16 output rows (8 when 16-row tiles
-//    would leave fewer than two workgroups per CU) and streams their weights
-//    over all of K from the packed slab-major layout (the rows' 128 bytes are
-//    contiguous per 64-k slab), 16 loads of 16 bytes in flight per lane
-//    per K chunk, products and accumulation in fp32.  The activation
-//    row is built in LDS while staging: RMSNorm is fused there (QKV,
-//    gate/up; each workgroup recomputes the row's scale, d floats per row);
+//  * gemv_stream_kernel: each workgroup owns 16 output rows (8 when 16-row
+//    tiles would leave fewer than two workgroups per CU) and streams their
+//    weights over all of K from the packed slab-major layout (the rows' 128
+//    bytes are contiguous per 64-k slab).  The input rows are staged into LDS
+//    once, in bf16, before the main loop: RMSNorm is fused there (QKV,
+//    gate/up; each workgroup recomputes the row's scale, d floats per row).
 //    SwiGLU runs once in a small kernel whose bf16 rows the down projection
-//    stages as they are, like the attention output for the O projection.
-//    Epilogues: raw fp32 store or fp32 residual add.
-//  * attn_decode_kernel: one workgroup per (sequence, head, 256-key split);
+//    stages as they are, like the attention output for the O projection
+//    (recomputing it per workgroup from the fp32 gate/up rows reads four
+//    times the bytes per workgroup and measured 14 us slower per launch).
+//    The main loop has no barrier, so two 1024-k chunks of weights
+//    (up to 16 loads of 16 bytes per lane) stay in flight; slabs past K read
+//    as zero through the buffer resource, so the loop has no branches.
+//    Products and accumulation in fp32.  Epilogues: raw fp32 store or fp32
+//    residual add.
+//  * gemv_chunk_kernel: the same product staging the input chunk by chunk
+//    (2048 k at a time, a barrier around each), for inputs too wide for the
+//    streaming kernel's LDS (four rows of a d_ff-wide input) or too short to
+//    fill its chunks.
+//  * attn_decode_kernel: one workgroup per (sequence, head, 128-key split);
 //    applies RoPE to q and to the new key at the token's position, appends the
 //    new key and value to the cache, and writes (max, sum, unnormalised
 //    output) partials that a small kernel combines into the bf16 attention
@@ -31,7 +40,7 @@ namespace {
 
 constexpr int GV_KCH = 2048;       // K elements staged per chunk
 constexpr int GV_MB = 4;           // largest batch
-constexpr int ATT_KC = 256;        // keys per attention split
+constexpr int ATT_KC = 128;        // keys per attention split
 
 __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
@@ -75,6 +84,14 @@ struct StageNorm {
     for (int b = 0; b < B; ++b)
       for (int i = tid; i < n; i += 256) xs[b * GV_KCH + i] = f2bf(h[(size_t)b * K + k0 + i] * sc[b] * g[k0 + i]);
   }
+  // dst[0, K) = row b, normalised (K % 4 == 0)
+  __device__ void fill_row(bf16_t* dst, const float* sc, int b, int K, int tid) const {
+    const float s = sc[b];
+    for (int i = tid * 4; i < K; i += 256 * 4) {
+      const f32x4 x = *(const f32x4*)(h + (size_t)b * K + i), gg = *(const f32x4*)(g + i);
+      *(u32x2*)(dst + i) = u32x2{pack_bf2(x[0] * s * gg[0], x[1] * s * gg[1]), pack_bf2(x[2] * s * gg[2], x[3] * s * gg[3])};
+    }
+  }
 };
 
 // x = a bf16 row already in global memory, a[B][K]
@@ -86,7 +103,12 @@ struct StageCopy {
       for (int i = tid * 8; i < n; i += 256 * 8)
         *(u32x4*)(xs + b * GV_KCH + i) = *(const u32x4*)(a + (size_t)b * K + k0 + i);
   }
+  __device__ void fill_row(bf16_t* dst, const float*, int b, int K, int tid) const {
+    for (int i = tid * 8; i < K; i += 256 * 8) *(u32x4*)(dst + i) = *(const u32x4*)(a + (size_t)b * K + i);
+  }
 };
+
+
 
 // a[b][f] = bf16(silu(gate) * up) from the raw gate/up product gu[B][2*fpad]
 // in the packed row order (each group of 64 rows: 32 gate rows, then their 32
@@ -122,7 +144,7 @@ struct EpiAdd {  // h[b][n] += acc
 // out[b][n] for n in [blockIdx.x*ROWS, +ROWS), b < B: the dot of row n of
 // the packed W [K/64][nblk][128][64] with the staged input row b.
 template <int ROWS, class Stage, class Epi>
-__global__ __launch_bounds__(256) void gemv_kernel(Stage sg, const bf16_t* __restrict__ W, int nblk, int N, int K,
+__global__ __launch_bounds__(256) void gemv_chunk_kernel(Stage sg, const bf16_t* __restrict__ W, int nblk, int N, int K,
                                                    int B, Epi epi) {
   constexpr int GV_ROWS = ROWS, J = ROWS / 8;  // rows per workgroup, 8-row groups per lane
   __shared__ __attribute__((aligned(16))) bf16_t xs[GV_MB * GV_KCH];
@@ -207,15 +229,143 @@ __global__ __launch_bounds__(256) void gemv_kernel(Stage sg, const bf16_t* __res
   }
 }
 
+constexpr int GS_KC = 1024;  // k per chunk of the streaming kernel: 16 slabs, 4 per wave
+constexpr int GS_D = 2;      // chunks in flight per lane
+
+__device__ __forceinline__ u32x4 buffer_load16(__amdgpu_buffer_rsrc_t r, unsigned off) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+
+// out[b][n] for n in [blockIdx.x*ROWS, +ROWS), b < B, over the input rows
+// staged whole in LDS (xs[B][Kp], zero past K; Kp a multiple of GS_KC*GS_D).
+template <int ROWS, class Stage, class Epi>
+__global__ __launch_bounds__(256) void gemv_stream_kernel(Stage sg, const bf16_t* __restrict__ W, int nblk, int N,
+                                                          int K, int B, int Kp, Epi epi) {
+  constexpr int J = ROWS / 8, U = GS_KC / 64 / 4;
+  extern __shared__ __attribute__((aligned(16))) bf16_t xs[];
+  __shared__ float red[4 * ROWS * GV_MB];
+  __shared__ float sc[GV_MB];
+  __shared__ float tmp[4];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n0 = blockIdx.x * ROWS;
+  const int r8 = lane >> 3, c8 = lane & 7;
+  // rows n0 + r8 + 8 j lie in the same 128-row block (ROWS | 128)
+  const int blk = n0 / SLAB_N, ra = n0 % SLAB_N + r8;
+  // the whole packed matrix; slabs past K read as zero
+  const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)W, (short)0, (int)((size_t)(K / 64) * nblk * SLAB_N * 64 * 2), 0x00020000);
+  const unsigned slab_stride = (unsigned)nblk * SLAB_N * 64 * 2;
+  const unsigned lane_off = (unsigned)(((size_t)blk * SLAB_N + ra) * 64 * 2 + c8 * 16);
+  // chunk c, wave w: slabs c*16 + w + 4u
+  u32x4 wv[GS_D][U][J];
+  auto issue = [&](int d, int c) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const unsigned sl = (unsigned)(c * 16 + wave + 4 * u);
+#pragma unroll
+      for (int j = 0; j < J; ++j) wv[d][u][j] = buffer_load16(rw, sl * slab_stride + lane_off + j * 8 * 64 * 2);
+    }
+  };
+#pragma unroll
+  for (int d = 0; d < GS_D; ++d) issue(d, d);
+  // the input rows (these barriers also give the first chunks time to land)
+  sg.prepare(sc, B, K, tid, tmp);
+  for (int b = 0; b < B; ++b) {
+    sg.fill_row(xs + (size_t)b * Kp, sc, b, K, tid);
+    for (int i = K + tid; i < Kp; i += 256) xs[(size_t)b * Kp + i] = 0;
+  }
+  __syncthreads();
+  float acc[J][GV_MB];
+#pragma unroll
+  for (int j = 0; j < J; ++j)
+#pragma unroll
+    for (int b = 0; b < GV_MB; ++b) acc[j][b] = 0.f;
+  const int nch = Kp / GS_KC;
+  for (int c0 = 0; c0 < nch; c0 += GS_D) {
+#pragma unroll
+    for (int d = 0; d < GS_D; ++d) {
+      const int c = c0 + d;
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int sl = c * 16 + wave + 4 * u;
+#pragma unroll
+        for (int b = 0; b < GV_MB; ++b)
+          if (b < B) {
+            const u32x4 xv = *(const u32x4*)(xs + (size_t)b * Kp + sl * 64 + c8 * 8);
+#pragma unroll
+            for (int j = 0; j < J; ++j) acc[j][b] = dot8(wv[d][u][j], xv, acc[j][b]);
+          }
+      }
+      issue(d, c + GS_D);  // past the last chunk: reads past K, zero and unused
+    }
+  }
+  // reduce over the 8 lanes of a row, then over the 4 waves
+#pragma unroll
+  for (int j = 0; j < J; ++j)
+#pragma unroll
+    for (int b = 0; b < GV_MB; ++b) {
+      float v = acc[j][b];
+      v += __shfl_xor(v, 1);
+      v += __shfl_xor(v, 2);
+      v += __shfl_xor(v, 4);
+      acc[j][b] = v;
+    }
+  if (c8 == 0)
+#pragma unroll
+    for (int j = 0; j < J; ++j)
+#pragma unroll
+      for (int b = 0; b < GV_MB; ++b) red[(wave * ROWS + r8 + 8 * j) * GV_MB + b] = acc[j][b];
+  __syncthreads();
+  if (tid < ROWS * GV_MB) {
+    const int row = tid / GV_MB, b = tid % GV_MB;
+    const int nn = n0 + row;
+    if (b < B && nn < N) {
+      float v = 0.f;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) v += red[(w * ROWS + row) * GV_MB + b];
+      epi(b, nn, v);
+    }
+  }
+}
+
+// the streaming kernel's input rows: B * Kp bf16 in LDS
+inline int stream_kp(int K) { return (K + GS_KC * GS_D - 1) / (GS_KC * GS_D) * (GS_KC * GS_D); }
+inline bool use_stream(int K, int B) { return K >= GS_KC && (size_t)B * stream_kp(K) * 2 <= 48 * 1024; }
+
+template <class Stage, class Epi>
+hipError_t gemv_stream(const Stage& sg, const WOperand& W, int N, int K, int B, const Epi& epi, hipStream_t s) {
+  const int Kp = stream_kp(K);
+  const size_t lds = (size_t)B * Kp * 2;
+  // the buffer resource's size and the offsets (up to 16 slabs past Kp) fit in 31 bits
+  if ((size_t)(Kp / 64 + 16) * W.nblk * SLAB_N * 64 * 2 >= (1ull << 31)) return hipErrorInvalidValue;
+  if ((N + 15) / 16 >= 512)
+    hipLaunchKernelGGL((gemv_stream_kernel<16, Stage, Epi>), dim3((N + 15) / 16), dim3(256), lds, s, sg, W.p, W.nblk,
+                       N, K, B, Kp, epi);
+  else
+    hipLaunchKernelGGL((gemv_stream_kernel<8, Stage, Epi>), dim3((N + 7) / 8), dim3(256), lds, s, sg, W.p, W.nblk, N,
+                       K, B, Kp, epi);
+  return hipGetLastError();
+}
+
+template <class Stage, class Epi>
+hipError_t gemv_chunk(const Stage& sg, const WOperand& W, int N, int K, int B, const Epi& epi, hipStream_t s) {
+  if ((N + 15) / 16 >= 512)
+    hipLaunchKernelGGL((gemv_chunk_kernel<16, Stage, Epi>), dim3((N + 15) / 16), dim3(256), 0, s, sg, W.p, W.nblk, N,
+                       K, B, epi);
+  else
+    hipLaunchKernelGGL((gemv_chunk_kernel<8, Stage, Epi>), dim3((N + 7) / 8), dim3(256), 0, s, sg, W.p, W.nblk, N, K,
+                       B, epi);
+  return hipGetLastError();
+}
+
+inline bool gemv_args_ok(const WOperand& W, int N, int K, int B) {
+  return B > 0 && B <= GV_MB && K % 64 == 0 && N > 0 && W.nblk * SLAB_N >= (N + 15) / 16 * 16;
+}
+
 template <class Stage, class Epi>
 hipError_t gemv(const Stage& sg, const WOperand& W, int N, int K, int B, const Epi& epi, hipStream_t s) {
-  if (B <= 0 || B > GV_MB || K % 64 || N <= 0 || W.nblk * SLAB_N < (N + 15) / 16 * 16) return hipErrorInvalidValue;
-  if ((N + 15) / 16 >= 512)
-    hipLaunchKernelGGL((gemv_kernel<16, Stage, Epi>), dim3((N + 15) / 16), dim3(256), 0, s, sg, W.p, W.nblk, N, K, B,
-                       epi);
-  else
-    hipLaunchKernelGGL((gemv_kernel<8, Stage, Epi>), dim3((N + 7) / 8), dim3(256), 0, s, sg, W.p, W.nblk, N, K, B, epi);
-  return hipGetLastError();
+  if (!gemv_args_ok(W, N, K, B)) return hipErrorInvalidValue;
+  return use_stream(K, B) ? gemv_stream(sg, W, N, K, B, epi, s) : gemv_chunk(sg, W, N, K, B, epi, s);
 }
 
 // packed QKV row of true dimension d of a head (the packing keeps every
@@ -235,7 +385,7 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const float* __restric
                                                           int nsplit, float* __restrict__ part) {
   constexpr int DL = DH / 8;  // dims per lane (8 lanes per key)
   __shared__ float sq[DH];
-  __shared__ bf16_t knew[DH], vnew[DH];
+  __shared__ __attribute__((aligned(16))) bf16_t knew[DH], vnew[DH];
   __shared__ float wm[4], wl[4];
   __shared__ float wo[4][DH];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -275,46 +425,67 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const float* __restric
   float q[DL];
 #pragma unroll
   for (int e = 0; e < DL; ++e) q[e] = sq[i8 * DL + e];
-  float m = -INFINITY, l = 0.f, o[DL];
-#pragma unroll
-  for (int e = 0; e < DL; ++e) o[e] = 0.f;
+  // rounds of 32 keys (8 per wave, 8 lanes per key); every key of this
+  // lane's rounds is loaded before any is used -- one round trip to memory,
+  // not one per round.  Keys past the split's end load its last key (in
+  // bounds) and are masked; the token's own key and value come from LDS,
+  // since the workgroup appending them to the cache may not have run yet.
+  constexpr int R = ATT_KC / 32, C = DL / 8;
   const int kbeg = split * ATT_KC, kend = min(pos + 1, kbeg + ATT_KC);
   const bf16_t* kb = kc + ((size_t)b * Hkv + hk) * L_cap * DH;
   const bf16_t* vb = vc + ((size_t)b * Hkv + hk) * L_cap * DH;
-  for (int j = kbeg + wave * 8 + g; j < kend; j += 32) {
-    float kk[DL], vv[DL];
-    if (j == pos) {
+  u32x4 kw[R][C], vw[R][C];
 #pragma unroll
-      for (int e = 0; e < DL; ++e) {
-        kk[e] = bf2f(knew[i8 * DL + e]);
-        vv[e] = bf2f(vnew[i8 * DL + e]);
-      }
-    } else {
+  for (int r = 0; r < R; ++r) {
+    const int j = min(kbeg + r * 32 + wave * 8 + g, kend - 1);
 #pragma unroll
-      for (int c = 0; c < DL / 8; ++c) {
-        const u32x4 kw = *(const u32x4*)(kb + (size_t)j * DH + i8 * DL + c * 8);
-        const u32x4 vw = *(const u32x4*)(vb + (size_t)j * DH + i8 * DL + c * 8);
+    for (int c = 0; c < C; ++c) {
+      kw[r][c] = *(const u32x4*)(kb + (size_t)j * DH + i8 * DL + c * 8);
+      vw[r][c] = *(const u32x4*)(vb + (size_t)j * DH + i8 * DL + c * 8);
+    }
+  }
+  float sd[R];
+  float m = -INFINITY;
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          kk[c * 8 + 2 * t] = bf_lo(kw[t]);
-          kk[c * 8 + 2 * t + 1] = bf_hi(kw[t]);
-          vv[c * 8 + 2 * t] = bf_lo(vw[t]);
-          vv[c * 8 + 2 * t + 1] = bf_hi(vw[t]);
-        }
+  for (int r = 0; r < R; ++r) {
+    const int j = kbeg + r * 32 + wave * 8 + g;
+    if (last && j == pos) {
+#pragma unroll
+      for (int c = 0; c < C; ++c) {
+        kw[r][c] = *(const u32x4*)(knew + i8 * DL + c * 8);
+        vw[r][c] = *(const u32x4*)(vnew + i8 * DL + c * 8);
       }
     }
     float sdot = 0.f;
 #pragma unroll
-    for (int e = 0; e < DL; ++e) sdot += q[e] * kk[e];
+    for (int c = 0; c < C; ++c)
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        sdot = fmaf(q[c * 8 + 2 * t], bf_lo(kw[r][c][t]), sdot);
+        sdot = fmaf(q[c * 8 + 2 * t + 1], bf_hi(kw[r][c][t]), sdot);
+      }
     sdot += __shfl_xor(sdot, 1);
     sdot += __shfl_xor(sdot, 2);
     sdot += __shfl_xor(sdot, 4);
-    const float mn = fmaxf(m, sdot);
-    const float a = exp2f(m - mn), p = exp2f(sdot - mn);
-    l = l * a + p;
+    sd[r] = j < kend ? sdot : -INFINITY;
+    m = fmaxf(m, sd[r]);
+  }
+  // this lane group's keys against their own maximum (none valid: l = o = 0)
+  const float mu = m == -INFINITY ? 0.f : m;
+  float l = 0.f, o[DL];
 #pragma unroll
-    for (int e = 0; e < DL; ++e) o[e] = o[e] * a + p * vv[e];
-    m = mn;
+  for (int e = 0; e < DL; ++e) o[e] = 0.f;
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const float p = exp2f(sd[r] - mu);
+    l += p;
+#pragma unroll
+    for (int c = 0; c < C; ++c)
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        o[c * 8 + 2 * t] = fmaf(p, bf_lo(vw[r][c][t]), o[c * 8 + 2 * t]);
+        o[c * 8 + 2 * t + 1] = fmaf(p, bf_hi(vw[r][c][t]), o[c * 8 + 2 * t + 1]);
+      }
   }
   // combine the 8 key groups of the wave (lanes 8 apart share dims)
 #pragma unroll
@@ -358,39 +529,41 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const float* __restric
 
 // o[b][h*dh + d] = bf16(sum_s 2^(m_s - m) o_s[d] / sum_s 2^(m_s - m) l_s) over
 // the split-key partials part[B][H][nsplit][2 + dh]: one workgroup per
-// (b, h), one thread per dimension; every split's values are loaded before
-// they are combined (independent loads, not a dependent chain)
+// (b, h), one thread per dimension.  Every split's values are loaded before
+// any is combined, without branches (indices past the last split repeat it
+// and get weight zero): per-element branches around the loads made the
+// compiler wait for each load in turn.
 template <int DH>
 __global__ __launch_bounds__(DH) void combine_kernel(const float* __restrict__ part, int nsplit,
                                                      bf16_t* __restrict__ o) {
-  constexpr int MAXS = 32;
+  constexpr int MAXS = 16;
   const int bh = blockIdx.x, d = threadIdx.x, stride = 2 + DH;
   const float* p = part + (size_t)bh * nsplit * stride;
   float m = -INFINITY, l = 0.f, acc = 0.f;
   for (int s0 = 0; s0 < nsplit; s0 += MAXS) {
-    const int n = min(MAXS, nsplit - s0);
     float ms[MAXS], ls[MAXS], os[MAXS];
 #pragma unroll
-    for (int s = 0; s < MAXS; ++s)
-      if (s < n) {
-        ms[s] = p[(s0 + s) * stride];
-        ls[s] = p[(s0 + s) * stride + 1];
-        os[s] = p[(s0 + s) * stride + 2 + d];
-      }
-    float mn = m;
+    for (int s = 0; s < MAXS; ++s) {
+      const int si = min(s0 + s, nsplit - 1);
+      ms[s] = p[si * stride];
+      ls[s] = p[si * stride + 1];
+      os[s] = p[si * stride + 2 + d];
+    }
 #pragma unroll
     for (int s = 0; s < MAXS; ++s)
-      if (s < n) mn = fmaxf(mn, ms[s]);
+      if (s0 + s >= nsplit) ms[s] = -INFINITY;
+    float mn = m;
+#pragma unroll
+    for (int s = 0; s < MAXS; ++s) mn = fmaxf(mn, ms[s]);
     const float r = m == -INFINITY ? 0.f : exp2f(m - mn);
     l *= r;
     acc *= r;
 #pragma unroll
-    for (int s = 0; s < MAXS; ++s)
-      if (s < n) {
-        const float w = exp2f(ms[s] - mn);
-        l += w * ls[s];
-        acc += w * os[s];
-      }
+    for (int s = 0; s < MAXS; ++s) {
+      const float w = ms[s] == -INFINITY ? 0.f : exp2f(ms[s] - mn);
+      l += w * ls[s];
+      acc += w * os[s];
+    }
     m = mn;
   }
   o[(size_t)bh * DH + d] = f2bf(acc / l);
@@ -401,6 +574,10 @@ __global__ __launch_bounds__(DH) void combine_kernel(const float* __restrict__ p
 hipError_t decode_qkv(const float* h, const float* g, float eps, const WOperand& W, float* raw, int B, int N, int K,
                       hipStream_t s) {
   return gemv(StageNorm{h, g, eps}, W, N, K, B, EpiRaw{raw, N}, s);
+}
+
+size_t decode_attention_scratch(int B, int H, int dh, int pos) {
+  return (size_t)B * H * (pos / ATT_KC + 1) * (2 + dh) * sizeof(float);
 }
 
 hipError_t decode_attention(const float* qkv, int qkv_n, const float* rope_cos, const float* rope_sin, bf16_t* kc,
@@ -437,6 +614,7 @@ hipError_t decode_up(const float* h, const float* g, float eps, const WOperand& 
 
 hipError_t decode_down(const float* gu, int F, int fpad, const WOperand& W, float* h, bf16_t* a, int B, int N,
                        hipStream_t s) {
+  if (!gemv_args_ok(W, N, fpad, B)) return hipErrorInvalidValue;
   const int n = B * fpad;
   hipLaunchKernelGGL(swiglu_kernel, dim3((n + 255) / 256), dim3(256), 0, s, gu, F, fpad, B, a);
   hipError_t e = hipGetLastError();

@@ -94,8 +94,9 @@ hipError_t decode_qkv(const float* h, const float* g, float eps, const WOperand&
                       hipStream_t s);
 // Attention of the token at position pos over cache rows [0, pos] of
 // kc/vc [B][Hkv][L_cap][dh]: RoPE on q and the new key, the new key and value
-// appended at pos, o[B][H*dh] (bf16).  Scratch: split-key partials
-// part[B][H][pos / 256 + 1][2 + dh].
+// appended at pos, o[B][H*dh] (bf16).  Scratch: split-key partials, fp32,
+// decode_attention_scratch(B, H, dh, pos) bytes.
+size_t decode_attention_scratch(int B, int H, int dh, int pos);
 hipError_t decode_attention(const float* qkv, int qkv_n, const float* rope_cos, const float* rope_sin, bf16_t* kc,
                             bf16_t* vc, int L_cap, int pos, int B, int H, int Hkv, int dh, float* part, bf16_t* o,
                             hipStream_t s);

@@ -839,8 +839,7 @@ Status decode_step(vla_ctx* c, uint64_t frame_id, const void* x, int B, int pos,
   // scratch borrowed from the prefill workspace
   Workspace& ws = c->ws[VLA_STACK_LLM];
   const size_t M = s.m_max;
-  const int nsplit = pos / 256 + 1;
-  if ((size_t)B * s.qkv_n * 4 > M * s.hd * 2 || (size_t)B * H * nsplit * (2 + dh) * 4 > M * s.hd * 2 ||
+  if ((size_t)B * s.qkv_n * 4 > M * s.hd * 2 || vla::decode_attention_scratch(B, H, dh, pos) > M * s.hd * 2 ||
       (size_t)B * 2 * s.f_pad * 4 > M * s.f_pad * 2 || (size_t)B * s.hd > M * d || (size_t)B * s.f_pad > M * d)
     return fail(VLA_ERR_SHAPE, "workspace too small for a decode step at position %d (raise max_tokens)", pos);
   for (auto& sl : c->slots)

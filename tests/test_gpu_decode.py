@@ -50,7 +50,7 @@ def _oracle_rows(wl, W, toks, L, steps, k):
 @pytest.mark.parametrize("name,shape,B,L,k", [
     ("dec_gqa", llama_like(2, 256, 4, 2, 64, 704), 2, 77, 2),
     ("dec_dh128", llama_like(2, 256, 2, 1, 128, 512), 1, 130, 2),
-    ("dec_split", llama_like(1, 192, 3, 3, 64, 448), 2, 300, 1),   # keys cross a 256-key split
+    ("dec_split", llama_like(1, 192, 3, 3, 64, 448), 2, 300, 1),   # keys cross two 128-key splits
     ("dec_short", llama_like(3, 128, 2, 2, 64, 320), 1, 1, 3),     # a one-token prefix
 ])
 def test_decode_steps_match_oracle(name, shape, B, L, k):
