@@ -52,6 +52,10 @@ def _oracle_rows(wl, W, toks, L, steps, k):
     ("dec_dh128", llama_like(2, 256, 2, 1, 128, 512), 1, 130, 2),
     ("dec_split", llama_like(1, 192, 3, 3, 64, 448), 2, 300, 1),   # keys cross two 128-key splits
     ("dec_short", llama_like(3, 128, 2, 2, 64, 320), 1, 1, 3),     # a one-token prefix
+    # d = 1024 and d_ff = 2816: every product takes the streaming GEMV (input
+    # rows staged whole in LDS), with three and four sequences
+    ("dec_stream4", llama_like(2, 1024, 8, 2, 128, 2816), 4, 100, 2),
+    ("dec_stream3", llama_like(1, 1024, 16, 4, 64, 2816), 3, 257, 1),
 ])
 def test_decode_steps_match_oracle(name, shape, B, L, k):
     steps = 3
