@@ -10,10 +10,12 @@
 //    bytes are contiguous per 64-k slab).  The input rows are staged into LDS
 //    once, in bf16, before the main loop: RMSNorm is fused there (QKV,
 //    gate/up; each workgroup recomputes the row's scale, d floats per row).
-//    SwiGLU runs once in a small kernel whose bf16 rows the down projection
-//    stages as they are, like the attention output for the O projection
-//    (recomputing it per workgroup from the fp32 gate/up rows reads four
-//    times the bytes per workgroup and measured 14 us slower per launch).
+//    The gate/up product runs paired: a workgroup owns 16 features' gate
+//    rows and their up rows and writes the gated bf16 activation, which the
+//    down projection stages as it is, like the attention output for the O
+//    projection.  (Gating inside the down projection's staging instead, from
+//    the fp32 gate/up rows, reads four times the bytes per workgroup and
+//    measured 14 us slower per launch.)
 //    The main loop has no barrier, so two 1024-k chunks of weights
 //    (up to 16 loads of 16 bytes per lane) stay in flight; slabs past K read
 //    as zero through the buffer resource, so the loop has no branches.
@@ -112,19 +114,15 @@ struct StageCopy {
 
 // a[b][f] = bf16(silu(gate) * up) from the raw gate/up product gu[B][2*fpad]
 // in the packed row order (each group of 64 rows: 32 gate rows, then their 32
-// up rows); columns [F, fpad) are zero
-__global__ __launch_bounds__(256) void swiglu_kernel(const float* __restrict__ gu, int F, int fpad, int B,
+// up rows).  Features past d_ff have zero weight rows, so they come out zero.
+__global__ __launch_bounds__(256) void swiglu_kernel(const float* __restrict__ gu, int fpad, int B,
                                                      bf16_t* __restrict__ a) {
   const int i = blockIdx.x * 256 + threadIdx.x;
   if (i >= B * fpad) return;
   const int b = i / fpad, f = i % fpad;
-  float v = 0.f;
-  if (f < F) {
-    const float* r = gu + (size_t)b * 2 * fpad + (f / 32) * 64 + f % 32;
-    const float g = r[0];
-    v = g / (1.f + __expf(-g)) * r[32];
-  }
-  a[i] = f2bf(v);
+  const float* r = gu + (size_t)b * 2 * fpad + (f / 32) * 64 + f % 32;
+  const float g = r[0];
+  a[i] = f2bf(g / (1.f + __expf(-g)) * r[32]);
 }
 
 // ---------------------------------------------------------------- epilogues
@@ -139,6 +137,15 @@ struct EpiAdd {  // h[b][n] += acc
   float* h;
   int ld;
   __device__ void operator()(int b, int n, float v) const { h[(size_t)b * ld + n] += v; }
+};
+
+// a[b][f] = bf16(silu(gate) * up), from the gate and up sums of feature f
+struct EpiGated {
+  bf16_t* a;
+  int ld;
+  __device__ void operator()(int b, int f, float g, float u) const {
+    a[(size_t)b * ld + f] = f2bf(g / (1.f + __expf(-g)) * u);
+  }
 };
 
 // out[b][n] for n in [blockIdx.x*ROWS, +ROWS), b < B: the dot of row n of
@@ -237,33 +244,50 @@ __device__ __forceinline__ u32x4 buffer_load16(__amdgpu_buffer_rsrc_t r, unsigne
 }
 
 // out[b][n] for n in [blockIdx.x*ROWS, +ROWS), b < B, over the input rows
-// staged whole in LDS (xs[B][Kp], zero past K; Kp a multiple of GS_KC*GS_D).
-template <int ROWS, class Stage, class Epi>
+// staged whole in LDS (xs[B][Kp], zero past K; Kp a multiple of KC*GS_D).
+// PAIR: the gate/up product with SwiGLU in the epilogue.  Workgroup w owns
+// features [16 w, 16 w + 16): their 16 gate rows and 16 up rows, 32 rows apart
+// in the packed order (each 64-row group: 32 gate rows, then their 32 up
+// rows), and epi(b, f, gate, up) writes the gated activation.
+template <int ROWS, bool PAIR, class Stage, class Epi>
 __global__ __launch_bounds__(256) void gemv_stream_kernel(Stage sg, const bf16_t* __restrict__ W, int nblk, int N,
                                                           int K, int B, int Kp, Epi epi) {
-  constexpr int J = ROWS / 8, U = GS_KC / 64 / 4;
+  static_assert(!PAIR || ROWS == 32, "a paired workgroup owns 16 gate and 16 up rows");
+  constexpr int J = ROWS / 8;
+  constexpr int KC = PAIR ? GS_KC / 2 : GS_KC;  // the paired kernel keeps the same bytes in flight
+  constexpr int U = KC / 64 / 4;
+  constexpr int SPC = KC / 64;                 // slabs per chunk
   extern __shared__ __attribute__((aligned(16))) bf16_t xs[];
   __shared__ float red[4 * ROWS * GV_MB];
   __shared__ float sc[GV_MB];
   __shared__ float tmp[4];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int n0 = blockIdx.x * ROWS;
   const int r8 = lane >> 3, c8 = lane & 7;
-  // rows n0 + r8 + 8 j lie in the same 128-row block (ROWS | 128)
-  const int blk = n0 / SLAB_N, ra = n0 % SLAB_N + r8;
+  // this lane's rows: block blk, rows rb + roff(j) inside it (all in one 128-row block)
+  int blk, rb;
+  if constexpr (PAIR) {
+    const int w = blockIdx.x;
+    blk = w / 4;
+    rb = 64 * ((w / 2) % 2) + 16 * (w % 2) + r8;
+  } else {
+    const int n0 = blockIdx.x * ROWS;
+    blk = n0 / SLAB_N;
+    rb = n0 % SLAB_N + r8;
+  }
+  auto roff = [](int j) { return PAIR ? 8 * (j % 2) + 32 * (j / 2) : 8 * j; };
   // the whole packed matrix; slabs past K read as zero
   const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
       (void*)W, (short)0, (int)((size_t)(K / 64) * nblk * SLAB_N * 64 * 2), 0x00020000);
   const unsigned slab_stride = (unsigned)nblk * SLAB_N * 64 * 2;
-  const unsigned lane_off = (unsigned)(((size_t)blk * SLAB_N + ra) * 64 * 2 + c8 * 16);
-  // chunk c, wave w: slabs c*16 + w + 4u
+  const unsigned lane_off = (unsigned)(((size_t)blk * SLAB_N + rb) * 64 * 2 + c8 * 16);
+  // chunk c, wave w: slabs c*SPC + w + 4u
   u32x4 wv[GS_D][U][J];
   auto issue = [&](int d, int c) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const unsigned sl = (unsigned)(c * 16 + wave + 4 * u);
+      const unsigned sl = (unsigned)(c * SPC + wave + 4 * u);
 #pragma unroll
-      for (int j = 0; j < J; ++j) wv[d][u][j] = buffer_load16(rw, sl * slab_stride + lane_off + j * 8 * 64 * 2);
+      for (int j = 0; j < J; ++j) wv[d][u][j] = buffer_load16(rw, sl * slab_stride + lane_off + roff(j) * 64 * 2);
     }
   };
 #pragma unroll
@@ -280,14 +304,14 @@ __global__ __launch_bounds__(256) void gemv_stream_kernel(Stage sg, const bf16_t
   for (int j = 0; j < J; ++j)
 #pragma unroll
     for (int b = 0; b < GV_MB; ++b) acc[j][b] = 0.f;
-  const int nch = Kp / GS_KC;
+  const int nch = Kp / KC;
   for (int c0 = 0; c0 < nch; c0 += GS_D) {
 #pragma unroll
     for (int d = 0; d < GS_D; ++d) {
       const int c = c0 + d;
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        const int sl = c * 16 + wave + 4 * u;
+        const int sl = c * SPC + wave + 4 * u;
 #pragma unroll
         for (int b = 0; b < GV_MB; ++b)
           if (b < B) {
@@ -299,7 +323,8 @@ __global__ __launch_bounds__(256) void gemv_stream_kernel(Stage sg, const bf16_t
       issue(d, c + GS_D);  // past the last chunk: reads past K, zero and unused
     }
   }
-  // reduce over the 8 lanes of a row, then over the 4 waves
+  // reduce over the 8 lanes of a row, then over the 4 waves; red row r8 + 8 j
+  // is this lane's row j (paired: rows 0-15 gate, 16-31 their up partners)
 #pragma unroll
   for (int j = 0; j < J; ++j)
 #pragma unroll
@@ -316,14 +341,29 @@ __global__ __launch_bounds__(256) void gemv_stream_kernel(Stage sg, const bf16_t
 #pragma unroll
       for (int b = 0; b < GV_MB; ++b) red[(wave * ROWS + r8 + 8 * j) * GV_MB + b] = acc[j][b];
   __syncthreads();
-  if (tid < ROWS * GV_MB) {
-    const int row = tid / GV_MB, b = tid % GV_MB;
-    const int nn = n0 + row;
-    if (b < B && nn < N) {
-      float v = 0.f;
+  if constexpr (PAIR) {
+    if (tid < 16 * GV_MB) {
+      const int fl = tid / GV_MB, b = tid % GV_MB;
+      if (b < B) {
+        float g = 0.f, u = 0.f;
 #pragma unroll
-      for (int w = 0; w < 4; ++w) v += red[(w * ROWS + row) * GV_MB + b];
-      epi(b, nn, v);
+        for (int w = 0; w < 4; ++w) {
+          g += red[(w * ROWS + fl) * GV_MB + b];
+          u += red[(w * ROWS + 16 + fl) * GV_MB + b];
+        }
+        epi(b, blockIdx.x * 16 + fl, g, u);
+      }
+    }
+  } else {
+    if (tid < ROWS * GV_MB) {
+      const int row = tid / GV_MB, b = tid % GV_MB;
+      const int nn = blockIdx.x * ROWS + row;
+      if (b < B && nn < N) {
+        float v = 0.f;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) v += red[(w * ROWS + row) * GV_MB + b];
+        epi(b, nn, v);
+      }
     }
   }
 }
@@ -331,19 +371,22 @@ __global__ __launch_bounds__(256) void gemv_stream_kernel(Stage sg, const bf16_t
 // the streaming kernel's input rows: B * Kp bf16 in LDS
 inline int stream_kp(int K) { return (K + GS_KC * GS_D - 1) / (GS_KC * GS_D) * (GS_KC * GS_D); }
 inline bool use_stream(int K, int B) { return K >= GS_KC && (size_t)B * stream_kp(K) * 2 <= 48 * 1024; }
+// the buffer resource's size and the offsets (up to 16 slabs past Kp) fit in 31 bits
+inline bool stream_offsets_ok(const WOperand& W, int Kp) {
+  return (size_t)(Kp / 64 + 16) * W.nblk * SLAB_N * 64 * 2 < (1ull << 31);
+}
 
 template <class Stage, class Epi>
 hipError_t gemv_stream(const Stage& sg, const WOperand& W, int N, int K, int B, const Epi& epi, hipStream_t s) {
   const int Kp = stream_kp(K);
   const size_t lds = (size_t)B * Kp * 2;
-  // the buffer resource's size and the offsets (up to 16 slabs past Kp) fit in 31 bits
-  if ((size_t)(Kp / 64 + 16) * W.nblk * SLAB_N * 64 * 2 >= (1ull << 31)) return hipErrorInvalidValue;
+  if (!stream_offsets_ok(W, Kp)) return hipErrorInvalidValue;
   if ((N + 15) / 16 >= 512)
-    hipLaunchKernelGGL((gemv_stream_kernel<16, Stage, Epi>), dim3((N + 15) / 16), dim3(256), lds, s, sg, W.p, W.nblk,
-                       N, K, B, Kp, epi);
+    hipLaunchKernelGGL((gemv_stream_kernel<16, false, Stage, Epi>), dim3((N + 15) / 16), dim3(256), lds, s, sg, W.p,
+                       W.nblk, N, K, B, Kp, epi);
   else
-    hipLaunchKernelGGL((gemv_stream_kernel<8, Stage, Epi>), dim3((N + 7) / 8), dim3(256), lds, s, sg, W.p, W.nblk, N,
-                       K, B, Kp, epi);
+    hipLaunchKernelGGL((gemv_stream_kernel<8, false, Stage, Epi>), dim3((N + 7) / 8), dim3(256), lds, s, sg, W.p,
+                       W.nblk, N, K, B, Kp, epi);
   return hipGetLastError();
 }
 
@@ -607,18 +650,26 @@ hipError_t decode_oproj(const bf16_t* o, int K, const WOperand& W, float* h, int
   return gemv(StageCopy{o}, W, N, K, B, EpiAdd{h, N}, s);
 }
 
-hipError_t decode_up(const float* h, const float* g, float eps, const WOperand& W, float* gu, int B, int N, int K,
-                     hipStream_t s) {
-  return gemv(StageNorm{h, g, eps}, W, N, K, B, EpiRaw{gu, N}, s);
+hipError_t decode_up(const float* h, const float* g, float eps, const WOperand& W, int fpad, float* gu, bf16_t* a,
+                     int B, int K, hipStream_t s) {
+  const int N = 2 * fpad;
+  if (!gemv_args_ok(W, N, K, B) || fpad % 64) return hipErrorInvalidValue;
+  if (use_stream(K, B)) {
+    // SwiGLU in the product's epilogue, 16 features per workgroup
+    const int Kp = stream_kp(K);
+    if (!stream_offsets_ok(W, Kp)) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((gemv_stream_kernel<32, true, StageNorm, EpiGated>), dim3(fpad / 16), dim3(256),
+                       (size_t)B * Kp * 2, s, StageNorm{h, g, eps}, W.p, W.nblk, N, K, B, Kp, EpiGated{a, fpad});
+    return hipGetLastError();
+  }
+  hipError_t e = gemv_chunk(StageNorm{h, g, eps}, W, N, K, B, EpiRaw{gu, N}, s);
+  if (e != hipSuccess) return e;
+  const int n = B * fpad;
+  hipLaunchKernelGGL(swiglu_kernel, dim3((n + 255) / 256), dim3(256), 0, s, gu, fpad, B, a);
+  return hipGetLastError();
 }
 
-hipError_t decode_down(const float* gu, int F, int fpad, const WOperand& W, float* h, bf16_t* a, int B, int N,
-                       hipStream_t s) {
-  if (!gemv_args_ok(W, N, fpad, B)) return hipErrorInvalidValue;
-  const int n = B * fpad;
-  hipLaunchKernelGGL(swiglu_kernel, dim3((n + 255) / 256), dim3(256), 0, s, gu, F, fpad, B, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+hipError_t decode_down(const bf16_t* a, int fpad, const WOperand& W, float* h, int B, int N, hipStream_t s) {
   return gemv(StageCopy{a}, W, N, fpad, B, EpiAdd{h, N}, s);
 }
 

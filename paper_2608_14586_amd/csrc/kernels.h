@@ -102,12 +102,13 @@ hipError_t decode_attention(const float* qkv, int qkv_n, const float* rope_cos, 
                             hipStream_t s);
 // h[b] += o[b] . W^T (the O projection, o [B][K] bf16)
 hipError_t decode_oproj(const bf16_t* o, int K, const WOperand& W, float* h, int B, int N, hipStream_t s);
-hipError_t decode_up(const float* h, const float* g, float eps, const WOperand& W, float* gu, int B, int N, int K,
-                     hipStream_t s);
-// a[b] = swiglu(gu[b]) (bf16 scratch [B][fpad]); h[b] += a[b] . W^T (the
-// down projection over the padded width fpad)
-hipError_t decode_down(const float* gu, int F, int fpad, const WOperand& W, float* h, bf16_t* a, int B, int N,
-                       hipStream_t s);
+// a[b] = bf16(swiglu(RMSNorm(h[b]) g . W^T)) over the interleaved gate/up
+// rows (N = 2 fpad), the gated activation [B][fpad]; gu [B][2 fpad] fp32 is
+// scratch for inputs too wide to stage whole.
+hipError_t decode_up(const float* h, const float* g, float eps, const WOperand& W, int fpad, float* gu, bf16_t* a,
+                     int B, int K, hipStream_t s);
+// h[b] += a[b] . W^T (the down projection over the padded width fpad)
+hipError_t decode_down(const bf16_t* a, int fpad, const WOperand& W, float* h, int B, int N, hipStream_t s);
 
 // ----------------------------------------------------- norms and elementwise
 // y[M][d] = norm(x[M][d]) (fp32 in); RMSNorm when beta == NULL and !layernorm.

@@ -873,8 +873,8 @@ Status decode_step(vla_ctx* c, uint64_t frame_id, const void* x, int B, int pos,
                                                              cf.use_rope ? c->rope_sin : nullptr, kc, vc, L_cap, pos, B,
                                                              H, Hkv, dh, part, obuf, cs));
     PLAUNCH(c, VLA_STACK_LLM, VLA_K_OPROJ, vla::decode_oproj(obuf, s.hd, Stack::packed(w.w_o, d), h, B, d, cs));
-    PLAUNCH(c, VLA_STACK_LLM, VLA_K_MLP_UP, vla::decode_up(h, w.n2g, cf.norm_eps, Stack::packed(w.w_up, 2 * s.f_pad), gu, B, 2 * s.f_pad, d, cs));
-    PLAUNCH(c, VLA_STACK_LLM, VLA_K_MLP_DOWN, vla::decode_down(gu, cf.d_ff, s.f_pad, Stack::packed(w.w_down, d), h, abuf, B, d, cs));
+    PLAUNCH(c, VLA_STACK_LLM, VLA_K_MLP_UP, vla::decode_up(h, w.n2g, cf.norm_eps, Stack::packed(w.w_up, 2 * s.f_pad), s.f_pad, gu, abuf, B, d, cs));
+    PLAUNCH(c, VLA_STACK_LLM, VLA_K_MLP_DOWN, vla::decode_down(abuf, s.f_pad, Stack::packed(w.w_down, d), h, B, d, cs));
   }
   if (out->out_dtype == VLA_BF16)
     PLAUNCH(c, VLA_STACK_LLM, VLA_K_OTHER, vla::f32_to_bf16(h, (bf16_t*)sl.hid, n, cs));
