@@ -116,9 +116,13 @@ def cpu_baseline(wl, k, budget_s=20.0):
     import numpy as np
     import oracle
     import synth
+    blas = "unknown"
     try:
         from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+        info = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        threads = max([i.get("num_threads", 1) for i in info] or [1])
+        if info:
+            blas = "%s %s (%s)" % (info[0].get("internal_api"), info[0].get("version"), info[0].get("architecture"))
     except Exception:
         threads = len(os.sched_getaffinity(0))
     tok = synth.as_f32(synth.tokens(wl, frame=0))
@@ -141,7 +145,7 @@ def cpu_baseline(wl, k, budget_s=20.0):
             "sample": "%d decoder block(s) at L=%d and %d ViT block(s) over %dx%d patches, numpy fp32, "
                       "scaled to %d decoder + %d encoder blocks per frame (%.1f s per frame)"
                       % (n_llm, wl.seq, n_enc, wl.n_img, wl.img_tokens, k, wl.enc.n_blocks, per_frame),
-            "blas": "numpy %s" % np.__version__}
+            "blas": "numpy %s, %s" % (np.__version__, blas), "affinity_cores": len(os.sched_getaffinity(0))}
 
 
 def decode_bench(args):
@@ -272,6 +276,32 @@ def decode_across(args, ctx, wl, bnd, cache, xs, ob, L_cap):
          "host_prefill_ms": round(prefill_ms, 1), "steps": len(tc)}
     sfx.vla_suffix_destroy()
     return r
+
+
+def norm_large():
+    """RMSNorm over a 1 GiB fp32 input (65536 x 4096 -> bf16): a working set
+    four times the 256 MiB Infinity Cache, so the rate is HBM's, not the
+    cache's (the frame's norms read a residual the previous GEMM just wrote)."""
+    import torch
+    from paper_2608_14586_amd import binding as vb
+    M, d = 65536, 4096
+    x = torch.randn((M, d), dtype=torch.float32, device="cuda")
+    g = torch.ones(d, dtype=torch.float32, device="cuda")
+    y = torch.empty((M, d), dtype=torch.bfloat16, device="cuda")
+    st = torch.cuda.current_stream()
+    for _ in range(3):
+        vb.vla_op_norm_bf16(x, g, None, 1e-6, y, M, d, st.cuda_stream)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    n = 10
+    ev[0].record(st)
+    for _ in range(n):
+        vb.vla_op_norm_bf16(x, g, None, 1e-6, y, M, d, st.cuda_stream)
+    ev[1].record(st)
+    torch.cuda.synchronize()
+    us = ev[0].elapsed_time(ev[1]) * 1000 / n
+    nbytes = M * d * (4 + 2) + d * 4
+    return {"shape": [M, d], "avg_us": round(us, 1), "gbs": round(nbytes / us / 1e3, 1),
+            "frac": round(nbytes / us / 1e3 / PEAK_HBM_GBS, 4), "bytes": nbytes}
 
 
 def dual_bench(args):
@@ -703,7 +733,7 @@ def main():
         if profile:
             ctx.vla_profile(False)
         enc_ms.append(ev0.elapsed_time(ev1))
-        times = [ctx.vla_frame_times(f) for f in ids[-3:]]
+        times = [ctx.vla_frame_times(f) for f in ids]
         return wall * 1000.0 / n, times, enc_ms[0]
 
     results = {}
@@ -717,9 +747,15 @@ def main():
             run(k, args.steps, profile=True)
         foot = vb.vla_query_sizes(vb.stack_cfg(s, "bf16", max_tokens=L, max_batch=1, n_blocks=k), enc_cfg,
                                   1, L, k)
+        tg = np.array([t[0] for t in times])
+        tx = np.array([t[1] for t in times])
         r = {"ms_per_frame": round(ms, 3), "prefix_tokens_per_s": round(L / (ms / 1000.0), 1),
-             "t_gpu_prefix_ms": round(float(np.mean([t[0] for t in times])), 3),
-             "t_boundary_copy_ms": round(float(np.mean([t[1] for t in times])), 4),
+             "t_gpu_prefix_ms": round(float(np.mean(tg)), 3),
+             "t_gpu_prefix_ms_median": round(float(np.median(tg)), 3),
+             "t_gpu_prefix_ms_std": round(float(np.std(tg)), 3),
+             "frames_timed": len(tg),
+             "t_boundary_copy_ms": round(float(np.mean(tx)), 4),
+             "d2h_gbs": round(L * s.d_model * 2 / (float(np.mean(tx)) / 1000) / 1e9, 1),
              "t_prefix_plus_handoff_ms": round(float(np.mean([t[2] for t in times])), 3),
              "t_encoder_ms": round(enc_ms, 3),
              "frame_tflops": round(frame_flops(wl, k, images) / 1e12, 3),
@@ -779,6 +815,7 @@ def main():
         "sweep": {str(k): {kk: v for kk, v in r.items() if kk != "kernels"} for k, r in results.items()},
     }
     ctx.vla_destroy()
+    out["norm_large"] = norm_large()
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
         out["cpu_baseline"] = cpu_baseline(wl, args.k)
