@@ -27,6 +27,7 @@
 #include <thread>
 #include <vector>
 
+#include "host_pool.h"
 #include "host_suffix.h"
 
 namespace vla {
@@ -73,84 +74,6 @@ static inline __m512 exp512(__m512 x) {
   const __m512 r = _mm512_scalef_ps(p, n);
   return _mm512_maskz_mov_ps(_mm512_cmp_ps_mask(x, _mm512_set1_ps(-87.f), _CMP_GT_OQ), r);
 }
-
-// ------------------------------------------------------------------ thread pool
-
-class Pool {
- public:
-  explicit Pool(int n) : n_(std::max(1, n)) {
-    for (int i = 1; i < n_; ++i) th_.emplace_back([this] { worker(); });
-  }
-  ~Pool() {
-    {
-      std::lock_guard<std::mutex> g(mu_);
-      stop_ = true;
-      ++gen_;
-    }
-    cv_.notify_all();
-    for (auto& t : th_) t.join();
-  }
-  int size() const { return n_; }
-  // fn(i) for i in [0, n), on the pool and the calling thread; returns when all ran
-  void run(int n, const std::function<void(int)>& fn) {
-    if (n <= 0) return;
-    if (n == 1 || n_ == 1) {
-      for (int i = 0; i < n; ++i) fn(i);
-      return;
-    }
-    {
-      std::lock_guard<std::mutex> g(mu_);
-      fn_ = &fn;
-      ntask_ = n;
-      next_.store(0);
-      done_ = 0;
-      ++gen_;
-    }
-    cv_.notify_all();
-    drain();
-    std::unique_lock<std::mutex> lk(mu_);
-    done_cv_.wait(lk, [&] { return done_ == ntask_; });
-    fn_ = nullptr;
-  }
-
- private:
-  void drain() {
-    int did = 0;
-    for (;;) {
-      const int i = next_.fetch_add(1);
-      if (i >= ntask_) break;
-      (*fn_)(i);
-      ++did;
-    }
-    if (did) {
-      std::lock_guard<std::mutex> g(mu_);
-      done_ += did;
-      if (done_ == ntask_) done_cv_.notify_all();
-    }
-  }
-  void worker() {
-    uint64_t seen = 0;
-    for (;;) {
-      {
-        std::unique_lock<std::mutex> lk(mu_);
-        cv_.wait(lk, [&] { return gen_ != seen; });
-        seen = gen_;
-        if (stop_) return;
-        if (!fn_) continue;
-      }
-      drain();
-    }
-  }
-  int n_;
-  std::vector<std::thread> th_;
-  std::mutex mu_;
-  std::condition_variable cv_, done_cv_;
-  const std::function<void(int)>* fn_ = nullptr;
-  std::atomic<int> next_{0};
-  int ntask_ = 0, done_ = 0;
-  uint64_t gen_ = 0;
-  bool stop_ = false;
-};
 
 // ------------------------------------------------------------------ packed operand
 //
