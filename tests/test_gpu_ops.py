@@ -17,7 +17,8 @@ def _dev_bf16(a_u16):
 
 
 @pytest.mark.parametrize("M,N,K", [(128, 128, 64), (200, 320, 128), (77, 96, 256), (1024, 1152, 896),
-                                   (33, 4096, 4096), (2048, 16384, 128), (2000, 16400, 192)])
+                                   (33, 4096, 4096), (2048, 16384, 128), (2000, 16400, 192),
+                                   (6104, 1000, 192)])
 def test_gemm_bf16(M, N, K):
     import torch
     from paper_2608_14586_amd import binding as vb
