@@ -55,16 +55,17 @@ __device__ __forceinline__ f32x4 ld4(const float* p) { return *(const f32x4*)p; 
 // Exact GELU z * Phi(z) with Phi(z) = erfc(-z / sqrt 2) / 2, erfc from the
 // rational approximation of Abramowitz & Stegun 7.1.26 (|error| <= 1.5e-7,
 // far below bf16 resolution); erfc of |x| is formed directly, so the negative
-// tail does not cancel.  The one division is the hardware reciprocal (1 ulp):
-// an IEEE divide would cost ten VALU instructions per element of a
-// [M][d_ff] epilogue that no MFMA work overlaps.
+// tail does not cancel.  Arithmetic folded for the epilogue, which no MFMA
+// work overlaps: t = 1 / (1 + p |z| / sqrt 2) is one FMA and the hardware
+// reciprocal (1 ulp; an IEEE divide costs ten VALU instructions), the 1/2 of
+// Phi sits in the polynomial's coefficients, and e^(-z^2 / 2) is one exp2.
 __device__ __forceinline__ float gelu_as(float z) {
-  const float x = fabsf(z) * 0.70710678118654752f;
-  const float t = __builtin_amdgcn_rcpf(1.f + 0.3275911f * x);
-  const float poly = t * (0.254829592f + t * (-0.284496736f + t * (1.421413741f + t * (-1.453152027f + t * 1.061405429f))));
-  const float ec = poly * __expf(-x * x);  // erfc(x), x >= 0
-  const float phi = z >= 0.f ? 1.f - 0.5f * ec : 0.5f * ec;
-  return z * phi;
+  const float t = __builtin_amdgcn_rcpf(fmaf(fabsf(z), 0.3275911f * 0.70710678118654752f, 1.f));
+  // (a1 t + a2 t^2 + ... + a5 t^5) / 2
+  const float hp =
+      t * (0.127414796f + t * (-0.142248368f + t * (0.7107068705f + t * (-0.7265760135f + t * 0.5307027145f))));
+  const float h = hp * __builtin_amdgcn_exp2f(z * (z * -0.72134752044448170f));  // erfc(|z| / sqrt 2) / 2
+  return z * (z >= 0.f ? 1.f - h : h);
 }
 
 // largest divisor of n that is at most 16
@@ -74,7 +75,11 @@ constexpr int batch_of(int n) {
   return b;
 }
 
-__device__ __forceinline__ float silu(float g) { return g / (1.f + __expf(-g)); }
+// silu(g) = g / (1 + e^-g), the division by the hardware reciprocal (1 ulp),
+// as in the GELU: an IEEE divide costs ten VALU instructions per element of
+// an epilogue that no MFMA work overlaps.  Large negative g: e^-g overflows
+// to inf, whose reciprocal is 0, so the result is -0 as with the divide.
+__device__ __forceinline__ float silu(float g) { return g * __builtin_amdgcn_rcpf(1.f + __expf(-g)); }
 
 struct EpiStoreF32 {
   static constexpr bool kViaLds = false, kBig = true;
@@ -127,15 +132,21 @@ struct EpiBF16 {
   template <int R, int NC>
   __device__ void drain(const float* T, int m0, int n0, int tid) const {
     constexpr int CH = NC / 8;  // 16-byte output chunks per row
-    static_assert((R * CH) % 256 == 0, "tile must split evenly over the workgroup");
+    static_assert((R * CH) % 256 == 0 && 256 % CH == 0, "tile must split evenly over the workgroup");
+    // a thread's columns are the same in every chunk it drains
+    const int c8 = (tid % CH) * 8, gc = n0 + c8;
+    if (gc >= N) return;
+    f32x4 b0 = {0.f, 0.f, 0.f, 0.f}, b1 = b0;
+    if (bias) {
+      b0 = ld4(bias + gc);
+      b1 = ld4(bias + gc + 4);
+    }
 #pragma unroll 4
     for (int j = 0; j < R * CH / 256; ++j) {
-      const int f = tid + 256 * j, row = f / CH, c8 = (f % CH) * 8;
-      const int gr = m0 + row, gc = n0 + c8;
-      if (gr >= M || gc >= N) continue;
+      const int row = (tid + 256 * j) / CH, gr = m0 + row;
+      if (gr >= M) continue;
       f32x4 x0 = ld4(T + row * NC + c8), x1 = ld4(T + row * NC + c8 + 4);
       if (bias) {
-        f32x4 b0 = ld4(bias + gc), b1 = ld4(bias + gc + 4);
         x0 += b0;
         x1 += b1;
       }
