@@ -47,14 +47,24 @@ constexpr int ATT_KC = 128;        // keys per attention split
 __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
-// 8 bf16 products accumulated in fp32 (plain FMAs: the loop is bound by the
-// weight stream, not by VALU issue)
+// acc + sum of the 8 products of bf16 pairs, two per v_dot2_f32_bf16: the
+// bf16 operands go in as they are (no conversion to fp32) and every product
+// is exact in fp32.  With several sequences each weight feeds several
+// products, and converting both operands per product made the step VALU-bound.
+// The pairs are taken by shuffling the 8-lane bf16 view of each operand:
+// bit-casting the 32-bit words w[i] one by one instead compiled to a loop
+// that read word 0 four times.
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 __device__ __forceinline__ float dot8(const u32x4& w, const u32x4& x, float acc) {
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    acc = fmaf(bf_lo(w[i]), bf_lo(x[i]), acc);
-    acc = fmaf(bf_hi(w[i]), bf_hi(x[i]), acc);
-  }
+  const bf16x8_t a = __builtin_bit_cast(bf16x8_t, w), b = __builtin_bit_cast(bf16x8_t, x);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 0, 1), __builtin_shufflevector(b, b, 0, 1), acc,
+                                        false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 2, 3), __builtin_shufflevector(b, b, 2, 3), acc,
+                                        false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 4, 5), __builtin_shufflevector(b, b, 4, 5), acc,
+                                        false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 6, 7), __builtin_shufflevector(b, b, 6, 7), acc,
+                                        false);
   return acc;
 }
 
