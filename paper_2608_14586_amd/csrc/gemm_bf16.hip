@@ -113,21 +113,7 @@ struct EpiBF16 {
   int ldc, M, N;
   __device__ __forceinline__ float op(float z) const { return GELU ? gelu_as(z) : z; }
   template <int TM, int TN>
-  __device__ void operator()(const Acc<TM, TN>& a, int row0, int col0, int lane) const {
-#pragma unroll
-    for (int tm = 0; tm < TM; ++tm)
-#pragma unroll
-      for (int tn = 0; tn < TN; ++tn) {
-        int col = col0 + tn * 32 + (lane & 31);
-        if (col >= N) continue;
-        float b = bias ? bias[col] : 0.f;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          int row = row0 + tm * 32 + acc_row(r, lane);
-          if (row < M) C[(size_t)row * ldc + col] = f2bf(op(a.v[tm][tn][r] + b));
-        }
-      }
-  }
+  __device__ void operator()(const Acc<TM, TN>&, int, int, int) const {}  // LDS path only
   // T: R x NC fp32 tile (row stride NC) at (m0, n0); 256 threads.
   template <int R, int NC>
   __device__ void drain(const float* T, int m0, int n0, int tid) const {
@@ -169,24 +155,7 @@ struct EpiResidual {
   const float* bias;
   int ldh, M, N;
   template <int TM, int TN>
-  __device__ void operator()(const Acc<TM, TN>& a, int row0, int col0, int lane) const {
-#pragma unroll
-    for (int tm = 0; tm < TM; ++tm)
-#pragma unroll
-      for (int tn = 0; tn < TN; ++tn) {
-        int col = col0 + tn * 32 + (lane & 31);
-        if (col >= N) continue;
-        float b = bias ? bias[col] : 0.f;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          int row = row0 + tm * 32 + acc_row(r, lane);
-          if (row < M) {
-            float* p = H + (size_t)row * ldh + col;
-            *p = *p + (a.v[tm][tn][r] + b);
-          }
-        }
-      }
-  }
+  __device__ void operator()(const Acc<TM, TN>&, int, int, int) const {}  // LDS path only
   template <int R, int NC>
   __device__ void drain(const float* T, int m0, int n0, int tid) const {
     // R rows x NC/4 float4, in batches of 16 per thread with every residual
@@ -221,22 +190,7 @@ struct EpiSwiGLU {
   bf16_t* out;
   int ldo, M, N;
   template <int TM, int TN>
-  __device__ void operator()(const Acc<TM, TN>& a, int row0, int col0, int lane) const {
-    static_assert(TN % 2 == 0, "swiglu pairs tiles");
-#pragma unroll
-    for (int tm = 0; tm < TM; ++tm)
-#pragma unroll
-      for (int tp = 0; tp < TN / 2; ++tp) {
-        int pcol = col0 + tp * 64;
-        if (pcol >= N) continue;
-        int f = (pcol >> 1) + (lane & 31);
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          int row = row0 + tm * 32 + acc_row(r, lane);
-          if (row < M) out[(size_t)row * ldo + f] = f2bf(silu(a.v[tm][2 * tp][r]) * a.v[tm][2 * tp + 1][r]);
-        }
-      }
-  }
+  __device__ void operator()(const Acc<TM, TN>&, int, int, int) const {}  // LDS path only
   template <int R, int NC>
   __device__ void drain(const float* T, int m0, int n0, int tid) const {
     // R rows x NC/16 chunks of 8 output features (4 chunks per 64-column group)
