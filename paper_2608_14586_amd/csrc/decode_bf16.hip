@@ -77,20 +77,36 @@ struct StageNorm {
   const float* h;
   const float* g;
   float eps;
+  // sc[b] = 1 / rms(h[b]) for the B rows at once: every row's 16-byte loads
+  // are issued before any sum, and one pair of barriers serves all rows
+  // (red: 4 x GV_MB floats)
   __device__ void prepare(float* sc, int B, int K, int tid, float* red) const {
-    for (int b = 0; b < B; ++b) {
-      float s = 0.f;
-      for (int i = tid; i < K; i += 256) {
-        const float v = h[(size_t)b * K + i];
-        s += v * v;
-      }
+    float s[GV_MB] = {0.f, 0.f, 0.f, 0.f};
+    const int K4 = (K % 4 == 0) ? K : 0;  // rows 16-byte aligned
+    for (int i = tid * 4; i < K4; i += 256 * 4) {
+      f32x4 v[GV_MB];
 #pragma unroll
-      for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
-      if ((tid & 63) == 0) red[tid >> 6] = s;
-      __syncthreads();
-      if (tid == 0) sc[b] = 1.f / sqrtf((red[0] + red[1] + red[2] + red[3]) / (float)K + eps);
-      __syncthreads();
+      for (int b = 0; b < GV_MB; ++b)
+        if (b < B) v[b] = *(const f32x4*)(h + (size_t)b * K + i);
+#pragma unroll
+      for (int b = 0; b < GV_MB; ++b)
+        if (b < B) s[b] += v[b][0] * v[b][0] + v[b][1] * v[b][1] + v[b][2] * v[b][2] + v[b][3] * v[b][3];
     }
+    for (int i = K4 + tid; i < K; i += 256)
+#pragma unroll
+      for (int b = 0; b < GV_MB; ++b)
+        if (b < B) s[b] += h[(size_t)b * K + i] * h[(size_t)b * K + i];
+#pragma unroll
+    for (int b = 0; b < GV_MB; ++b) {
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) s[b] += __shfl_xor(s[b], o);
+      if ((tid & 63) == 0) red[(tid >> 6) * GV_MB + b] = s[b];
+    }
+    __syncthreads();
+    if (tid < B)
+      sc[tid] = 1.f / sqrtf((red[tid] + red[GV_MB + tid] + red[2 * GV_MB + tid] + red[3 * GV_MB + tid]) / (float)K +
+                            eps);
+    __syncthreads();
   }
   __device__ void fill(bf16_t* xs, const float* sc, int B, int K, int k0, int n, int tid) const {
     for (int b = 0; b < B; ++b)
@@ -167,7 +183,7 @@ __global__ __launch_bounds__(256) void gemv_chunk_kernel(Stage sg, const bf16_t*
   __shared__ __attribute__((aligned(16))) bf16_t xs[GV_MB * GV_KCH];
   __shared__ float red[4 * GV_ROWS * GV_MB];
   __shared__ float sc[GV_MB];
-  __shared__ float tmp[4];
+  __shared__ float tmp[4 * GV_MB];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n0 = blockIdx.x * GV_ROWS;
   const int r8 = lane >> 3, c8 = lane & 7;
@@ -270,7 +286,7 @@ __global__ __launch_bounds__(256) void gemv_stream_kernel(Stage sg, const bf16_t
   extern __shared__ __attribute__((aligned(16))) bf16_t xs[];
   __shared__ float red[4 * ROWS * GV_MB];
   __shared__ float sc[GV_MB];
-  __shared__ float tmp[4];
+  __shared__ float tmp[4 * GV_MB];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r8 = lane >> 3, c8 = lane & 7;
   // this lane's rows: block blk, rows rb + roff(j) inside it (all in one 128-row block)
