@@ -396,7 +396,17 @@ __global__ __launch_bounds__(256) void gemv_stream_kernel(Stage sg, const bf16_t
 
 // the streaming kernel's input rows: B * Kp bf16 in LDS
 inline int stream_kp(int K) { return (K + GS_KC * GS_D - 1) / (GS_KC * GS_D) * (GS_KC * GS_D); }
-inline bool use_stream(int K, int B) { return K >= GS_KC && (size_t)B * stream_kp(K) * 2 <= 48 * 1024; }
+// up to 48 KB the kernel runs several workgroups per CU; up to 96 KB (four
+// d_ff-wide rows) one, and the grid then takes 16-row workgroups once 256 of
+// them fill the CUs
+constexpr size_t GS_LDS_SHARED = 48 * 1024, GS_LDS_MAX = 96 * 1024;
+inline bool use_stream(int K, int B) { return K >= GS_KC && (size_t)B * stream_kp(K) * 2 <= GS_LDS_MAX; }
+// dynamic LDS above the 64 KB default needs the kernel's attribute raised
+template <class F>
+hipError_t allow_lds(F* kernel, size_t bytes) {
+  if (bytes <= 64 * 1024) return hipSuccess;
+  return hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+}
 // the buffer resource's size and the offsets (up to 16 slabs past Kp) fit in 31 bits
 inline bool stream_offsets_ok(const WOperand& W, int Kp) {
   return (size_t)(Kp / 64 + 16) * W.nblk * SLAB_N * 64 * 2 < (1ull << 31);
@@ -407,12 +417,17 @@ hipError_t gemv_stream(const Stage& sg, const WOperand& W, int N, int K, int B, 
   const int Kp = stream_kp(K);
   const size_t lds = (size_t)B * Kp * 2;
   if (!stream_offsets_ok(W, Kp)) return hipErrorInvalidValue;
-  if ((N + 15) / 16 >= 512)
+  if ((N + 15) / 16 >= (lds > GS_LDS_SHARED ? 256 : 512)) {
+    hipError_t e = allow_lds(gemv_stream_kernel<16, false, Stage, Epi>, lds);
+    if (e != hipSuccess) return e;
     hipLaunchKernelGGL((gemv_stream_kernel<16, false, Stage, Epi>), dim3((N + 15) / 16), dim3(256), lds, s, sg, W.p,
                        W.nblk, N, K, B, Kp, epi);
-  else
+  } else {
+    hipError_t e = allow_lds(gemv_stream_kernel<8, false, Stage, Epi>, lds);
+    if (e != hipSuccess) return e;
     hipLaunchKernelGGL((gemv_stream_kernel<8, false, Stage, Epi>), dim3((N + 7) / 8), dim3(256), lds, s, sg, W.p,
                        W.nblk, N, K, B, Kp, epi);
+  }
   return hipGetLastError();
 }
 
@@ -684,6 +699,8 @@ hipError_t decode_up(const float* h, const float* g, float eps, const WOperand& 
     // SwiGLU in the product's epilogue, 16 features per workgroup
     const int Kp = stream_kp(K);
     if (!stream_offsets_ok(W, Kp)) return hipErrorInvalidValue;
+    hipError_t e = allow_lds(gemv_stream_kernel<32, true, StageNorm, EpiGated>, (size_t)B * Kp * 2);
+    if (e != hipSuccess) return e;
     hipLaunchKernelGGL((gemv_stream_kernel<32, true, StageNorm, EpiGated>), dim3(fpad / 16), dim3(256),
                        (size_t)B * Kp * 2, s, StageNorm{h, g, eps}, W.p, W.nblk, N, K, B, Kp, EpiGated{a, fpad});
     return hipGetLastError();

@@ -56,6 +56,9 @@ def _oracle_rows(wl, W, toks, L, steps, k):
     # rows staged whole in LDS), with three and four sequences
     ("dec_stream4", llama_like(2, 1024, 8, 2, 128, 2816), 4, 100, 2),
     ("dec_stream3", llama_like(1, 1024, 16, 4, 64, 2816), 3, 257, 1),
+    # d_ff = 11008 with four sequences: the down product stages 96 KB of input
+    # rows (one workgroup per CU)
+    ("dec_stream_big", llama_like(1, 512, 8, 2, 64, 11008), 4, 60, 1),
 ])
 def test_decode_steps_match_oracle(name, shape, B, L, k):
     steps = 3
