@@ -324,7 +324,9 @@ def dual_bench(args):
     assert all(0 <= k <= N for k in ks)
     lcfg = vb.stack_cfg(s, "bf16", max_tokens=L, max_batch=1, n_blocks=N)
     ctx = [vb.Context(llm=lcfg, enc=vb.stack_cfg(e, "bf16", max_tokens=vis.L_img, max_batch=n_img))]
-    ctx.append(vb.Context(llm=lcfg, compute_stream=ctx[0].compute_stream))
+    # the second stack on compute and copy streams of its own: the two
+    # stacks' small GEMMs overlap instead of queueing behind each other
+    ctx.append(vb.Context(llm=lcfg))
     t0 = time.time()
     for l in range(e.n_blocks):
         ctx[0].vla_load_block_weights(vb.VLA_STACK_ENC, l, synth.vit_block_weights(wl, l))
@@ -337,7 +339,10 @@ def dual_bench(args):
     dev = torch.device("cuda:0")
     imgs = [torch.from_numpy(synth.images(wl, frame=f).view(np.int16)).to(dev) for f in range(2)]
     texts = [torch.from_numpy(synth.text(wl, frame=f).view(np.int16)).to(dev) for f in range(2)]
-    tok = torch.empty((L, s.d_model), dtype=torch.bfloat16, device=dev)
+    # token rows rotate over three buffers: the vision of frame f + 3 waits for
+    # the second stack's read of frame f (with its handoff behind it)
+    NTOK = 3
+    toks = [torch.empty((L, s.d_model), dtype=torch.bfloat16, device=dev) for _ in range(NTOK)]
     torch.cuda.synchronize()
     log("dual stack resident (%.0fs)" % (time.time() - t0))
     fid = [1]
@@ -351,16 +356,26 @@ def dual_bench(args):
             ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
             torch.cuda.synchronize()
             t = time.perf_counter()
+            read_done = [None] * NTOK
             for i in range(n):
                 f = fid[0]
                 fid[0] += 1
+                tok = toks[i % NTOK]
+                if read_done[i % NTOK] is not None:
+                    ctx[0].compute_stream.wait_event(read_done[i % NTOK])
                 if i == 0:
                     ev[0].record(ctx[0].compute_stream)
                 ctx[0].vla_run_vision(f, imgs[i % 2], n_img, texts[i % 2], T, tok)
+                ready = torch.cuda.Event()
+                ready.record(ctx[0].compute_stream)
                 if i == 0:
                     ev[1].record(ctx[0].compute_stream)
+                ctx[1].compute_stream.wait_event(ready)
                 for j in range(2):
                     ctx[j].vla_run_prefix(f, tok, 1, L, k, bnds[j][i % 3])
+                done = torch.cuda.Event()
+                done.record(ctx[1].compute_stream)
+                read_done[i % NTOK] = done
                 ids.append((f, i % 3))
             for f, _ in ids[-3:]:
                 for j in range(2):

@@ -163,6 +163,61 @@ def test_dual_stack_over_one_frame():
     assert rel_l2(outs[(2, 0)][2].hidden.numpy(), outs[(2, 1)][2].hidden.numpy()) > 1e-2
 
 
+def test_dual_stacks_on_two_streams_match_one_stream():
+    # the two stacks on compute streams of their own, overlapping: the second
+    # stream waits for each frame's vision output by an event, the token rows
+    # alternate between two buffers, and the vision of frame f + 2 waits for
+    # the second stack's read of frame f.  Every boundary equals that of the
+    # same contexts run one step at a time, bit for bit.
+    import torch
+    llm = llama_like(2, 128, 2, 1, 64, 320)
+    vis = VisionShape(3, 56, 56, 14, 2, 128, 128)
+    c = VisionCase("vis_dual2", "bf16", SMALL_ENC, vis, 2, 5, llm=llm, k=2)
+    wl2 = Workload("vis_dual2_b", "bf16", llm, None)
+    ctx2 = vb.Context(llm=vb.stack_cfg(llm, "bf16", max_tokens=c.L, max_batch=1, n_blocks=2))  # own streams
+    for l in range(2):
+        ctx2.vla_load_block_weights(vb.VLA_STACK_LLM, l, synth.llm_block_weights(wl2, l, perturbed=True))
+    ctxs, frames = (c.ctx, ctx2), range(4)
+    new_bnd = lambda: vb.Boundary(1, c.L, llm.d_model, 2, llm.n_kv_heads, llm.head_dim, out_dtype="f32")
+
+    ref = {}
+    tok = torch.empty((c.L, vis.d_out), dtype=torch.bfloat16, device="cuda")
+    for f in frames:
+        images, text = c.inputs(f)
+        c.ctx.vla_run_vision(100 + f, images, c.n_img, text, c.T, tok)
+        for j, ctx in enumerate(ctxs):
+            b = new_bnd()
+            ctx.vla_run_prefix(100 + f, tok, 1, c.L, 2, b)
+            ctx.vla_wait_boundary(100 + f, 60000)
+            torch.cuda.synchronize()
+            ref[(f, j)] = b.hidden.numpy().copy()
+
+    toks = [torch.empty_like(tok) for _ in range(2)]
+    read_done = [None, None]
+    got = []
+    for f in frames:
+        images, text = c.inputs(f)
+        t = toks[f % 2]
+        if read_done[f % 2] is not None:
+            c.ctx.compute_stream.wait_event(read_done[f % 2])
+        c.ctx.vla_run_vision(200 + f, images, c.n_img, text, c.T, t)
+        ready = torch.cuda.Event()
+        ready.record(c.ctx.compute_stream)
+        ctx2.compute_stream.wait_event(ready)
+        for j, ctx in enumerate(ctxs):
+            b = new_bnd()
+            ctx.vla_run_prefix(200 + f, t, 1, c.L, 2, b)
+            got.append((f, j, ctx, b))
+        done = torch.cuda.Event()
+        done.record(ctx2.compute_stream)
+        read_done[f % 2] = done
+    for f, j, ctx, b in got:
+        ctx.vla_wait_boundary(200 + f, 60000)
+    torch.cuda.synchronize()
+    for f, j, ctx, b in got:
+        assert np.array_equal(b.hidden.numpy(), ref[(f, j)]), (f, j)
+
+
 def test_vision_rejects_bad_calls():
     import torch
     vis = VisionShape(3, 56, 56, 14, 2, 128, 128)
