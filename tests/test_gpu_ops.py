@@ -18,7 +18,7 @@ def _dev_bf16(a_u16):
 
 @pytest.mark.parametrize("M,N,K", [(128, 128, 64), (200, 320, 128), (77, 96, 256), (1024, 1152, 896),
                                    (33, 4096, 4096), (2048, 16384, 128), (2000, 16400, 192),
-                                   (6104, 1000, 192)])
+                                   (6104, 1000, 192), (1, 1, 64), (1, 8, 128), (3, 200, 64)])
 def test_gemm_bf16(M, N, K):
     import torch
     from paper_2608_14586_amd import binding as vb
@@ -34,7 +34,9 @@ def test_gemm_bf16(M, N, K):
 
 @pytest.mark.parametrize("B,H,Hkv,L,dh,causal", [
     (1, 4, 4, 128, 128, True), (1, 4, 4, 200, 128, True), (2, 6, 2, 77, 64, True), (1, 14, 2, 300, 64, True),
-    (3, 4, 4, 130, 64, False), (1, 2, 2, 1024, 64, False), (1, 2, 1, 513, 128, False)])
+    (3, 4, 4, 130, 64, False), (1, 2, 2, 1024, 64, False), (1, 2, 1, 513, 128, False),
+    # degenerate lengths: one token, less than one 16-key group, exactly one key tile
+    (1, 2, 2, 1, 64, True), (1, 2, 1, 1, 128, False), (2, 4, 2, 15, 64, True), (1, 2, 2, 64, 128, True)])
 def test_attention_bf16(B, H, Hkv, L, dh, causal):
     import torch
     from paper_2608_14586_amd import binding as vb
@@ -62,7 +64,7 @@ def test_attention_bf16(B, H, Hkv, L, dh, causal):
 
 
 @pytest.mark.parametrize("M,d,ln", [(5, 256, False), (300, 896, False), (64, 4096, False), (70, 1024, True),
-                                    (9, 4096, True)])
+                                    (9, 4096, True), (1, 4, False), (1, 4, True), (3, 36, True)])
 def test_norms_bf16(M, d, ln):
     import torch
     from paper_2608_14586_amd import binding as vb
