@@ -115,7 +115,10 @@ typedef struct {
 } vla_boundary;
 
 /* Device arena bytes a context needs for these stacks (enc may be NULL), and
- * the hidden / KV handoff sizes of a run of k blocks at batch B, length L. */
+ * the hidden / KV handoff sizes of a run of k blocks at batch B, length L:
+ * hidden_bytes = S_hid = B * L * D * b of Eq. (11) (b the stack dtype's
+ * element bytes), kv_bytes = k * 2 * B * n_kv_heads * L * head_dim * b.
+ * Negative B, L or k: VLA_ERR_INVALID_ARG; nothing is allocated. */
 vla_status vla_query_sizes(const vla_stack_cfg *llm, const vla_stack_cfg *enc, int B, int L, int k,
                            size_t *arena_bytes, size_t *hidden_bytes, size_t *kv_bytes);
 
@@ -245,8 +248,12 @@ vla_status vla_run_blocks(vla_ctx *ctx, uint64_t frame_id, const void *tokens, v
 vla_status vla_decode_step(vla_ctx *ctx, uint64_t frame_id, const void *x, int B, int pos, int k, void *kv_cache,
                            int L_cap, vla_boundary *out);
 
-/* Block the host until frame_id's handoff is complete (its host buffers are
- * then readable), or timeout_ms elapses (< 0: wait forever). */
+/* The consumer side of the producer-consumer handoff (Sec. IV-C): block the
+ * host until frame_id's handoff is complete (its host buffers are then
+ * readable), or timeout_ms elapses (< 0: wait forever).  VLA_ERR_TIMEOUT
+ * leaves the frame in flight, so a later wait can still collect it;
+ * VLA_ERR_UNKNOWN_FRAME for an id neither in flight nor among the last 256
+ * finished frames. */
 vla_status vla_wait_boundary(vla_ctx *ctx, uint64_t frame_id, int timeout_ms);
 
 /* Stage times of a completed frame (Eq. (8)-(9)): t_gpu_ms from the start of
@@ -278,6 +285,34 @@ vla_status vla_profile(vla_ctx *ctx, int enable);
 /* Totals since vla_profile(ctx, 1) for one stack and class: summed kernel
  * time in ms and launch count.  Synchronises the compute and encoder streams. */
 vla_status vla_profile_read(vla_ctx *ctx, vla_stack which, vla_kernel_class cls, double *ms_total, int *launches);
+
+/*
+ * Precision of the activation operands of a bf16 decoder stack's QKV,
+ * gate/up and down products.  Sec. IV-B rests the partitioned model's
+ * fidelity on computing the same blocks (Eq. (5)-(6)); with bf16 operands
+ * every product input is rounded to 8 significant bits, and with random-init
+ * d=4096 blocks that rounding alone moves the boundary h^(k) away from an
+ * fp32 computation by more than 1e-2 (relative L2) beyond about 8 blocks.
+ *  VLA_PREC_BF16   (default) each operand is one bf16 value.
+ *  VLA_PREC_SPLIT  the RMSNorm outputs and the gated activation are carried
+ *                  as hi = bf16(v) and lo = bf16(v - hi), and each product
+ *                  is hi W^T + lo W^T accumulated in fp32: a 16-bit
+ *                  significand in place of 8, for twice the MFMA work of
+ *                  those three products.  Weights, the attention path, the
+ *                  KV cache and the boundary are unchanged.
+ * Applies to runs enqueued after the call.  VLA_ERR_UNSUPPORTED for encoder
+ * stacks and fp32 stacks (the fp32 debug path has no reduced precision).
+ */
+typedef enum { VLA_PREC_BF16 = 0, VLA_PREC_SPLIT = 1 } vla_precision;
+vla_status vla_set_precision(vla_ctx *ctx, vla_stack which, vla_precision prec);
+
+/* Fault injection for the error paths (tests and harnesses): after
+ * `launches` further kernel launches have been enqueued, the next launch is
+ * not made and its call fails with VLA_ERR_HIP as a failing launch would;
+ * launches < 0 switches it off.  The failure takes the frame's work as far
+ * as it was enqueued, waits for it, and forgets the frame id: every kernel
+ * still runs to completion and later frames run normally. */
+vla_status vla_inject_fault(vla_ctx *ctx, long launches);
 
 /* Bytes of the arena in use after the loads so far (weights + workspace). */
 vla_status vla_arena_used(const vla_ctx *ctx, size_t *bytes);

@@ -24,6 +24,7 @@ STATUS = {0: "VLA_OK", -1: "VLA_ERR_INVALID_ARG", -2: "VLA_ERR_SHAPE", -3: "VLA_
           -8: "VLA_ERR_UNSUPPORTED", -9: "VLA_ERR_UNKNOWN_FRAME"}
 VLA_BF16, VLA_F32 = 0, 1
 VLA_STACK_LLM, VLA_STACK_ENC = 0, 1
+VLA_PREC_BF16, VLA_PREC_SPLIT = 0, 1
 KERNEL_CLASSES = ["norm", "qkv", "attn", "oproj", "mlp_up", "mlp_down", "other", "stem", "connector"]
 
 
@@ -97,6 +98,8 @@ def lib():
             "vla_wait_boundary": [c_void_p, c_uint64, c_int],
             "vla_frame_times": [c_void_p, c_uint64, P(c_float), P(c_float), P(c_float)],
             "vla_arena_used": [c_void_p, P(c_size_t)],
+            "vla_set_precision": [c_void_p, c_int, c_int],
+            "vla_inject_fault": [c_void_p, ctypes.c_long],
             "vla_op_gemm_bf16": [c_void_p, c_void_p, c_void_p, c_int, c_int, c_int, c_void_p],
             "vla_op_attention_bf16": [c_void_p, c_void_p, c_void_p, c_int, c_void_p, c_int, c_int, c_int, c_int,
                                       c_int, c_int, c_void_p],
@@ -307,6 +310,12 @@ class Context:
         g, x, t = c_float(), c_float(), c_float()
         _check(lib().vla_frame_times(self.h, frame_id, ctypes.byref(g), ctypes.byref(x), ctypes.byref(t)), self.h)
         return g.value, x.value, t.value
+
+    def vla_set_precision(self, which: int, prec: int):
+        _check(lib().vla_set_precision(self.h, which, prec), self.h)
+
+    def vla_inject_fault(self, launches: int):
+        _check(lib().vla_inject_fault(self.h, launches), self.h)
 
     def vla_arena_used(self) -> int:
         n = c_size_t()

@@ -512,8 +512,11 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const float* __restric
   // rounds of 32 keys (8 per wave, 8 lanes per key); every key of this
   // lane's rounds is loaded before any is used -- one round trip to memory,
   // not one per round.  Keys past the split's end load its last key (in
-  // bounds) and are masked; the token's own key and value come from LDS,
-  // since the workgroup appending them to the cache may not have run yet.
+  // bounds) and are masked.  In the split holding pos, every lane whose key
+  // index is pos or beyond takes the token's own key and value from LDS: the
+  // workgroup appending them to the cache may not have run yet, and the
+  // masked lanes' weight of zero must multiply a finite value (the cache
+  // rows from pos on may hold anything, NaN included).
   constexpr int R = ATT_KC / 32, C = DL / 8;
   const int kbeg = split * ATT_KC, kend = min(pos + 1, kbeg + ATT_KC);
   const bf16_t* kb = kc + ((size_t)b * Hkv + hk) * L_cap * DH;
@@ -533,7 +536,7 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const float* __restric
 #pragma unroll
   for (int r = 0; r < R; ++r) {
     const int j = kbeg + r * 32 + wave * 8 + g;
-    if (last && j == pos) {
+    if (last && j >= pos) {
 #pragma unroll
       for (int c = 0; c < C; ++c) {
         kw[r][c] = *(const u32x4*)(knew + i8 * DL + c * 8);

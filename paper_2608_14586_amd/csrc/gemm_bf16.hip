@@ -52,6 +52,12 @@ __device__ __forceinline__ u32x4 pack8(const f32x4& a, const f32x4& b) {
 
 __device__ __forceinline__ f32x4 ld4(const float* p) { return *(const f32x4*)p; }
 
+// the four bf16 values of words (w, w+1) of a packed chunk, widened
+__device__ __forceinline__ f32x4 unpack_lo4(const u32x4& v, int w) {
+  return f32x4{__uint_as_float(v[w] << 16), __uint_as_float(v[w] & 0xFFFF0000u), __uint_as_float(v[w + 1] << 16),
+               __uint_as_float(v[w + 1] & 0xFFFF0000u)};
+}
+
 // Exact GELU z * Phi(z) with Phi(z) = erfc(-z / sqrt 2) / 2, erfc from the
 // rational approximation of Abramowitz & Stegun 7.1.26 (|error| <= 1.5e-7,
 // far below bf16 resolution); erfc of |x| is formed directly, so the negative
@@ -185,10 +191,13 @@ struct EpiResidual {
 };
 
 // Pairs tiles (2p, 2p+1) = (gate, up) of the same 32 features: out[M][N/2].
+// lo > 0: the activation is also written as its bf16 remainder
+// bf16(y - bf16(y)) at column lo + c, so that hi + lo carries y to 16
+// significant bits into the down projection.
 struct EpiSwiGLU {
   static constexpr bool kViaLds = true, kBig = true;
   bf16_t* out;
-  int ldo, M, N;
+  int ldo, M, N, lo;
   template <int TM, int TN>
   __device__ void operator()(const Acc<TM, TN>&, int, int, int) const {}  // LDS path only
   template <int R, int NC>
@@ -210,7 +219,10 @@ struct EpiSwiGLU {
         y0[e] = silu(g0[e]) * u0[e];
         y1[e] = silu(g1[e]) * u1[e];
       }
-      *(u32x4*)(out + (size_t)gr * ldo + (n0 >> 1) + gsel * 32 + w) = pack8(y0, y1);
+      bf16_t* dst = out + (size_t)gr * ldo + (n0 >> 1) + gsel * 32 + w;
+      const u32x4 hi = pack8(y0, y1);
+      *(u32x4*)dst = hi;
+      if (lo) *(u32x4*)(dst + lo) = pack8(y0 - unpack_lo4(hi, 0), y1 - unpack_lo4(hi, 2));
     }
   }
 };
@@ -329,9 +341,13 @@ __device__ __forceinline__ void buffer_load_lds16(__amdgpu_buffer_rsrc_t r, void
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, voff, 0, 0, 0);
 }
 
+// K is the k extent of A, Kw that of W (K = Kw or 2 Kw): A's column blocks
+// [0, Kw) and [Kw, 2 Kw) multiply the same W, so an operand carried as
+// a hi + lo pair of bf16 values side by side ([M][2 Kw]) yields
+// hi * W^T + lo * W^T in one accumulator.
 template <int BM, int BN, int WM, int WN, int NW, bool WT, class Epi>
 __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __restrict__ A, int lda, WOperand W,
-                                                                int M, int N, int K, Epi epi) {
+                                                                int M, int N, int K, int Kw, Epi epi) {
   constexpr int TM = WM / 32, TN = WN / 32;
   constexpr int WAVES_N = BN / WN;
   static_assert((BM / WM) * (BN / WN) == NW, "wave grid must cover the tile");
@@ -361,7 +377,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __
   // a tile lies inside it: the packing pads N to whole 256-row pairs)
   const int ldw = W.ld, nblk = W.nblk, nb0 = n0 / SLAB_N;
   const __amdgpu_buffer_rsrc_t rb =
-      WT ? __builtin_amdgcn_make_buffer_rsrc((void*)W.p, (short)0, (int)((size_t)nblk * SLAB_N * K * 2), 0x00020000)
+      WT ? __builtin_amdgcn_make_buffer_rsrc((void*)W.p, (short)0, (int)((size_t)nblk * SLAB_N * Kw * 2), 0x00020000)
          : __builtin_amdgcn_make_buffer_rsrc((void*)(W.p + (size_t)n0 * ldw), (short)0,
                                              (int)((size_t)(N - n0) * ldw * 2), 0x00020000);
 
@@ -370,6 +386,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __
   const int lrow = lane >> 3, lslot = lane & 7;
   auto issue = [&](int k0, int buf) {
     char* base = smem + buf * (BM + BN) * ROWB;
+    const int kw0 = k0 >= Kw ? k0 - Kw : k0;  // the same W slab for both column blocks of A
 #pragma unroll
     for (int j = 0; j < A_INST; ++j) {
       const int row = (wave * A_INST + j) * 8 + lrow;
@@ -382,8 +399,8 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __
       const int ch = lslot ^ ((row >> 1) & 7);
       // packed: the slab of 128 rows x 64 k is one contiguous 16 KB block
       const unsigned off =
-          WT ? (unsigned)((((k0 / BK) * nblk + nb0 + row / SLAB_N) * SLAB_N + row % SLAB_N) * ROWB + ch * 16)
-             : (unsigned)((row * ldw + k0 + ch * 8) * 2);
+          WT ? (unsigned)((((kw0 / BK) * nblk + nb0 + row / SLAB_N) * SLAB_N + row % SLAB_N) * ROWB + ch * 16)
+             : (unsigned)((row * ldw + kw0 + ch * 8) * 2);
       buffer_load_lds16(rb, base + BM * ROWB + (wave * B_INST + j) * 1024, off);
     }
   };
@@ -469,10 +486,13 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __
   }
 }
 
+// A [M][a_parts * K]: a_parts column blocks of K, each multiplied by the
+// same W [N][K] into one accumulator (2: a hi + lo operand pair).
 template <bool WT, class Epi>
-hipError_t launch(const bf16_t* A, int lda, const WOperand& W, int M, int N, int K, const Epi& epi, hipStream_t s) {
+hipError_t launch(const bf16_t* A, int lda, const WOperand& W, int M, int N, int K, const Epi& epi, hipStream_t s,
+                  int a_parts = 1) {
   if (M <= 0 || N <= 0) return hipSuccess;
-  if (K % BK != 0 || lda % 8 != 0) return hipErrorInvalidValue;
+  if (K % BK != 0 || lda % 8 != 0 || a_parts < 1 || a_parts > 2 || lda < a_parts * K) return hipErrorInvalidValue;
   if (WT) {
     // every 256-column tile inside the packing, 32-bit byte offsets
     if (W.nblk <= 0 || W.nblk % 2 || W.nblk * SLAB_N < N || (size_t)W.nblk * SLAB_N * K * 2 >= (1u << 31))
@@ -491,13 +511,13 @@ hipError_t launch(const bf16_t* A, int lda, const WOperand& W, int M, int N, int
       big = true;
       int grid = ((M + 255) / 256) * ((N + 255) / 256);
       hipLaunchKernelGGL((gemm_bf16_dma_kernel<256, 256, 128, 64, 8, WT, Epi>), dim3(grid), dim3(512), 0, s, A, lda,
-                         W, M, N, K, epi);
+                         W, M, N, a_parts * K, K, epi);
     }
   }
   if (!big) {
     int grid = ((M + 127) / 128) * ((N + 127) / 128);
     hipLaunchKernelGGL((gemm_bf16_dma_kernel<128, 128, 64, 64, 4, WT, Epi>), dim3(grid), dim3(256), 0, s, A, lda, W,
-                       M, N, K, epi);
+                       M, N, a_parts * K, K, epi);
   }
   return hipGetLastError();
 }
@@ -510,16 +530,17 @@ hipError_t gemm_bf16_store_f32(const bf16_t* A, int lda, const bf16_t* W, int ld
 }
 
 hipError_t gemm_bf16_residual(const bf16_t* A, int lda, const WOperand& W, float* H, int ldh, const float* bias, int M,
-                              int N, int K, hipStream_t s) {
+                              int N, int K, hipStream_t s, int a_parts) {
   if (N % 4 || ldh % 4) return hipErrorInvalidValue;
-  return launch<true>(A, lda, W, M, N, K, EpiResidual{H, bias, ldh, M, N}, s);
+  return launch<true>(A, lda, W, M, N, K, EpiResidual{H, bias, ldh, M, N}, s, a_parts);
 }
 
 hipError_t gemm_bf16_swiglu(const bf16_t* A, int lda, const WOperand& W, bf16_t* out, int ldo, int M, int N, int K,
-                            hipStream_t s) {
+                            hipStream_t s, int a_parts, int lo_col) {
   if (N % 64 != 0) return hipErrorInvalidValue;
-  if (ldo % 8) return hipErrorInvalidValue;
-  return launch<true>(A, lda, W, M, N, K, EpiSwiGLU{out, ldo, M, N}, s);
+  if (ldo % 8 || lo_col % 8 || lo_col < 0 || (lo_col > 0 && (lo_col < N / 2 || ldo < lo_col + N / 2)))
+    return hipErrorInvalidValue;
+  return launch<true>(A, lda, W, M, N, K, EpiSwiGLU{out, ldo, M, N, lo_col}, s, a_parts);
 }
 
 hipError_t gemm_bf16_gelu(const bf16_t* A, int lda, const WOperand& W, bf16_t* out, int ldo, const float* bias, int M,
@@ -535,9 +556,9 @@ hipError_t gemm_bf16_bias(const bf16_t* A, int lda, const WOperand& W, bf16_t* o
 }
 
 hipError_t gemm_bf16_qkv(const bf16_t* A, int lda, const WOperand& W, const QkvArgs& qa, int M, int N, int K,
-                         hipStream_t s) {
+                         hipStream_t s, int a_parts) {
   if (qa.dh % 64 != 0 || N % 64 != 0) return hipErrorInvalidValue;
-  return launch<true>(A, lda, W, M, N, K, EpiQKV{qa, M}, s);
+  return launch<true>(A, lda, W, M, N, K, EpiQKV{qa, M}, s, a_parts);
 }
 
 }  // namespace vla

@@ -33,14 +33,19 @@ struct WOperand {
 // C (fp32) = acc, W row-major [N][ldw] (ldw % 8 == 0)
 hipError_t gemm_bf16_store_f32(const bf16_t* A, int lda, const bf16_t* W, int ldw, float* C, int ldc, int M,
                                int N, int K, hipStream_t s);
-// The block GEMMs below take packed weights.
+// The block GEMMs below take packed weights.  a_parts = 2 (split operand):
+// A is [M][2K], a hi + lo pair of bf16 values per element side by side
+// (columns [0, K) hi, [K, 2K) lo), and acc = hi * W^T + lo * W^T, twice the
+// MFMA work of a plain bf16 operand and a 16-bit significand in its place.
 // H (fp32 residual) += acc + bias (bias may be NULL)
 hipError_t gemm_bf16_residual(const bf16_t* A, int lda, const WOperand& W, float* H, int ldh, const float* bias,
-                              int M, int N, int K, hipStream_t s);
+                              int M, int N, int K, hipStream_t s, int a_parts = 1);
 // out (bf16) [M][N/2] = silu(gate) * up, W rows interleaved in groups of 32
 // (32 gate rows, then the 32 up rows of the same features); N % 64 == 0.
+// lo_col > 0: the remainder bf16(y - bf16(y)) of each output also goes to
+// column lo_col + c of its row (lo_col >= N/2, ldo >= lo_col + N/2).
 hipError_t gemm_bf16_swiglu(const bf16_t* A, int lda, const WOperand& W, bf16_t* out, int ldo, int M, int N, int K,
-                            hipStream_t s);
+                            hipStream_t s, int a_parts = 1, int lo_col = 0);
 // out (bf16) = gelu_erf(acc + bias)
 hipError_t gemm_bf16_gelu(const bf16_t* A, int lda, const WOperand& W, bf16_t* out, int ldo, const float* bias,
                           int M, int N, int K, hipStream_t s);
@@ -62,7 +67,7 @@ struct QkvArgs {
   int L, H, Hkv, dh;
 };
 hipError_t gemm_bf16_qkv(const bf16_t* A, int lda, const WOperand& W, const QkvArgs& qa, int M, int N, int K,
-                         hipStream_t s);
+                         hipStream_t s, int a_parts = 1);
 
 // out (bf16) = acc + bias (bias may be NULL); N % 8 == 0, ldo % 8 == 0
 hipError_t gemm_bf16_bias(const bf16_t* A, int lda, const WOperand& W, bf16_t* out, int ldo, const float* bias,
@@ -113,6 +118,9 @@ hipError_t decode_down(const bf16_t* a, int fpad, const WOperand& W, float* h, i
 // ----------------------------------------------------- norms and elementwise
 // y[M][d] = norm(x[M][d]) (fp32 in); RMSNorm when beta == NULL and !layernorm.
 hipError_t rmsnorm_bf16(const float* x, const float* g, float eps, bf16_t* y, int M, int d, hipStream_t s);
+// RMSNorm as a split operand: y[M][2d], columns [0, d) bf16(v), [d, 2d) the
+// remainder bf16(v - bf16(v)) of the fp32 result v.
+hipError_t rmsnorm_bf16_split(const float* x, const float* g, float eps, bf16_t* y, int M, int d, hipStream_t s);
 hipError_t layernorm_bf16(const float* x, const float* g, const float* b, float eps, bf16_t* y, int M, int d,
                           hipStream_t s);
 hipError_t rmsnorm_f32(const float* x, const float* g, float eps, float* y, int M, int d, hipStream_t s);

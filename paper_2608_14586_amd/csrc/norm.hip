@@ -25,10 +25,12 @@ struct RowsMerged {
   }
 };
 
+// lo > 0 (bf16 output only): the remainder bf16(v - bf16(v)) of each output
+// v also goes to y + rows(row) + lo + column.
 template <int NCH, bool LAYERNORM, class OutT, class Rows>
 __global__ __launch_bounds__(256) void norm_kernel(const float* __restrict__ x, const float* __restrict__ g,
                                                    const float* __restrict__ bta, float eps, OutT* __restrict__ y,
-                                                   int M, int d, Rows rows) {
+                                                   int M, int d, Rows rows, int lo) {
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= M) return;
@@ -84,6 +86,11 @@ __global__ __launch_bounds__(256) void norm_kernel(const float* __restrict__ x, 
     if constexpr (sizeof(OutT) == 2) {
       u32x2 w = {pack_bf2(o[0], o[1]), pack_bf2(o[2], o[3])};
       *(u32x2*)((bf16_t*)y + at) = w;
+      if (lo) {
+        const u32x2 r = {pack_bf2(o[0] - __uint_as_float(w[0] << 16), o[1] - __uint_as_float(w[0] & 0xFFFF0000u)),
+                         pack_bf2(o[2] - __uint_as_float(w[1] << 16), o[3] - __uint_as_float(w[1] & 0xFFFF0000u))};
+        *(u32x2*)((bf16_t*)y + at + lo) = r;
+      }
     } else {
       *(f32x4*)((float*)y + at) = o;
     }
@@ -92,12 +99,13 @@ __global__ __launch_bounds__(256) void norm_kernel(const float* __restrict__ x, 
 
 template <bool LN, class OutT, class Rows>
 hipError_t launch_norm(const float* x, const float* g, const float* b, float eps, OutT* y, int M, int d,
-                       Rows rows, hipStream_t s) {
+                       Rows rows, hipStream_t s, int lo = 0) {
   if (M <= 0) return hipSuccess;
   if (d % 4 != 0) return hipErrorInvalidValue;
   const int n4 = d / 4;
   dim3 grid((M + 3) / 4), block(256);
-#define VLA_NORM(NCH) hipLaunchKernelGGL((norm_kernel<NCH, LN, OutT, Rows>), grid, block, 0, s, x, g, b, eps, y, M, d, rows)
+#define VLA_NORM(NCH) \
+  hipLaunchKernelGGL((norm_kernel<NCH, LN, OutT, Rows>), grid, block, 0, s, x, g, b, eps, y, M, d, rows, lo)
   if (n4 <= 64) VLA_NORM(1);
   else if (n4 <= 128) VLA_NORM(2);
   else if (n4 <= 256) VLA_NORM(4);
@@ -163,6 +171,9 @@ inline unsigned ew_grid(size_t n) {
 
 hipError_t rmsnorm_bf16(const float* x, const float* g, float eps, bf16_t* y, int M, int d, hipStream_t s) {
   return launch_norm<false>(x, g, (const float*)nullptr, eps, y, M, d, RowsPlain{d}, s);
+}
+hipError_t rmsnorm_bf16_split(const float* x, const float* g, float eps, bf16_t* y, int M, int d, hipStream_t s) {
+  return launch_norm<false>(x, g, (const float*)nullptr, eps, y, M, d, RowsPlain{2 * d}, s, d);
 }
 hipError_t layernorm_bf16(const float* x, const float* g, const float* b, float eps, bf16_t* y, int M, int d,
                           hipStream_t s) {

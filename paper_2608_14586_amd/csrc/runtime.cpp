@@ -69,8 +69,15 @@ struct Stack {
   };
   std::vector<Block> blocks;
 
+  // activation operands of the QKV, gate/up and down GEMMs: bf16, or split
+  // into a hi + lo pair of bf16 values (bf16 decoder stacks)
+  vla_precision prec = VLA_PREC_BF16;
   bool bf16() const { return c.dtype == VLA_BF16; }
   bool llm() const { return !c.norm_is_layernorm; }
+  // the operand buffers hold a split pair (bf16 decoder stacks), so either
+  // precision can run without a new arena
+  bool split_room() const { return bf16() && llm(); }
+  int parts() const { return prec == VLA_PREC_SPLIT ? 2 : 1; }
   // rows of the up projection: interleaved gate/up (LLM) or fc1 (encoder)
   int up_rows() const { return llm() ? 2 * f_pad : f_pad; }
   // arena bytes of a weight matrix [N][K]: bf16 stacks hold it packed
@@ -235,6 +242,8 @@ struct vla_ctx {
     int idx;
     hipEvent_t a, b;
   };
+  // launches left before an injected failure (vla_inject_fault); < 0: none
+  long fault_after = -1;
   bool prof_on = false;
   std::vector<hipEvent_t> prof_pool;
   size_t prof_used = 0;
@@ -294,8 +303,9 @@ void layout(vla_ctx* c, Bump& a) {
     if (!s->present) continue;
     Workspace& w = c->ws[si];
     const size_t M = s->m_max, d = s->c.d_model, e = s->esz;
+    const size_t pairs = s->split_room() ? 2 : 1;
     w.h = (float*)a.take(M * d * 4);
-    w.x = a.take(M * d * e);
+    w.x = a.take(pairs * M * d * e);
     w.q = a.take(M * s->hd * e);
     if (!s->llm()) {
       w.ek = a.take(M * s->kvd * e);
@@ -303,7 +313,7 @@ void layout(vla_ctx* c, Bump& a) {
     }
     w.vt = a.take((size_t)s->c.max_batch * s->kvd * s->ldvt * e);
     w.o = a.take(M * s->hd * e);
-    w.act = a.take(s->bf16() ? M * s->f_pad * e : M * (size_t)s->c.d_ff * (s->llm() ? 3 : 1) * 4);
+    w.act = a.take(s->bf16() ? pairs * M * s->f_pad * e : M * (size_t)s->c.d_ff * (s->llm() ? 3 : 1) * 4);
     if (!s->bf16()) w.qkv_raw = (float*)a.take(M * s->qkv_n * 4);
     w.tok = a.take(M * d * e);
   }
@@ -571,6 +581,8 @@ Status prof_drain(vla_ctx* c) {
 // with a pair of events on that stream attributed to (stack, class).
 #define PLAUNCH(c, stk, cls, expr)                                                          \
   do {                                                                                      \
+    if ((c)->fault_after >= 0 && (c)->fault_after-- == 0)                                   \
+      return fail(VLA_ERR_HIP, "injected failure before launch %s", #expr);                 \
     hipEvent_t a_ = nullptr, b_ = nullptr;                                                  \
     if ((c)->prof_on) {                                                                     \
       Status s_ = prof_event((c), &a_);                                                     \
@@ -618,11 +630,15 @@ Status llm_block_bf16(vla_ctx* c, const Stack::Block& w, int B, int L, bf16_t* k
   const int M = B * L, d = k.d_model;
   hipStream_t st = c->compute;
   Workspace& ws = c->ws[VLA_STACK_LLM];
-  PLAUNCH(c, VLA_STACK_LLM, VLA_K_NORM, vla::rmsnorm_bf16(ws.h, w.n1g, k.norm_eps, (bf16_t*)ws.x, M, d, st));
+  const int P = s.parts();
+  if (P == 2)
+    PLAUNCH(c, VLA_STACK_LLM, VLA_K_NORM, vla::rmsnorm_bf16_split(ws.h, w.n1g, k.norm_eps, (bf16_t*)ws.x, M, d, st));
+  else
+    PLAUNCH(c, VLA_STACK_LLM, VLA_K_NORM, vla::rmsnorm_bf16(ws.h, w.n1g, k.norm_eps, (bf16_t*)ws.x, M, d, st));
   vla::QkvArgs qa{nullptr, k.use_rope ? c->rope_cos : nullptr, k.use_rope ? c->rope_sin : nullptr,
                   (bf16_t*)ws.q, kdst, vdst, (bf16_t*)ws.vt, round_up(L, 64), L, k.n_heads, k.n_kv_heads,
                   k.head_dim};
-  PLAUNCH(c, VLA_STACK_LLM, VLA_K_QKV, vla::gemm_bf16_qkv((const bf16_t*)ws.x, d, Stack::packed(w.w_qkv, s.qkv_n), qa, M, s.qkv_n, d, st));
+  PLAUNCH(c, VLA_STACK_LLM, VLA_K_QKV, vla::gemm_bf16_qkv((const bf16_t*)ws.x, P * d, Stack::packed(w.w_qkv, s.qkv_n), qa, M, s.qkv_n, d, st, P));
   return OK;
 }
 
@@ -635,11 +651,15 @@ Status llm_block_bf16_rest(vla_ctx* c, const Stack::Block& w, int B, int L, cons
   PLAUNCH(c, VLA_STACK_LLM, VLA_K_ATTN, vla::attention_bf16((const bf16_t*)ws.q, kdst, (const bf16_t*)ws.vt, round_up(L, 64), (bf16_t*)ws.o, B,
                            k.n_heads, k.n_kv_heads, L, k.head_dim, k.causal != 0, st));
   PLAUNCH(c, VLA_STACK_LLM, VLA_K_OPROJ, vla::gemm_bf16_residual((const bf16_t*)ws.o, s.hd, Stack::packed(w.w_o, d), ws.h, d, nullptr, M, d, s.hd, st));
-  PLAUNCH(c, VLA_STACK_LLM, VLA_K_NORM, vla::rmsnorm_bf16(ws.h, w.n2g, k.norm_eps, (bf16_t*)ws.x, M, d, st));
-  PLAUNCH(c, VLA_STACK_LLM, VLA_K_MLP_UP, vla::gemm_bf16_swiglu((const bf16_t*)ws.x, d, Stack::packed(w.w_up, 2 * s.f_pad), (bf16_t*)ws.act, s.f_pad,
-                                                      M, 2 * s.f_pad, d, st));
-  PLAUNCH(c, VLA_STACK_LLM, VLA_K_MLP_DOWN, vla::gemm_bf16_residual((const bf16_t*)ws.act, s.f_pad, Stack::packed(w.w_down, d), ws.h, d, nullptr,
-                                                          M, d, s.f_pad, st));
+  const int P = s.parts(), F = s.f_pad;
+  if (P == 2)
+    PLAUNCH(c, VLA_STACK_LLM, VLA_K_NORM, vla::rmsnorm_bf16_split(ws.h, w.n2g, k.norm_eps, (bf16_t*)ws.x, M, d, st));
+  else
+    PLAUNCH(c, VLA_STACK_LLM, VLA_K_NORM, vla::rmsnorm_bf16(ws.h, w.n2g, k.norm_eps, (bf16_t*)ws.x, M, d, st));
+  PLAUNCH(c, VLA_STACK_LLM, VLA_K_MLP_UP, vla::gemm_bf16_swiglu((const bf16_t*)ws.x, P * d, Stack::packed(w.w_up, 2 * F), (bf16_t*)ws.act,
+                                                                P * F, M, 2 * F, d, st, P, P == 2 ? F : 0));
+  PLAUNCH(c, VLA_STACK_LLM, VLA_K_MLP_DOWN, vla::gemm_bf16_residual((const bf16_t*)ws.act, P * F, Stack::packed(w.w_down, d), ws.h, d, nullptr,
+                                                                    M, d, F, st, P));
   return OK;
 }
 
@@ -729,6 +749,24 @@ Status retire_slot(vla_ctx* c, Slot& sl) {
   return OK;
 }
 
+// A frame whose enqueueing failed part-way: wait for what was enqueued (the
+// copies into the caller's buffers included), then free its slot and forget
+// the frame, so the context runs the next frames as before and
+// vla_wait_boundary reports the id as unknown.
+Status abandon_frame(vla_ctx* c, Slot& sl, const Status& why) {
+  (void)hipStreamSynchronize(c->compute);
+  if (c->encs != c->compute) (void)hipStreamSynchronize(c->encs);
+  (void)hipStreamSynchronize(c->copy);
+  sl.used = false;
+  c->history.erase(sl.frame_id);
+  return why;
+}
+
+Status enqueue_blocks(vla_ctx* c, Slot& sl, const void* tokens, vla_dtype in_dt, int B, int L, int k0, int k1,
+                      vla_boundary* out);
+Status enqueue_decode(vla_ctx* c, Slot& sl, const void* x, int B, int pos, int k, void* kv_cache, int L_cap,
+                      vla_boundary* out);
+
 Status run_blocks(vla_ctx* c, uint64_t frame_id, const void* tokens, vla_dtype in_dt, int B, int L, int k0,
                   int k1, vla_boundary* out) {
   if (!c->llm.present) return fail(VLA_ERR_INVALID_ARG, "context has no decoder stack");
@@ -749,7 +787,6 @@ Status run_blocks(vla_ctx* c, uint64_t frame_id, const void* tokens, vla_dtype i
   const size_t kv_bytes = (size_t)(k1 - k0) * layer_elems * s.esz;
   if (out->hidden_bytes < hid_bytes)
     return fail(VLA_ERR_SHAPE, "hidden buffer %zu bytes < %zu", out->hidden_bytes, hid_bytes);
-  const bool want_kv = out->kv != nullptr && kv_bytes > 0;
   if (out->kv && out->kv_bytes < kv_bytes) return fail(VLA_ERR_SHAPE, "kv buffer %zu bytes < %zu", out->kv_bytes, kv_bytes);
   if (!is_pinned_host(out->hidden)) return fail(VLA_ERR_NOT_PINNED, "hidden buffer is not pinned host memory");
   if (out->kv && !is_pinned_host(out->kv)) return fail(VLA_ERR_NOT_PINNED, "kv buffer is not pinned host memory");
@@ -765,7 +802,19 @@ Status run_blocks(vla_ctx* c, uint64_t frame_id, const void* tokens, vla_dtype i
   sl.frame_id = frame_id;
   sl.used = true;
   out->frame_id = frame_id;
+  st = enqueue_blocks(c, sl, tokens, in_dt, B, L, k0, k1, out);
+  return st.code ? abandon_frame(c, sl, st) : OK;
+}
 
+Status enqueue_blocks(vla_ctx* c, Slot& sl, const void* tokens, vla_dtype in_dt, int B, int L, int k0, int k1,
+                      vla_boundary* out) {
+  const Stack& s = c->llm;
+  const size_t n = (size_t)B * L * s.c.d_model;
+  const size_t hid_bytes = n * dtype_size(out->out_dtype);
+  const size_t layer_elems = (size_t)2 * B * s.kvd * L;
+  const size_t kv_bytes = (size_t)(k1 - k0) * layer_elems * s.esz;
+  const bool want_kv = out->kv != nullptr && kv_bytes > 0;
+  Status st;
   // the tokens may be the output of an encoder run enqueued before this call
   const bool split = c->encs != c->compute;
   if (split && c->enc_recorded) HIPTRY(hipStreamWaitEvent(c->compute, c->ev_enc_done, 0));
@@ -831,13 +880,11 @@ Status decode_step(vla_ctx* c, uint64_t frame_id, const void* x, int B, int pos,
   for (int l = 0; l < k; ++l)
     if (!s.blocks[l].loaded) return fail(VLA_ERR_NOT_LOADED, "decoder block %d has no weights", l);
   if (!is_device(kv_cache)) return fail(VLA_ERR_INVALID_ARG, "the KV cache must be device memory");
-  const int d = cf.d_model, H = cf.n_heads, Hkv = cf.n_kv_heads, dh = cf.head_dim;
-  const size_t n = (size_t)B * d;
-  const size_t hid_bytes = n * dtype_size(out->out_dtype);
+  const int d = cf.d_model, H = cf.n_heads, dh = cf.head_dim;
+  const size_t hid_bytes = (size_t)B * d * dtype_size(out->out_dtype);
   if (out->hidden_bytes < hid_bytes) return fail(VLA_ERR_SHAPE, "hidden buffer %zu bytes < %zu", out->hidden_bytes, hid_bytes);
   if (!is_pinned_host(out->hidden)) return fail(VLA_ERR_NOT_PINNED, "hidden buffer is not pinned host memory");
   // scratch borrowed from the prefill workspace
-  Workspace& ws = c->ws[VLA_STACK_LLM];
   const size_t M = s.m_max;
   if ((size_t)B * s.qkv_n * 4 > M * s.hd * 2 || vla::decode_attention_scratch(B, H, dh, pos) > M * s.hd * 2 ||
       (size_t)B * 2 * s.f_pad * 4 > M * s.f_pad * 2 || (size_t)B * s.hd > M * d || (size_t)B * s.f_pad > M * d)
@@ -854,6 +901,19 @@ Status decode_step(vla_ctx* c, uint64_t frame_id, const void* x, int B, int pos,
   sl.frame_id = frame_id;
   sl.used = true;
   out->frame_id = frame_id;
+  st = enqueue_decode(c, sl, x, B, pos, k, kv_cache, L_cap, out);
+  return st.code ? abandon_frame(c, sl, st) : OK;
+}
+
+Status enqueue_decode(vla_ctx* c, Slot& sl, const void* x, int B, int pos, int k, void* kv_cache, int L_cap,
+                      vla_boundary* out) {
+  const Stack& s = c->llm;
+  const vla_stack_cfg& cf = s.c;
+  const int d = cf.d_model, H = cf.n_heads, Hkv = cf.n_kv_heads, dh = cf.head_dim;
+  const size_t n = (size_t)B * d;
+  const size_t hid_bytes = n * dtype_size(out->out_dtype);
+  Workspace& ws = c->ws[VLA_STACK_LLM];
+  Status st;
   hipStream_t cs = c->compute;
   HIPTRY(hipEventRecord(sl.ev_start, cs));
   if ((st = intake(c, VLA_STACK_LLM, VLA_BF16, x, n)).code) return st;
@@ -1349,6 +1409,25 @@ vla_status vla_profile_read(vla_ctx* ctx, vla_stack which, vla_kernel_class cls,
   } catch (...) {
     return finish(ctx, fail(VLA_ERR_INVALID_ARG, "internal error"));
   }
+}
+
+vla_status vla_set_precision(vla_ctx* ctx, vla_stack which, vla_precision prec) {
+  if (!ctx) return finish(nullptr, fail(VLA_ERR_INVALID_ARG, "NULL context"));
+  if (which != VLA_STACK_LLM && which != VLA_STACK_ENC) return finish(ctx, fail(VLA_ERR_INVALID_ARG, "bad stack"));
+  if (prec != VLA_PREC_BF16 && prec != VLA_PREC_SPLIT) return finish(ctx, fail(VLA_ERR_INVALID_ARG, "bad precision"));
+  Stack& s = which == VLA_STACK_LLM ? ctx->llm : ctx->enc;
+  if (!s.present) return finish(ctx, fail(VLA_ERR_INVALID_ARG, "context has no such stack"));
+  if (prec == VLA_PREC_SPLIT && !s.split_room())
+    return finish(ctx, fail(VLA_ERR_UNSUPPORTED, "split operands are implemented for bf16 decoder stacks"));
+  // launches already enqueued keep the precision they were enqueued with
+  s.prec = prec;
+  return finish(ctx, OK);
+}
+
+vla_status vla_inject_fault(vla_ctx* ctx, long launches) {
+  if (!ctx) return finish(nullptr, fail(VLA_ERR_INVALID_ARG, "NULL context"));
+  ctx->fault_after = launches < 0 ? -1 : launches;
+  return finish(ctx, OK);
 }
 
 vla_status vla_arena_used(const vla_ctx* ctx, size_t* bytes) {

@@ -11,12 +11,12 @@ import synth
 from synth.configs import llama_like, Workload
 
 from paper_2608_14586_amd import binding as vb
-from prefix_cases import log, rel_l2
+from prefix_cases import f32_weights, log, rel_l2
 
 pytestmark = pytest.mark.gpu
 
 
-def _run(shape, B, L, k, steps, name, out_dtype="f32"):
+def _run(shape, B, L, k, steps, name, out_dtype="f32", nan_tail=False):
     import torch
     wl = Workload(name, "bf16", shape, None)
     W = [synth.llm_block_weights(wl, l, perturbed=True) for l in range(k)]
@@ -30,6 +30,9 @@ def _run(shape, B, L, k, steps, name, out_dtype="f32"):
     ctx.vla_run_prefix(1, np.ascontiguousarray(toks[:, :L]), B, L, k, bnd)
     ctx.vla_wait_boundary(1, 60000)
     cache = torch.zeros((k, 2, B, Hkv, L_cap, dh), dtype=torch.bfloat16, device="cuda")
+    if nan_tail:
+        # rows past the prefix hold bf16 NaN (0x7FC0): the interface asks only for rows [0, pos)
+        cache.view(torch.int16).fill_(0x7FC0)
     cache[:, :, :, :, :L] = bnd.kv.cuda()
     outs = []
     for t in range(steps):
@@ -72,6 +75,26 @@ def test_decode_steps_match_oracle(name, shape, B, L, k):
             assert e < 1e-2, (name, t, b, e)
 
 
+def test_decode_ignores_cache_rows_past_pos():
+    # GQA 14/2: the rows from pos on hold NaN before each step (the step
+    # writes row pos itself); the keys past pos in the last split are masked
+    # and must not reach the output
+    shape = llama_like(2, 896, 14, 2, 64, 1216)
+    B, L, k, steps = 2, 130, 2, 3
+    wl, W, toks, outs, cache, _ = _run(shape, B, L, k, steps, "dec_nan", nan_tail=True)
+    x, ref = _oracle_rows(wl, W, toks, L, steps, k)
+    for t in range(steps):
+        for b in range(B):
+            assert np.isfinite(outs[t][b]).all(), (t, b)
+            e = rel_l2(outs[t][b] - x[b, t], ref[b, t] - x[b, t])
+            log("dec_nan step %d seq %d: update rel L2 %.2e" % (t, b, e))
+            assert e < 1e-2, (t, b, e)
+    # every appended row is finite, the rows after them still NaN
+    import torch
+    assert torch.isfinite(cache[:, :, :, :, :L + steps].float()).all()
+    assert torch.isnan(cache[:, :, :, :, L + steps:].float()).all()
+
+
 def test_decode_appends_the_prefill_keys():
     # the cache rows a decode step appends agree with what a prefill over the
     # longer sequence writes (bf16 rounding of nearly equal inputs apart)
@@ -112,9 +135,10 @@ def test_decode_k0_returns_input_and_rejects_bad_calls():
         assert e.value.name == code, (args[0], e.value.name)
 
 
-def test_decode_full_size_against_gpu_prefill():
-    # 7B-shaped blocks at the bench length: the step at L against row L of the
-    # GPU's own prefill over L + 1 tokens
+def test_decode_full_size_against_oracle():
+    # 7B-shaped blocks at the bench length: the step at position L against
+    # row L of the oracle's prefill over L + 1 tokens (Eq. (6) applied per
+    # token), and against row L of the GPU's own prefill
     import torch
     wl = synth.CONFIGS["sweep7b"]
     s = wl.llm
@@ -134,10 +158,15 @@ def test_decode_full_size_against_gpu_prefill():
     ctx.vla_wait_boundary(2, 120000)
     x = synth.as_f32(toks[:, L])
     got = ob.hidden.numpy().reshape(B, s.d_model)
-    want = full.hidden.numpy()[:, L]
-    e = rel_l2(got - x, want - x)
-    log("7B-shaped decode at position %d: update rel L2 vs the prefill's row %.2e" % (L, e))
-    assert e < 1e-2
+    Wf = [f32_weights(w) for w in W]
+    ref, kv = oracle.run_prefix(synth.as_f32(toks), lambda l: Wf[l], s, k)
+    e = rel_l2(got - x, ref[:, L] - x)
+    e_pf = rel_l2(got - x, full.hidden.numpy()[:, L] - x)
+    # the appended key and value rows against the oracle's cache row L
+    e_kv = rel_l2(cache[:, :, :, :, L].float().cpu().numpy(), kv[:, :, :, :, L])
+    log("7B-shaped decode at position %d: update rel L2 vs the oracle %.2e, vs the GPU prefill %.2e, "
+        "appended K/V %.2e" % (L, e, e_pf, e_kv))
+    assert e < 1e-2 and e_pf < 1e-2 and e_kv < 1e-2
 
 
 def test_decode_across_the_boundary():

@@ -71,6 +71,10 @@ def test_fp32_prefix_gqa_ragged():
     e_h, e_kv = rel_l2(bnd.hidden.numpy(), ref), rel_l2(bnd.kv.numpy(), kv)
     log("  fp32 GQA ragged: boundary %.2e kv %.2e" % (e_h, e_kv))
     assert e_h <= 1e-4 and e_kv <= 1e-4
+    # the fp32 debug path has no reduced-precision operand to split
+    with pytest.raises(vb.VlaError) as e:
+        c.ctx.vla_set_precision(vb.VLA_STACK_LLM, vb.VLA_PREC_SPLIT)
+    assert e.value.name == "VLA_ERR_UNSUPPORTED"
     c.close()
 
 
@@ -265,4 +269,134 @@ def test_error_paths():
     ctx2.vla_run_prefix(1, tok, 1, 64, 1, c.boundary(n_layers=1))
     ctx2.vla_wait_boundary(1, 10000)
     ctx2.vla_destroy()
+    c.close()
+
+
+@pytest.mark.parametrize("k", [0, 1, 2, 3, 4])
+def test_split_invariance_against_oracle(k):
+    """Eq. (5)-(6): the GPU prefix [0, k) handed over as the bf16 boundary
+    (b = 2, Eq. (11)) and continued by the oracle over [k, N) equals the
+    oracle over the whole stack, for every partition point of an N = 4 stack."""
+    import synth
+    import oracle
+    from prefix_cases import f32_weights
+    N, L = 4, 256
+    c = LlmCase("small_llm", L, N, perturbed=True)
+    tok = c.tokens(frame=11)
+    full, _ = c.oracle(tok, k0=0, k1=N, keep_kv=False)
+    bnd = c.boundary(n_layers=k)
+    c.ctx.vla_run_prefix(20 + k, tok, 1, L, k, bnd)
+    c.ctx.vla_wait_boundary(20 + k, 60000)
+    h = to_f32(bnd.hidden)
+    rest, _ = oracle.run_prefix(h, lambda l: f32_weights(c.W[k + l]), c.s, N - k, keep_kv=False)
+    e = rel_l2(rest, full)
+    log("  split at k=%d of N=%d: GPU [0,k) + oracle [k,N) vs oracle [0,N): %.2e" % (k, N, e))
+    assert e <= 1e-2
+    if k == 0:
+        assert np.array_equal(bnd.hidden.view(__import__("torch").int16).numpy().view(np.uint16), tok)
+    c.close()
+
+
+def test_wait_boundary_times_out_then_collects():
+    """vla_wait_boundary with a zero budget right after a long prefix is
+    enqueued reports VLA_ERR_TIMEOUT and leaves the frame in flight; an
+    unbounded wait then collects it, identical to an undisturbed run."""
+    import torch
+    from paper_2608_14586_amd import binding as vb
+    c = LlmCase("small_llm", 4096, 12)
+    tok = c.tokens(frame=0)
+    ref = c.run(tok, frame=1)
+    bnd = c.boundary()
+    c.ctx.vla_run_prefix(2, tok, 1, c.L, c.k, bnd)
+    with pytest.raises(vb.VlaError) as e:
+        c.ctx.vla_wait_boundary(2, 0)
+    assert e.value.name == "VLA_ERR_TIMEOUT"
+    c.ctx.vla_wait_boundary(2, -1)
+    bits = lambda t: t.view(torch.int16).numpy()
+    assert np.array_equal(bits(bnd.hidden), bits(ref.hidden))
+    assert np.array_equal(bits(bnd.kv), bits(ref.kv))
+    g, x, t = c.ctx.vla_frame_times(2)
+    assert 0 < g <= t
+    c.close()
+
+
+# a 3-block prefix makes 23 launches (intake, 7 per block, the bf16
+# boundary cast), a 3-block decode step with an f32 boundary 16 (intake, 5
+# per block; the boundary is a copy)
+@pytest.mark.parametrize("after", [0, 1, 7, 22])
+def test_failure_mid_frame_frees_its_slot(after):
+    """A launch failing part-way through a frame (injected before launch
+    `after` of the frame; every kernel still runs to completion) fails that
+    call, forgets the frame, and leaves the context working: more frames than
+    there are slots then run bit for bit as on a fresh context."""
+    import torch
+    from paper_2608_14586_amd import binding as vb
+    c = LlmCase("small_llm", 128, 3)
+    toks = [c.tokens(frame=f) for f in range(5)]
+    clean = [c.run(t, frame=100 + f) for f, t in enumerate(toks)]
+    c.ctx.vla_inject_fault(after)
+    with pytest.raises(vb.VlaError) as e:
+        c.ctx.vla_run_prefix(7, toks[0], 1, c.L, c.k, c.boundary())
+    assert e.value.name == "VLA_ERR_HIP" and "injected" in str(e.value)
+    with pytest.raises(vb.VlaError) as e:
+        c.ctx.vla_wait_boundary(7, 1000)
+    assert e.value.name == "VLA_ERR_UNKNOWN_FRAME"
+    bnds = [c.boundary() for _ in toks]
+    for f, t in enumerate(toks):
+        c.ctx.vla_run_prefix(200 + f, t, 1, c.L, c.k, bnds[f])
+    bits = lambda t: t.view(torch.int16).numpy()
+    for f in range(len(toks)):
+        c.ctx.vla_wait_boundary(200 + f, 60000)
+        assert np.array_equal(bits(bnds[f].hidden), bits(clean[f].hidden)), f
+        assert np.array_equal(bits(bnds[f].kv), bits(clean[f].kv)), f
+    # the same for a decode step over the first frame's cache
+    s, pos = c.s, 100
+    cache = torch.zeros((c.k, 2, 1, s.n_kv_heads, c.L, s.head_dim), dtype=torch.bfloat16, device="cuda")
+    cache[:, :, :, :, :pos] = clean[0].kv[:, :, :, :, :pos].cuda()
+    x = np.ascontiguousarray(toks[1][:, pos])
+    want = vb.Boundary(1, 1, s.d_model, 0, s.n_kv_heads, s.head_dim, out_dtype="f32", with_kv=False)
+    c.ctx.vla_decode_step(300, x, 1, pos, c.k, cache.clone(), c.L, want)
+    c.ctx.vla_wait_boundary(300, 60000)
+    c.ctx.vla_inject_fault(min(after, 15))
+    with pytest.raises(vb.VlaError) as e:
+        c.ctx.vla_decode_step(301, x, 1, pos, c.k, cache.clone(), c.L,
+                              vb.Boundary(1, 1, s.d_model, 0, s.n_kv_heads, s.head_dim, out_dtype="f32", with_kv=False))
+    assert e.value.name == "VLA_ERR_HIP"
+    got = vb.Boundary(1, 1, s.d_model, 0, s.n_kv_heads, s.head_dim, out_dtype="f32", with_kv=False)
+    c.ctx.vla_decode_step(302, x, 1, pos, c.k, cache.clone(), c.L, got)
+    c.ctx.vla_wait_boundary(302, 60000)
+    assert np.array_equal(got.hidden.numpy(), want.hidden.numpy())
+    c.close()
+
+
+def test_split_precision_small_stack():
+    """VLA_PREC_SPLIT carries the products' activation operands as hi + lo
+    bf16 pairs: the boundary and every KV layer move closer to the fp32
+    oracle than with plain bf16 operands, on a ragged, perturbed GQA stack;
+    switching back restores the bf16 result bit for bit."""
+    import torch
+    from paper_2608_14586_amd import binding as vb
+    c = LlmCase("small_llm", 333, 6, perturbed=True)
+    tok = c.tokens(frame=4)
+    ref, kv = c.oracle(tok)
+    plain = c.run(tok, frame=1, out_dtype="f32")
+    c.ctx.vla_set_precision(vb.VLA_STACK_LLM, vb.VLA_PREC_SPLIT)
+    split = c.run(tok, frame=2, out_dtype="f32")
+    c.ctx.vla_set_precision(vb.VLA_STACK_LLM, vb.VLA_PREC_BF16)
+    again = c.run(tok, frame=3, out_dtype="f32")
+    e_b, e_s = rel_l2(plain.hidden.numpy(), ref), rel_l2(split.hidden.numpy(), ref)
+    kv_b = [rel_l2(to_f32(plain.kv[l]), kv[l]) for l in range(6)]
+    kv_s = [rel_l2(to_f32(split.kv[l]), kv[l]) for l in range(6)]
+    log("  small_llm L=333 k=6: boundary bf16 %.2e, split %.2e; kv max bf16 %.2e, split %.2e"
+        % (e_b, e_s, max(kv_b), max(kv_s)))
+    assert e_s <= 0.7 * e_b and e_s <= 1e-2 and max(kv_s) <= 1e-2
+    # the first layer's K/V see only the first RMSNorm's split operand
+    assert kv_s[0] <= kv_b[0] and max(kv_s[1:]) <= 0.8 * max(kv_b[1:])
+    assert np.array_equal(again.hidden.numpy(), plain.hidden.numpy())
+    with pytest.raises(vb.VlaError) as e:
+        c.ctx.vla_set_precision(vb.VLA_STACK_ENC, vb.VLA_PREC_SPLIT)
+    assert e.value.name == "VLA_ERR_INVALID_ARG"
+    with pytest.raises(vb.VlaError) as e:
+        c.ctx.vla_set_precision(vb.VLA_STACK_LLM, 7)
+    assert e.value.name == "VLA_ERR_INVALID_ARG"
     c.close()
