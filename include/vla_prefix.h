@@ -248,6 +248,22 @@ vla_status vla_run_blocks(vla_ctx *ctx, uint64_t frame_id, const void *tokens, v
 vla_status vla_decode_step(vla_ctx *ctx, uint64_t frame_id, const void *x, int B, int pos, int k, void *kv_cache,
                            int L_cap, vla_boundary *out);
 
+/* vla_decode_step for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * the same arguments, result and errors, but every scratch buffer of the step
+ * (residual, QKV rows, split-key attention partials, gate/up rows, attention
+ * output, gated activation, input and boundary staging) lies in a fixed
+ * device array of 4 MiB that the library holds on each GPU it runs on until
+ * the process ends, instead of the context's workspace; the call allocates
+ * nothing.  Larger steps fail with VLA_ERR_SHAPE before any launch (the
+ * 7B-shaped stack fits up to position ~6400 at B = 4, ~30000 at B = 1).
+ * Every call on one GPU shares that GPU's array, which keeps the last call's
+ * contents (nothing in it needs to start at zero): calls from different
+ * contexts or streams that overlap on one GPU race.  Within one context a
+ * step waits for the context's earlier copies before it writes the array. */
+vla_status vla_decode_step_static(vla_ctx *ctx, uint64_t frame_id, const void *x, int B, int pos, int k,
+                                  void *kv_cache, int L_cap, vla_boundary *out);
+
 /* The consumer side of the producer-consumer handoff (Sec. IV-C): block the
  * host until frame_id's handoff is complete (its host buffers are then
  * readable), or timeout_ms elapses (< 0: wait forever).  VLA_ERR_TIMEOUT

@@ -89,6 +89,8 @@ def lib():
             "vla_run_prefix": [c_void_p, c_uint64, c_void_p, c_int, c_int, c_int, P(vla_boundary)],
             "vla_run_blocks": [c_void_p, c_uint64, c_void_p, c_int, c_int, c_int, c_int, c_int, P(vla_boundary)],
             "vla_decode_step": [c_void_p, c_uint64, c_void_p, c_int, c_int, c_int, c_void_p, c_int, P(vla_boundary)],
+            "vla_decode_step_static": [c_void_p, c_uint64, c_void_p, c_int, c_int, c_int, c_void_p, c_int,
+                                       P(vla_boundary)],
             "vla_query_vision_sizes": [P(vla_stack_cfg), P(vla_vision_cfg), P(c_size_t)],
             "vla_attach_vision": [c_void_p, P(vla_vision_cfg), c_void_p, c_size_t],
             "vla_load_vision_weights": [c_void_p, P(vla_vision_weights)],
@@ -294,6 +296,11 @@ class Context:
     def vla_decode_step(self, frame_id: int, x, B: int, pos: int, k: int, kv_cache, L_cap: int, out: Boundary):
         _check(lib().vla_decode_step(self.h, frame_id, _ptr(x), B, pos, k, _ptr(kv_cache), L_cap, ctypes.byref(out.c)),
                self.h)
+
+    def vla_decode_step_static(self, frame_id: int, x, B: int, pos: int, k: int, kv_cache, L_cap: int,
+                               out: Boundary):
+        _check(lib().vla_decode_step_static(self.h, frame_id, _ptr(x), B, pos, k, _ptr(kv_cache), L_cap,
+                                            ctypes.byref(out.c)), self.h)
 
     def vla_profile(self, enable: bool):
         _check(lib().vla_profile(self.h, int(enable)), self.h)

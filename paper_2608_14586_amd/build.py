@@ -20,6 +20,7 @@ DEVICE_FLAGS = ["--offload-arch=" + ARCH, "-O3", "-fPIC", "-std=c++17", "-Xclang
 HOST_FLAGS = ["-O2", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-result"]
 
 SOURCES = ["gemm_bf16.hip", "attention_bf16.hip", "decode_bf16.hip", "norm.hip", "fp32_path.hip", "vision.hip",
+           "static_scratch.hip",
            "runtime.cpp",
            "ops.cpp",
            "host_suffix.cpp", "host_suffix_api.cpp", "sched.cpp"]

@@ -115,6 +115,12 @@ hipError_t decode_up(const float* h, const float* g, float eps, const WOperand& 
 // h[b] += a[b] . W^T (the down projection over the padded width fpad)
 hipError_t decode_down(const bf16_t* a, int fpad, const WOperand& W, float* h, int B, int N, hipStream_t s);
 
+// Fixed device scratch of the decode step that allocates nothing
+// (static_scratch.hip): its size, and its address on `device` (resolved once
+// per device; `device` must be the current device the first time).
+size_t static_scratch_bytes();
+hipError_t static_scratch_resolve(int device, void** out);
+
 // ----------------------------------------------------- norms and elementwise
 // y[M][d] = norm(x[M][d]) (fp32 in); RMSNorm when beta == NULL and !layernorm.
 hipError_t rmsnorm_bf16(const float* x, const float* g, float eps, bf16_t* y, int M, int d, hipStream_t s);

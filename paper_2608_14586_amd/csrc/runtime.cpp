@@ -11,7 +11,6 @@
 #include <chrono>
 #include <cmath>
 #include <memory>
-#include <map>
 #include <string>
 #include <thread>
 #include <vector>
@@ -198,6 +197,32 @@ struct FrameTimes {
   float gpu, xfer, total;
 };
 
+// Times of the last HISTORY finished frames, in a fixed ring (recording a
+// frame allocates nothing).
+struct History {
+  struct Entry {
+    uint64_t id = 0;
+    bool used = false;
+    FrameTimes t{};
+  };
+  Entry e[HISTORY];
+  size_t next = 0;
+  const FrameTimes* find(uint64_t id) const {
+    for (const Entry& x : e)
+      if (x.used && x.id == id) return &x.t;
+    return nullptr;
+  }
+  void erase(uint64_t id) {
+    for (Entry& x : e)
+      if (x.used && x.id == id) x.used = false;
+  }
+  void put(uint64_t id, const FrameTimes& t) {
+    erase(id);
+    e[next] = Entry{id, true, t};
+    next = (next + 1) % HISTORY;
+  }
+};
+
 // Scratch of one stack.  The encoder and the decoder run on streams of their
 // own and overlap, so each stack owns its workspace.
 struct Workspace {
@@ -235,7 +260,11 @@ struct vla_ctx {
   bool enc_recorded = false, intake_recorded = false;
   Slot slots[NSLOT];
   int next_slot = 0;
-  std::map<uint64_t, FrameTimes> history;
+  History history;
+  // the fixed decode scratch of this device (vla_decode_step_static), and an
+  // event marking the copy stream's tail when such a step starts
+  void* sscratch = nullptr;
+  hipEvent_t ev_copy_tail = nullptr;
 
   // kernel profiler: event pairs around each launch on the compute stream
   struct ProfRec {
@@ -602,26 +631,31 @@ Status prof_drain(vla_ctx* c) {
     }                                                                                       \
   } while (0)
 
-// input[B*L][d] (host or device, element type in_dt) -> the stack's fp32 residual
-Status intake(vla_ctx* c, int stk, vla_dtype in_dt, const void* in, size_t n) {
-  Workspace& ws = c->ws[stk];
+// input[B*L][d] (host or device, element type in_dt) -> the fp32 residual h,
+// through the staging buffer tok for host bf16 input
+Status intake_to(vla_ctx* c, int stk, vla_dtype in_dt, const void* in, size_t n, float* h, void* tok) {
   const hipStream_t st = stream_of(c, stk);
   const void* src = in;
   if (!is_device(in)) {
     // host input: fp32 goes straight into the residual, bf16 through the
     // input staging buffer
     if (in_dt == VLA_F32) {
-      HIPTRY(hipMemcpyAsync(ws.h, in, n * 4, hipMemcpyHostToDevice, st));
+      HIPTRY(hipMemcpyAsync(h, in, n * 4, hipMemcpyHostToDevice, st));
       return OK;
     }
-    HIPTRY(hipMemcpyAsync(ws.tok, in, n * 2, hipMemcpyHostToDevice, st));
-    src = ws.tok;
+    HIPTRY(hipMemcpyAsync(tok, in, n * 2, hipMemcpyHostToDevice, st));
+    src = tok;
   }
   if (in_dt == VLA_BF16)
-    PLAUNCH(c, stk, VLA_K_OTHER, vla::bf16_to_f32((const bf16_t*)src, ws.h, n, st));
+    PLAUNCH(c, stk, VLA_K_OTHER, vla::bf16_to_f32((const bf16_t*)src, h, n, st));
   else
-    HIPTRY(hipMemcpyAsync(ws.h, src, n * 4, hipMemcpyDeviceToDevice, st));
+    HIPTRY(hipMemcpyAsync(h, src, n * 4, hipMemcpyDeviceToDevice, st));
   return OK;
+}
+
+// ... into the stack's own workspace
+Status intake(vla_ctx* c, int stk, vla_dtype in_dt, const void* in, size_t n) {
+  return intake_to(c, stk, in_dt, in, n, c->ws[stk].h, c->ws[stk].tok);
 }
 
 Status llm_block_bf16(vla_ctx* c, const Stack::Block& w, int B, int L, bf16_t* kdst, bf16_t* vdst) {
@@ -743,8 +777,7 @@ Status retire_slot(vla_ctx* c, Slot& sl) {
   HIPTRY(hipEventElapsedTime(&t.gpu, sl.ev_start, sl.ev_done));
   HIPTRY(hipEventElapsedTime(&t.xfer, sl.ev_hid, sl.ev_copied));
   HIPTRY(hipEventElapsedTime(&t.total, sl.ev_start, sl.ev_copied));
-  c->history[sl.frame_id] = t;
-  while (c->history.size() > HISTORY) c->history.erase(c->history.begin());
+  c->history.put(sl.frame_id, t);
   sl.used = false;
   return OK;
 }
@@ -762,10 +795,41 @@ Status abandon_frame(vla_ctx* c, Slot& sl, const Status& why) {
   return why;
 }
 
+// Device buffers of one decode step: from the prefill workspace, or carved
+// out of the device's fixed scratch (vla_decode_step_static).
+struct DecodeBufs {
+  float* h = nullptr;       // residual [B][d]
+  void* tok = nullptr;      // staging of host input [B][d] bf16
+  float* raw = nullptr;     // QKV rows [B][qkv_n]
+  float* part = nullptr;    // split-key attention partials
+  float* gu = nullptr;      // gate/up rows [B][2 f_pad] (inputs too wide to stage whole)
+  bf16_t* obuf = nullptr;   // attention output [B][H*dh]
+  bf16_t* abuf = nullptr;   // gated activation [B][f_pad]
+  void* hid = nullptr;      // boundary staging [B][d] (f32 at most)
+};
+
+// The fixed-scratch layout of a decode step at batch B, position pos;
+// returns its bytes, and fills `b` when base is not NULL.
+size_t static_decode_layout(const Stack& s, int B, int pos, char* base, DecodeBufs* b) {
+  const size_t d = s.c.d_model;
+  Bump a{base};
+  DecodeBufs t;
+  t.h = (float*)a.take((size_t)B * d * 4);
+  t.tok = a.take((size_t)B * d * 2);
+  t.raw = (float*)a.take((size_t)B * s.qkv_n * 4);
+  t.part = (float*)a.take(vla::decode_attention_scratch(B, s.c.n_heads, s.c.head_dim, pos));
+  t.gu = (float*)a.take((size_t)B * 2 * s.f_pad * 4);
+  t.obuf = (bf16_t*)a.take((size_t)B * s.hd * 2);
+  t.abuf = (bf16_t*)a.take((size_t)B * s.f_pad * 2);
+  t.hid = a.take((size_t)B * d * 4);
+  if (b) *b = t;
+  return align_up(a.off, ALIGN);
+}
+
 Status enqueue_blocks(vla_ctx* c, Slot& sl, const void* tokens, vla_dtype in_dt, int B, int L, int k0, int k1,
                       vla_boundary* out);
 Status enqueue_decode(vla_ctx* c, Slot& sl, const void* x, int B, int pos, int k, void* kv_cache, int L_cap,
-                      vla_boundary* out);
+                      vla_boundary* out, const DecodeBufs& buf, bool fixed);
 
 Status run_blocks(vla_ctx* c, uint64_t frame_id, const void* tokens, vla_dtype in_dt, int B, int L, int k0,
                   int k1, vla_boundary* out) {
@@ -863,8 +927,10 @@ Status enqueue_blocks(vla_ctx* c, Slot& sl, const void* tokens, vla_dtype in_dt,
 
 // One decode step of decoder blocks [0, k): B sequences, one token each at
 // position pos, over the caller's device KV cache [k][2][B][Hkv][L_cap][dh].
+// fixed: the step's scratch comes from the device's fixed array instead of
+// the prefill workspace.
 Status decode_step(vla_ctx* c, uint64_t frame_id, const void* x, int B, int pos, int k, void* kv_cache, int L_cap,
-                   vla_boundary* out) {
+                   vla_boundary* out, bool fixed) {
   if (!c->llm.present) return fail(VLA_ERR_INVALID_ARG, "context has no decoder stack");
   const Stack& s = c->llm;
   const vla_stack_cfg& cf = s.c;
@@ -884,11 +950,29 @@ Status decode_step(vla_ctx* c, uint64_t frame_id, const void* x, int B, int pos,
   const size_t hid_bytes = (size_t)B * d * dtype_size(out->out_dtype);
   if (out->hidden_bytes < hid_bytes) return fail(VLA_ERR_SHAPE, "hidden buffer %zu bytes < %zu", out->hidden_bytes, hid_bytes);
   if (!is_pinned_host(out->hidden)) return fail(VLA_ERR_NOT_PINNED, "hidden buffer is not pinned host memory");
-  // scratch borrowed from the prefill workspace
-  const size_t M = s.m_max;
-  if ((size_t)B * s.qkv_n * 4 > M * s.hd * 2 || vla::decode_attention_scratch(B, H, dh, pos) > M * s.hd * 2 ||
-      (size_t)B * 2 * s.f_pad * 4 > M * s.f_pad * 2 || (size_t)B * s.hd > M * d || (size_t)B * s.f_pad > M * d)
-    return fail(VLA_ERR_SHAPE, "workspace too small for a decode step at position %d (raise max_tokens)", pos);
+  DecodeBufs buf;
+  if (fixed) {
+    const size_t need = static_decode_layout(s, B, pos, nullptr, nullptr);
+    if (need > vla::static_scratch_bytes())
+      return fail(VLA_ERR_SHAPE, "decode step at B=%d, position %d needs %zu bytes of fixed scratch, above its %zu",
+                  B, pos, need, vla::static_scratch_bytes());
+    if (!c->sscratch) return fail(VLA_ERR_HIP, "no fixed scratch on device %d", c->device);
+    static_decode_layout(s, B, pos, (char*)c->sscratch, &buf);
+  } else {
+    // scratch borrowed from the prefill workspace
+    const size_t M = s.m_max;
+    if ((size_t)B * s.qkv_n * 4 > M * s.hd * 2 || vla::decode_attention_scratch(B, H, dh, pos) > M * s.hd * 2 ||
+        (size_t)B * 2 * s.f_pad * 4 > M * s.f_pad * 2 || (size_t)B * s.hd > M * d || (size_t)B * s.f_pad > M * d)
+      return fail(VLA_ERR_SHAPE, "workspace too small for a decode step at position %d (raise max_tokens)", pos);
+    Workspace& ws = c->ws[VLA_STACK_LLM];
+    buf.h = ws.h;
+    buf.tok = ws.tok;
+    buf.raw = (float*)ws.q;
+    buf.part = (float*)ws.o;
+    buf.gu = (float*)ws.act;
+    buf.obuf = (bf16_t*)ws.x;
+    buf.abuf = (bf16_t*)ws.tok;  // the intake is done with it
+  }
   for (auto& sl : c->slots)
     if (sl.used && sl.frame_id == frame_id)
       return fail(VLA_ERR_INVALID_ARG, "frame %llu is already in flight", (unsigned long long)frame_id);
@@ -901,28 +985,34 @@ Status decode_step(vla_ctx* c, uint64_t frame_id, const void* x, int B, int pos,
   sl.frame_id = frame_id;
   sl.used = true;
   out->frame_id = frame_id;
-  st = enqueue_decode(c, sl, x, B, pos, k, kv_cache, L_cap, out);
+  if (!buf.hid) buf.hid = sl.hid;
+  st = enqueue_decode(c, sl, x, B, pos, k, kv_cache, L_cap, out, buf, fixed);
   return st.code ? abandon_frame(c, sl, st) : OK;
 }
 
 Status enqueue_decode(vla_ctx* c, Slot& sl, const void* x, int B, int pos, int k, void* kv_cache, int L_cap,
-                      vla_boundary* out) {
+                      vla_boundary* out, const DecodeBufs& buf, bool fixed) {
   const Stack& s = c->llm;
   const vla_stack_cfg& cf = s.c;
   const int d = cf.d_model, H = cf.n_heads, Hkv = cf.n_kv_heads, dh = cf.head_dim;
   const size_t n = (size_t)B * d;
   const size_t hid_bytes = n * dtype_size(out->out_dtype);
-  Workspace& ws = c->ws[VLA_STACK_LLM];
   Status st;
   hipStream_t cs = c->compute;
+  if (fixed) {
+    // the fixed scratch also stages the boundary: an earlier step's copy out
+    // of it (on the copy stream) must finish before this step writes it
+    HIPTRY(hipEventRecord(c->ev_copy_tail, c->copy));
+    HIPTRY(hipStreamWaitEvent(cs, c->ev_copy_tail, 0));
+  }
   HIPTRY(hipEventRecord(sl.ev_start, cs));
-  if ((st = intake(c, VLA_STACK_LLM, VLA_BF16, x, n)).code) return st;
-  float* h = ws.h;
-  float* raw = (float*)ws.q;
-  float* part = (float*)ws.o;
-  float* gu = (float*)ws.act;
-  bf16_t* obuf = (bf16_t*)ws.x;    // combined attention output [B][H*dh]
-  bf16_t* abuf = (bf16_t*)ws.tok;  // gated activation [B][f_pad] (the intake is done with it)
+  if ((st = intake_to(c, VLA_STACK_LLM, VLA_BF16, x, n, buf.h, buf.tok)).code) return st;
+  float* h = buf.h;
+  float* raw = buf.raw;
+  float* part = buf.part;
+  float* gu = buf.gu;
+  bf16_t* obuf = buf.obuf;
+  bf16_t* abuf = buf.abuf;
   const size_t layer = (size_t)B * Hkv * L_cap * dh;
   for (int l = 0; l < k; ++l) {
     const Stack::Block& w = s.blocks[l];
@@ -937,13 +1027,13 @@ Status enqueue_decode(vla_ctx* c, Slot& sl, const void* x, int B, int pos, int k
     PLAUNCH(c, VLA_STACK_LLM, VLA_K_MLP_DOWN, vla::decode_down(abuf, s.f_pad, Stack::packed(w.w_down, d), h, B, d, cs));
   }
   if (out->out_dtype == VLA_BF16)
-    PLAUNCH(c, VLA_STACK_LLM, VLA_K_OTHER, vla::f32_to_bf16(h, (bf16_t*)sl.hid, n, cs));
+    PLAUNCH(c, VLA_STACK_LLM, VLA_K_OTHER, vla::f32_to_bf16(h, (bf16_t*)buf.hid, n, cs));
   else
-    HIPTRY(hipMemcpyAsync(sl.hid, h, n * 4, hipMemcpyDeviceToDevice, cs));
+    HIPTRY(hipMemcpyAsync(buf.hid, h, n * 4, hipMemcpyDeviceToDevice, cs));
   HIPTRY(hipEventRecord(sl.ev_done, cs));
   HIPTRY(hipStreamWaitEvent(c->copy, sl.ev_done, 0));
   HIPTRY(hipEventRecord(sl.ev_hid, c->copy));
-  HIPTRY(hipMemcpyAsync(out->hidden, sl.hid, hid_bytes, hipMemcpyDeviceToHost, c->copy));
+  HIPTRY(hipMemcpyAsync(out->hidden, buf.hid, hid_bytes, hipMemcpyDeviceToHost, c->copy));
   HIPTRY(hipEventRecord(sl.ev_copied, c->copy));
   return OK;
 }
@@ -1141,6 +1231,9 @@ Status create(const vla_stack_cfg* llm, const vla_stack_cfg* enc, int device, vo
   }
   HIPTRY(hipEventCreateWithFlags(&c->ev_enc_done, hipEventDisableTiming));
   HIPTRY(hipEventCreateWithFlags(&c->ev_intake, hipEventDisableTiming));
+  HIPTRY(hipEventCreateWithFlags(&c->ev_copy_tail, hipEventDisableTiming));
+  // the device's fixed decode scratch, resolved with the device current
+  HIPTRY(vla::static_scratch_resolve(device, &c->sscratch));
   int nkv = c->llm.present ? c->llm.c.n_blocks : 0;
   for (auto& sl : c->slots) {
     HIPTRY(hipEventCreate(&sl.ev_start));
@@ -1169,7 +1262,7 @@ void destroy(vla_ctx* c) {
       if (e) (void)hipEventDestroy(e);
   }
   for (hipEvent_t e : c->prof_pool) (void)hipEventDestroy(e);
-  for (hipEvent_t e : {c->ev_enc_done, c->ev_intake})
+  for (hipEvent_t e : {c->ev_enc_done, c->ev_intake, c->ev_copy_tail})
     if (e) (void)hipEventDestroy(e);
   if (c->own_compute) (void)hipStreamDestroy(c->compute);
   if (c->own_copy) (void)hipStreamDestroy(c->copy);
@@ -1325,7 +1418,18 @@ vla_status vla_decode_step(vla_ctx* ctx, uint64_t frame_id, const void* x, int B
   if (!ctx) return finish(nullptr, fail(VLA_ERR_INVALID_ARG, "NULL context"));
   try {
     if (hipSetDevice(ctx->device) != hipSuccess) return finish(ctx, fail(VLA_ERR_HIP, "hipSetDevice failed"));
-    return finish(ctx, decode_step(ctx, frame_id, x, B, pos, k, kv_cache, L_cap, out));
+    return finish(ctx, decode_step(ctx, frame_id, x, B, pos, k, kv_cache, L_cap, out, false));
+  } catch (...) {
+    return finish(ctx, fail(VLA_ERR_INVALID_ARG, "internal error"));
+  }
+}
+
+vla_status vla_decode_step_static(vla_ctx* ctx, uint64_t frame_id, const void* x, int B, int pos, int k,
+                                  void* kv_cache, int L_cap, vla_boundary* out) {
+  if (!ctx) return finish(nullptr, fail(VLA_ERR_INVALID_ARG, "NULL context"));
+  try {
+    if (hipSetDevice(ctx->device) != hipSuccess) return finish(ctx, fail(VLA_ERR_HIP, "hipSetDevice failed"));
+    return finish(ctx, decode_step(ctx, frame_id, x, B, pos, k, kv_cache, L_cap, out, true));
   } catch (...) {
     return finish(ctx, fail(VLA_ERR_INVALID_ARG, "internal error"));
   }
@@ -1358,7 +1462,7 @@ vla_status vla_wait_boundary(vla_ctx* ctx, uint64_t frame_id, int timeout_ms) {
         std::this_thread::sleep_for(std::chrono::microseconds(20));
       }
     }
-    if (ctx->history.count(frame_id)) return finish(ctx, OK);
+    if (ctx->history.find(frame_id)) return finish(ctx, OK);
     return finish(ctx, fail(VLA_ERR_UNKNOWN_FRAME, "no frame %llu", (unsigned long long)frame_id));
   } catch (...) {
     return finish(ctx, fail(VLA_ERR_INVALID_ARG, "internal error"));
@@ -1367,12 +1471,12 @@ vla_status vla_wait_boundary(vla_ctx* ctx, uint64_t frame_id, int timeout_ms) {
 
 vla_status vla_frame_times(vla_ctx* ctx, uint64_t frame_id, float* t_gpu_ms, float* t_xfer_ms, float* t_total_ms) {
   if (!ctx) return finish(nullptr, fail(VLA_ERR_INVALID_ARG, "NULL context"));
-  auto it = ctx->history.find(frame_id);
-  if (it == ctx->history.end())
+  const FrameTimes* ft = ctx->history.find(frame_id);
+  if (!ft)
     return finish(ctx, fail(VLA_ERR_UNKNOWN_FRAME, "frame %llu has not been waited for", (unsigned long long)frame_id));
-  if (t_gpu_ms) *t_gpu_ms = it->second.gpu;
-  if (t_xfer_ms) *t_xfer_ms = it->second.xfer;
-  if (t_total_ms) *t_total_ms = it->second.total;
+  if (t_gpu_ms) *t_gpu_ms = ft->gpu;
+  if (t_xfer_ms) *t_xfer_ms = ft->xfer;
+  if (t_total_ms) *t_total_ms = ft->total;
   return finish(ctx, OK);
 }
 
