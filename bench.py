@@ -278,6 +278,78 @@ def decode_across(args, ctx, wl, bnd, cache, xs, ob, L_cap):
     return r
 
 
+def prefix_leg(ctx, wl, L, k, steps, warmup, weights_note):
+    """Decoder blocks [0, k) alone over one sequence of L device-resident
+    tokens, back to back, with the boundary and k-layer KV handoff to pinned
+    host memory on the copy stream: ms per frame, prefix tokens/s, T_G, T_X,
+    and per-class kernel times against the algorithmic work (a pass of its own
+    with per-launch events)."""
+    import numpy as np
+    import torch
+    import synth
+    from paper_2608_14586_amd import binding as vb
+    s = wl.llm
+    dev = torch.device("cuda:0")
+    toks = [torch.from_numpy(synth.tokens(wl, frame=f, L=L).view(np.int16)).to(dev) for f in range(2)]
+    bnds = [vb.Boundary(1, L, s.d_model, k, s.n_kv_heads, s.head_dim) for _ in range(3)]
+    fid = [50000 + 1000 * k + L]
+
+    def frames(n, profile=False):
+        ids = []
+        if profile:
+            ctx.vla_profile(True)
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        for i in range(n):
+            f = fid[0]
+            fid[0] += 1
+            ctx.vla_run_prefix(f, toks[i % 2], 1, L, k, bnds[i % 3])
+            ids.append(f)
+        for f in ids[-3:]:
+            ctx.vla_wait_boundary(f, 120000)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t
+        if profile:
+            ctx.vla_profile(False)
+        return wall * 1000.0 / n, [ctx.vla_frame_times(f) for f in ids]
+
+    frames(warmup)
+    ms, times = frames(steps)
+    frames(steps, profile=True)
+    tg = np.array([t[0] for t in times])
+    tx = np.array([t[1] for t in times])
+    work = class_work(wl, "llm", k)
+    classes = {}
+    flops = 0.0
+    for ci, cname in enumerate(vb.KERNEL_CLASSES):
+        tot, cnt = ctx.vla_profile_read(vb.VLA_STACK_LLM, ci)
+        if cnt == 0:
+            continue
+        ent = {"ms_total": round(tot, 4), "launches": cnt, "avg_us": round(tot / cnt * 1000, 2)}
+        if cname in work:
+            unit, per, group = work[cname]
+            avg_s = tot / cnt * group / 1000.0
+            if unit == "flop":
+                flops += per * k
+                ent["tflops"] = round(per / avg_s / 1e12, 1)
+                ent["frac"] = round(per / avg_s / 1e12 / PEAK_BF16_TFLOPS, 4)
+            else:
+                ent["gbs"] = round(per / avg_s / 1e9, 1)
+                ent["frac"] = round(per / avg_s / 1e9 / PEAK_HBM_GBS, 4)
+            ent["per_launch"] = per
+        classes["llm.%s" % cname] = ent
+    return {"workload": "%s: %d decoder blocks (d=%d, %dx%d heads, %d KV heads, SwiGLU %d) over 1x%d tokens, "
+                        "boundary + %d-layer KV to pinned host; %s"
+                        % (wl.name, k, s.d_model, s.n_heads, s.head_dim, s.n_kv_heads, s.d_ff, L, k, weights_note),
+            "k": k, "seq_len": L, "ms_per_frame": round(ms, 3), "prefix_tokens_per_s": round(L / (ms / 1000.0), 1),
+            "t_gpu_prefix_ms": round(float(np.mean(tg)), 3), "t_gpu_prefix_ms_median": round(float(np.median(tg)), 3),
+            "t_boundary_copy_ms": round(float(np.mean(tx)), 4),
+            "t_prefix_plus_handoff_ms": round(float(np.mean([t[2] for t in times])), 3),
+            "frame_tflops": round(flops / 1e12, 3),
+            "mfma_frac_of_bf16_peak": round(flops / (ms / 1000.0) / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "kernels": classes}
+
+
 def norm_large():
     """RMSNorm over a 1 GiB fp32 input (65536 x 4096 -> bf16): a working set
     four times the 256 MiB Infinity Cache, so the rate is HBM's, not the
@@ -627,6 +699,8 @@ def main():
     ap.add_argument("--k", type=int, default=16)
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-legs", action="store_true",
+                    help="skip the extra prefix-only legs (7B at L=1024, split precision, the 0.5B GQA stack)")
     ap.add_argument("--frame", choices=("embeddings", "images"), default="embeddings",
                     help="encoder input: synthetic patch embeddings, or camera images through the stem, with the "
                          "connector's tokens as the decoder's input")
@@ -829,7 +903,32 @@ def main():
         "kernels": kern,
         "sweep": {str(k): {kk: v for kk, v in r.items() if kk != "kernels"} for k, r in results.items()},
     }
+    # the 7B-shaped prefix at L=1024, k=16 (the shorter causal prefill: O-proj
+    # and down give 256 128x128 tiles, half the workgroup slots)
+    if not args.no_legs:
+        log("leg llm7b L=1024 k=16")
+        out["llm7b_L1024_k16"] = prefix_leg(ctx, synth.CONFIGS["llm7b"], 1024, 16, args.steps, args.warmup,
+                                            "the bench context's random-init 7B-shaped blocks")
+        # what the <= 1e-2 parity mode costs at the headline shape: split
+        # (hi + lo) activation operands into the QKV, gate/up and down GEMMs
+        log("leg precision split, L=%d k=%d" % (L, args.k))
+        ctx.vla_set_precision(vb.VLA_STACK_LLM, vb.VLA_PREC_SPLIT)
+        leg = prefix_leg(ctx, wl, L, args.k, args.steps, args.warmup,
+                         "activation operands of the QKV, gate/up and down GEMMs split into hi + lo bf16")
+        ctx.vla_set_precision(vb.VLA_STACK_LLM, vb.VLA_PREC_BF16)
+        leg["vs_bf16_operands_ms"] = round(leg["t_gpu_prefix_ms"] / head["t_gpu_prefix_ms"], 3)
+        out["precision_split_L%d_k%d" % (L, args.k)] = leg
     ctx.vla_destroy()
+    if not args.no_legs:
+        # the 0.5B-class GQA prefix: d=896, 14x64 heads over 2 KV heads, L=4096, k=12
+        sw = synth.CONFIGS["small_llm"]
+        log("leg small_llm L=%d k=%d" % (sw.seq, sw.k))
+        sctx = vb.Context(llm=vb.stack_cfg(sw.llm, "bf16", max_tokens=sw.seq, max_batch=1, n_blocks=sw.k))
+        for l in range(sw.k):
+            sctx.vla_load_block_weights(vb.VLA_STACK_LLM, l, synth.llm_block_weights(sw, l))
+        out["small_llm_L4096_k12"] = prefix_leg(sctx, sw, sw.seq, sw.k, args.steps, args.warmup,
+                                                "random-init N(0,0.02) weights")
+        sctx.vla_destroy()
     out["norm_large"] = norm_large()
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")

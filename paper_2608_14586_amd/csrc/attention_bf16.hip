@@ -7,7 +7,10 @@
 // ds_write) into a ring of stages, the 16-byte chunks of each row
 // XOR-swizzled so that fragment reads hit every bank once per 16-lane phase;
 // a barrier waits only for the tile about to be read (vmcnt(N)), so later
-// tiles stay in flight across it.  Key rows past L read as zero through the
+// tiles stay in flight across it.  Each stage is an LDS array of its own and
+// the tile loop is unrolled over the stages, so the compiler can tell a
+// stage's fragment reads from the DMA writes into the next stage and never
+// drains the ring before them.  Key rows past L read as zero through the
 // buffer resource; V^T columns past L are zeroed in LDS in the last tile.
 //
 // The scores are formed transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16
@@ -27,6 +30,8 @@
 // issued so that co-resident workgroups carry complementary amounts of work.
 
 #include <math.h>
+
+#include <type_traits>
 
 #include "kernels.h"
 
@@ -51,6 +56,13 @@ __device__ __forceinline__ void wait_barrier() {
   asm volatile("" ::: "memory");
 }
 
+// wait until at most N of this wave's global loads are outstanding
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
+}
+
 template <int DH, bool CAUSAL, int NS>
 __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
                                                        const bf16_t* __restrict__ vt, int ldvt,
@@ -61,7 +73,11 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict
   constexpr int STAGE = KT + VT;
   constexpr int KI = KT / 1024 / 4, VI = VT / 1024 / 4;  // 1 KB loads per wave per tile
   constexpr int ND = DH / 32;
-  __shared__ __attribute__((aligned(1024))) char smem[NS * STAGE];
+  // one array per stage: every access names its stage's array, so the
+  // compiler can tell a stage's fragment reads from another stage's DMA writes
+  __shared__ __attribute__((aligned(1024))) char sm0[STAGE];
+  __shared__ __attribute__((aligned(1024))) char sm1[STAGE];
+  __shared__ __attribute__((aligned(1024))) char sm2[NS > 2 ? STAGE : 16];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, li = lane & 31;
@@ -84,22 +100,21 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict
   const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc((void*)kh, (short)0, L * DH * 2, 0x00020000);
   const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc((void*)vh, (short)0, DH * ldvt * 2, 0x00020000);
 
+  // the wave's queries as MFMA B fragments, loaded without branches: lanes
+  // past L load row L-1 (their scores and outputs are never stored)
   bf16x8 fq[DH / 16];
+  const int qrow = min(qi, L - 1);
 #pragma unroll
-  for (int ks = 0; ks < DH / 16; ++ks) {
-    if (qi < L)
-      fq[ks] = *(const bf16x8*)(qh + (size_t)qi * DH + ks * 16 + half * 8);
-    else
-      fq[ks] = bf16x8{0, 0, 0, 0, 0, 0, 0, 0};
-  }
+  for (int ks = 0; ks < DH / 16; ++ks) fq[ks] = *(const bf16x8*)(qh + (size_t)qrow * DH + ks * 16 + half * 8);
 
   const int kend = CAUSAL ? min(L, q0 + BQ) : L;
   const int ntiles = (kend + BKV - 1) / BKV;
 
   // K row r of a tile: 16-byte chunk c stored at chunk c ^ ksw(r); V^T row d: chunk c at c ^ ((d >> 1) & 7)
   auto ksw = [](int r) { return DH == 128 ? (r & 15) : ((r >> 1) & 7); };
-  auto issue = [&](int t) {
-    char* st = smem + (t % NS) * STAGE;
+  auto issue = [&](auto S_, int t) {
+    constexpr int S = decltype(S_)::value;
+    char* st = S == 0 ? sm0 : (S == 1 ? sm1 : sm2);
     const int kb = t * BKV;
 #pragma unroll
     for (int j = 0; j < KI; ++j) {
@@ -127,15 +142,21 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict
   float m_run = -INFINITY, l_part = 0.f;
 
   constexpr int PER = KI + VI;   // loads per wave per tile
-#pragma unroll
-  for (int t = 0; t < NS - 1; ++t)
-    if (t < ntiles) issue(t);
+  // the first NS-1 stages, issued unconditionally (a stage past the last tile
+  // reads zeros through the buffer resources and is never used); then wait
+  // for the query fragments only, so that their loads are known complete
+  // inside the loop and never drain the ring there
+  issue(std::integral_constant<int, 0>{}, 0);
+  if constexpr (NS > 2) issue(std::integral_constant<int, 1>{}, 1);
+  wait_vm<(NS - 1) * PER>();
 
-  for (int it = 0; it < ntiles; ++it) {
+  // tile it in stage S (= it % NS)
+  auto body = [&](auto S_, int it) {
+    constexpr int S = decltype(S_)::value;
     // tile it landed (for every wave), and every wave is done with the stage the next issue overwrites
     if (it + NS - 2 < ntiles) wait_barrier<(NS - 2) * PER>(); else wait_barrier<0>();
     const int kb = it * BKV;
-    char* st = smem + (it % NS) * STAGE;
+    char* st = S == 0 ? sm0 : (S == 1 ? sm1 : sm2);
     if (kb + BKV > L) {
       // ragged last tile: V^T columns of keys >= L hold whatever lies past the
       // keys; zero them (their probabilities are zero, but 0 * NaN is not)
@@ -146,7 +167,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict
       }
       wait_barrier<0>();
     }
-    if (it + NS - 1 < ntiles) issue(it + NS - 1);
+    if (it + NS - 1 < ntiles) issue(std::integral_constant<int, (S + NS - 1) % NS>{}, it + NS - 1);
     const bool active = !CAUSAL || kb <= qw0 + 31;
     if (active && qw0 < L) {
       f32x16 s[2];
@@ -225,6 +246,12 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict
           }
         }
     }
+  };
+  for (int base = 0; base < ntiles; base += NS) {
+    body(std::integral_constant<int, 0>{}, base);
+    if (base + 1 < ntiles) body(std::integral_constant<int, 1>{}, base + 1);
+    if constexpr (NS > 2)
+      if (base + 2 < ntiles) body(std::integral_constant<int, 2>{}, base + 2);
   }
 
   const float l_tot = l_part + __shfl_xor(l_part, 32, 64);
