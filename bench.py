@@ -764,8 +764,14 @@ def main():
     llm_cfg = vb.stack_cfg(s, "bf16", max_tokens=L, max_batch=1, n_blocks=kmax)
     enc_cfg = vb.stack_cfg(e, "bf16", max_tokens=L_img, max_batch=n_img)
     t0 = time.time()
+    # device memory the context takes, by hipMemGetInfo before and after
+    # (its arena plus whatever the runtime adds for its streams and events)
+    torch.cuda.synchronize()
+    free0 = torch.cuda.mem_get_info()[0]
     ctx = vb.Context(llm=llm_cfg, enc=enc_cfg)
-    log("arena %.2f GiB" % (ctx.arena_bytes / 2 ** 30))
+    torch.cuda.synchronize()
+    mem_delta = free0 - torch.cuda.mem_get_info()[0]
+    log("arena %.2f GiB, hipMemGetInfo delta %.2f GiB" % (ctx.arena_bytes / 2 ** 30, mem_delta / 2 ** 30))
     for l in range(e.n_blocks):
         ctx.vla_load_block_weights(vb.VLA_STACK_ENC, l, synth.vit_block_weights(wl, l))
     for l in range(kmax):
@@ -851,6 +857,7 @@ def main():
              "mfma_frac_of_bf16_peak": round(frame_flops(wl, k, images) / (ms / 1000.0) / 1e12 / PEAK_BF16_TFLOPS,
                                              4),
              "hbm_footprint_gib": round(foot[0] / 2 ** 30, 3),
+             "hbm_footprint_note": "arena bytes with k resident decoder blocks (vla_query_sizes)",
              "handoff_bytes": foot[1] + foot[2]}
         if prof:
             classes = {}
@@ -899,6 +906,8 @@ def main():
                    "k": args.k, "seq_len": L, "batch": 1, "n_img": n_img, "img_tokens": L_img,
                    "frame_input": args.frame},
         "mfma_frac_of_bf16_peak": head["mfma_frac_of_bf16_peak"],
+        "hbm_context": {"resident_decoder_blocks": kmax, "arena_gib": round(ctx.arena_bytes / 2 ** 30, 3),
+                        "hipMemGetInfo_delta_gib": round(mem_delta / 2 ** 30, 3)},
         "roofline": roofline,
         "kernels": kern,
         "sweep": {str(k): {kk: v for kk, v in r.items() if kk != "kernels"} for k, r in results.items()},

@@ -3,13 +3,16 @@ configuration), through the C ABI, against the CPU oracle.
 
 * d=896 decoder (L=4096, k=12) and ViT-L encoder (6 x 1024, 24 blocks): whole
   boundary and every KV layer within relative L2 1e-2.
-* d=4096 decoder (L=1024, k=16; L=2048, k=32 as benched): exact bf16
-  arithmetic already drifts past 1e-2 with depth (tests/golden/
-  bf16_noise_floor.json, written by make_noise_floors.py from the oracle), so
-  (i) every block, fed the GPU's own bf16 boundary, matches the oracle's block
-  on that input within 1e-2 (hidden state and its KV), (ii) the whole boundary
-  stays within 1.5x that floor, and (iii) the fp32 debug path over the same
-  stack matches within 1e-4.
+* d=4096 decoder (L=1024, k=16; L=2048, k=32 as benched):
+  - with split activation operands (VLA_PREC_SPLIT: the RMSNorm outputs and
+    the gated activation enter the QKV, gate/up and down GEMMs as hi + lo
+    bf16 pairs), whole boundary and every KV layer within 1e-2;
+  - with plain bf16 operands, exact bf16 arithmetic itself drifts past 1e-2
+    with depth (tests/golden/bf16_noise_floor.json, written by
+    make_noise_floors.py from the oracle alone): the boundary and every KV
+    layer within 1.1x that floor, and every block, fed the GPU's own bf16
+    boundary, within 1e-2 of the oracle's block on that input;
+  - the fp32 debug path over the same stack within 1e-4.
 """
 import json
 import os
@@ -27,9 +30,29 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 
 
 def floor_of(key, block):
-    """bf16 noise floor after `block` + 1 blocks (tests/golden/bf16_noise_floor.json)."""
+    """bf16 noise floor after `block` + 1 blocks, or of block `block`'s KV
+    entries for a key ending in "_kv" (tests/golden/bf16_noise_floor.json)."""
     with open(os.path.join(HERE, "golden", "bf16_noise_floor.json")) as f:
         return json.load(f)[key][block]
+
+
+def _both_precisions(c, tok, ref, kv, key, n):
+    """The same frame with bf16 and with split activation operands against the
+    oracle's boundary `ref` (and KV `kv` unless None), n blocks."""
+    from paper_2608_14586_amd import binding as vb
+    res = {}
+    for name, prec in (("bf16", vb.VLA_PREC_BF16), ("split", vb.VLA_PREC_SPLIT)):
+        c.ctx.vla_set_precision(vb.VLA_STACK_LLM, prec)
+        bnd = c.run(tok, frame=prec + 1)
+        e_h = rel_l2(to_f32(bnd.hidden), ref)
+        e_kv = [rel_l2(to_f32(bnd.kv[l]), kv[l]) for l in range(n)] if kv is not None else []
+        res[name] = (e_h, e_kv)
+        floor = floor_of(key, n - 1)
+        log("  %s, %s operands: boundary %.2e (bf16 floor %.2e, ratio %.2f)%s"
+            % (key, name, e_h, floor, e_h / floor,
+               ", kv max %.2e" % max(e_kv) if e_kv else ""))
+    c.ctx.vla_set_precision(vb.VLA_STACK_LLM, vb.VLA_PREC_BF16)
+    return res
 
 
 def test_small_llm_full():
@@ -77,16 +100,16 @@ def _per_block(c, blocks, tok):
 def test_llm7b_full():
     c = LlmCase("llm7b", 1024, 16)
     tok = c.tokens(frame=0)
-    bnd = c.run(tok, frame=0)
     ref, kv = c.oracle(tok)
-    e_h = rel_l2(to_f32(bnd.hidden), ref)
-    floor = floor_of("llm7b_L1024", 15)
-    e_kv = [rel_l2(to_f32(bnd.kv[l]), kv[l]) for l in range(16)]
-    log("  llm7b L=1024 k=16: boundary %.2e (bf16 floor %.2e, ratio %.2f), kv layer 0 %.2e, layer 15 %.2e"
-        % (e_h, floor, e_h / floor, e_kv[0], e_kv[15]))
-    assert e_h <= 1.5 * floor
+    res = _both_precisions(c, tok, ref, kv, "llm7b_L1024", 16)
+    # split operands: the plain bar
+    e_h, e_kv = res["split"]
+    assert e_h <= 1e-2 and max(e_kv) <= 1e-2, (e_h, e_kv)
+    # bf16 operands: on the floor of exact bf16 arithmetic
+    e_h, e_kv = res["bf16"]
+    assert e_h <= 1.1 * floor_of("llm7b_L1024", 15)
     for l in range(16):
-        assert e_kv[l] <= 1.5 * max(floor_of("llm7b_L1024", max(l - 1, 0)), 1e-2 / 1.5)
+        assert e_kv[l] <= 1.1 * floor_of("llm7b_L1024_kv", l), (l, e_kv[l])
     errs = _per_block(c, list(range(16)), tok)
     for l, e_b, e_h, e_kv in errs:
         assert e_b <= 1e-2 and e_kv <= 1e-2, (l, e_b, e_kv)
@@ -117,15 +140,14 @@ def test_llm7b_fp32_debug_full():
 
 def test_sweep7b_bench_configuration():
     """The benched configuration: 32 resident blocks, L=2048.  Whole boundary
-    at k=32 within 1.5x the bf16 floor; blocks 0, 15 and 31 per block."""
+    at k=32 within 1e-2 with split operands and within 1.1x the bf16 floor
+    with bf16 operands; blocks 0, 15 and 31 per block."""
     c = LlmCase("sweep7b", 2048, 32)
     tok = c.tokens(frame=0)
-    bnd = c.run(tok, frame=0)
     ref, _ = c.oracle(tok, keep_kv=False)
-    e_h = rel_l2(to_f32(bnd.hidden), ref)
-    floor = floor_of("sweep7b_L2048", 31)
-    log("  sweep7b L=2048 k=32: boundary %.2e (bf16 floor %.2e, ratio %.2f)" % (e_h, floor, e_h / floor))
-    assert e_h <= 1.5 * floor
+    res = _both_precisions(c, tok, ref, None, "sweep7b_L2048", 32)
+    assert res["split"][0] <= 1e-2
+    assert res["bf16"][0] <= 1.1 * floor_of("sweep7b_L2048", 31)
     for l, e_b, e_blk, e_kv in _per_block(c, [0, 15, 31], tok):
         assert e_b <= 1e-2 and e_kv <= 1e-2, (l, e_b, e_kv)
     c.close()
