@@ -701,6 +701,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-legs", action="store_true",
                     help="skip the extra prefix-only legs (7B at L=1024, split precision, the 0.5B GQA stack)")
+    ap.add_argument("--only-leg", choices=("llm7b_L1024_k16", "small_llm_L4096_k12"), default=None,
+                    help="run one prefix-only leg alone (for profiling) and print its JSON")
     ap.add_argument("--frame", choices=("embeddings", "images"), default="embeddings",
                     help="encoder input: synthetic patch embeddings, or camera images through the stem, with the "
                          "connector's tokens as the decoder's input")
@@ -741,6 +743,21 @@ def main():
         return
     if args.dual:
         dual_bench(args)
+        return
+
+    if args.only_leg:
+        import synth
+        from paper_2608_14586_amd import binding as vb
+        name = args.only_leg.split("_L")[0]
+        lw = synth.CONFIGS[name]
+        L = 1024 if name == "llm7b" else lw.seq
+        k = 16 if name == "llm7b" else lw.k
+        lctx = vb.Context(llm=vb.stack_cfg(lw.llm, "bf16", max_tokens=L, max_batch=1, n_blocks=k))
+        for l in range(k):
+            lctx.vla_load_block_weights(vb.VLA_STACK_LLM, l, synth.llm_block_weights(lw, l))
+        leg = prefix_leg(lctx, lw, L, k, args.steps, args.warmup, "random-init N(0,0.02) weights")
+        lctx.vla_destroy()
+        print(json.dumps({args.only_leg: leg}), flush=True)
         return
 
     if args.copy_calibration:
