@@ -316,8 +316,12 @@ vla_status vla_profile_read(vla_ctx *ctx, vla_stack which, vla_kernel_class cls,
  *                  significand in place of 8, for twice the MFMA work of
  *                  those three products.  Weights, the attention path, the
  *                  KV cache and the boundary are unchanged.
- * Applies to runs enqueued after the call.  VLA_ERR_UNSUPPORTED for encoder
- * stacks and fp32 stacks (the fp32 debug path has no reduced precision).
+ * Applies to prefix and block runs (vla_run_prefix, vla_run_blocks)
+ * enqueued after the call.  Decode steps (vla_decode_step and its static
+ * variant) keep one bf16 operand per product in either mode: a step adds one
+ * token whose rounding does not accumulate over a long prefill.
+ * VLA_ERR_UNSUPPORTED for encoder stacks and fp32 stacks (the fp32 debug
+ * path has no reduced precision).
  */
 typedef enum { VLA_PREC_BF16 = 0, VLA_PREC_SPLIT = 1 } vla_precision;
 vla_status vla_set_precision(vla_ctx *ctx, vla_stack which, vla_precision prec);
