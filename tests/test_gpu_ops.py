@@ -36,7 +36,11 @@ def test_gemm_bf16(M, N, K):
     (1, 4, 4, 128, 128, True), (1, 4, 4, 200, 128, True), (2, 6, 2, 77, 64, True), (1, 14, 2, 300, 64, True),
     (3, 4, 4, 130, 64, False), (1, 2, 2, 1024, 64, False), (1, 2, 1, 513, 128, False),
     # degenerate lengths: one token, less than one 16-key group, exactly one key tile
-    (1, 2, 2, 1, 64, True), (1, 2, 1, 1, 128, False), (2, 4, 2, 15, 64, True), (1, 2, 2, 64, 128, True)])
+    (1, 2, 2, 1, 64, True), (1, 2, 1, 1, 128, False), (2, 4, 2, 15, 64, True), (1, 2, 2, 64, 128, True),
+    # wide grids: the decoder's own shape (L=2048, 32 heads); ragged with GQA; an odd block count, B=2; a last
+    # block one tile past its partner; one key tile and one token over 256 heads
+    (1, 32, 32, 2048, 128, True), (1, 64, 8, 1000, 128, True), (2, 64, 16, 330, 128, True),
+    (1, 256, 64, 138, 128, True), (1, 256, 256, 64, 128, True), (1, 256, 32, 1, 128, True)])
 def test_attention_bf16(B, H, Hkv, L, dh, causal):
     import torch
     from paper_2608_14586_amd import binding as vb
