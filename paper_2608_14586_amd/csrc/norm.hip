@@ -36,14 +36,24 @@ __global__ __launch_bounds__(256) void norm_kernel(const float* __restrict__ x, 
   if (row >= M) return;
   const int n4 = d >> 2;
   const f32x4* xr = (const f32x4*)(x + (size_t)row * d);
-  f32x4 v[NCH];
+  const f32x4* g4 = (const f32x4*)g;
+  const f32x4* b4 = (const f32x4*)bta;
+  f32x4 v[NCH], gv[NCH], bv[LAYERNORM ? NCH : 1];
   float s = 0.f;
 #pragma unroll
   for (int c = 0; c < NCH; ++c) {
     int i = lane + c * 64;
     v[c] = i < n4 ? xr[i] : f32x4{0.f, 0.f, 0.f, 0.f};
-    s += (v[c][0] + v[c][1]) + (v[c][2] + v[c][3]);
   }
+  // the gains (and biases) load beside the row, not after its reduction
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    int i = lane + c * 64;
+    gv[c] = i < n4 ? g4[i] : f32x4{0.f, 0.f, 0.f, 0.f};
+    if constexpr (LAYERNORM) bv[c] = i < n4 ? b4[i] : f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) s += (v[c][0] + v[c][1]) + (v[c][2] + v[c][3]);
   float mean = 0.f, rstd;
   if (LAYERNORM) {
     mean = warp_sum(s) / (float)d;
@@ -67,20 +77,17 @@ __global__ __launch_bounds__(256) void norm_kernel(const float* __restrict__ x, 
       for (int e = 0; e < 4; ++e) q += v[c][e] * v[c][e];
     rstd = rsqrtf(warp_sum(q) / (float)d + eps);
   }
-  const f32x4* g4 = (const f32x4*)g;
-  const f32x4* b4 = (const f32x4*)bta;
 #pragma unroll
   for (int c = 0; c < NCH; ++c) {
     int i = lane + c * 64;
     if (i >= n4) continue;
-    f32x4 gg = g4[i];
+    const f32x4 gg = gv[c];
     f32x4 o;
 #pragma unroll
     for (int e = 0; e < 4; ++e) o[e] = (v[c][e] - mean) * rstd * gg[e];
-    if (LAYERNORM) {
-      f32x4 bb = b4[i];
+    if constexpr (LAYERNORM) {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) o[e] += bb[e];
+      for (int e = 0; e < 4; ++e) o[e] += bv[c][e];
     }
     const size_t at = rows(row) + (size_t)i * 4;
     if constexpr (sizeof(OutT) == 2) {
