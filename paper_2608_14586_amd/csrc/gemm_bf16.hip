@@ -17,6 +17,8 @@
 // The MFMA 32x32 accumulator layout used by every epilogue: register r of
 // lane l holds row (r/4)*8 + (l/32)*4 + (r%4), column l % 32.
 
+#include <type_traits>
+
 #include "kernels.h"
 
 namespace vla {
@@ -376,7 +378,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __
       (void*)(A + (size_t)m0 * lda), (short)0, (int)((size_t)(M - m0) * lda * 2), 0x00020000);
   // W: row-major rows from n0 on, or the whole packed matrix (every block of
   // a tile lies inside it: the packing pads N to whole 256-row pairs)
-  const int ldw = W.ld, nblk = W.nblk, nb0 = n0 / SLAB_N;
+  const int ldw = W.ld, nblk = W.nblk;
   const __amdgpu_buffer_rsrc_t rb =
       WT ? __builtin_amdgcn_make_buffer_rsrc((void*)W.p, (short)0, (int)((size_t)nblk * SLAB_N * Kw * 2), 0x00020000)
          : __builtin_amdgcn_make_buffer_rsrc((void*)(W.p + (size_t)n0 * ldw), (short)0,
@@ -399,8 +401,9 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __
       const int row = (wave * B_INST + j) * 8 + lrow;
       const int ch = lslot ^ ((row >> 1) & 7);
       // packed: the slab of 128 rows x 64 k is one contiguous 16 KB block
+      const int grow = n0 + row;  // tiles need not start on a 128-row block
       const unsigned off =
-          WT ? (unsigned)((((kw0 / BK) * nblk + nb0 + row / SLAB_N) * SLAB_N + row % SLAB_N) * ROWB + ch * 16)
+          WT ? (unsigned)((((kw0 / BK) * nblk + grow / SLAB_N) * SLAB_N + grow % SLAB_N) * ROWB + ch * 16)
              : (unsigned)((row * ldw + kw0 + ch * 8) * 2);
       buffer_load_lds16(rb, base + BM * ROWB + (wave * B_INST + j) * 1024, off);
     }
@@ -462,7 +465,8 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __
   if constexpr (Epi::kViaLds) {
     // Park one wave row (BM/2 x BN fp32) at a time in the idle slab buffers;
     // 256-thread groups then drain BM/4 (8 waves) or BM/2 (4 waves) rows each.
-    static_assert(BM == 2 * WM, "two wave rows");
+    constexpr int WR = BM / WM, HR = WR / 2;  // wave rows, parked per half
+    static_assert(WR % 2 == 0, "an even number of wave rows");
     static_assert((BM / 2) * BN * 4 <= sizeof(smem), "half tile must fit the slab buffers");
     constexpr int GROUPS = NW / 4, RG = BM / 2 / GROUPS;
     float* T = (float*)smem;
@@ -470,14 +474,15 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       __syncthreads();
-      if (wm == h) {
+      if (wm / HR == h) {
+        const int r0 = (wm % HR) * WM;
 #pragma unroll
         for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
           for (int tn = 0; tn < TN; ++tn)
 #pragma unroll
             for (int r = 0; r < 16; ++r)
-              T[(tm * 32 + acc_row(r, lane)) * BN + wn * WN + tn * 32 + (lane & 31)] = acc.v[tm][tn][r];
+              T[(r0 + tm * 32 + acc_row(r, lane)) * BN + wn * WN + tn * 32 + (lane & 31)] = acc.v[tm][tn][r];
       }
       __syncthreads();
       epi.template drain<RG, BN>(T + grp * RG * BN, m0 + h * (BM / 2) + grp * RG, n0, t);
@@ -509,6 +514,16 @@ hipError_t launch(const bf16_t* A, int lda, const WOperand& W, int M, int N, int
   // slots (two per CU; measured: O-projection and down at M = 1024 4-6%
   // faster, a 288-tile grid 7% slower); otherwise 128x128 tiles (4 waves of
   // 64x64, two workgroups per CU)
+  // QKV: 256x192 tiles (8 waves of 64x96) when they fill whole rounds of one
+  // workgroup per CU
+  if constexpr (std::is_same<Epi, EpiQKV>::value) {
+    const long t192 = (long)((M + 255) / 256) * (N / 192);
+    if (N % 192 == 0 && t192 >= 256 && t192 % 256 == 0) {
+      hipLaunchKernelGGL((gemm_bf16_dma_kernel<256, 192, 64, 96, 8, WT, Epi>), dim3((unsigned)t192), dim3(512), 0, s,
+                         A, lda, W, M, N, a_parts * K, K, epi);
+      return hipGetLastError();
+    }
+  }
   const long tiles256 = (long)((M + 255) / 256) * ((N + 255) / 256);
   const long tiles128 = (long)((M + 127) / 128) * ((N + 127) / 128);
   bool big = false;
