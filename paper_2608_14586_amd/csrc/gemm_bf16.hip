@@ -256,10 +256,11 @@ struct EpiQKV {
     const int dh = q.dh, L = q.L;
     // R tokens x NC/64 column groups x 4 chunks of 8 dims
     constexpr int CH = NC / 16;
-    static_assert((R * CH) % 256 == 0 && R % 16 == 0, "tile must split evenly over the workgroup");
+    static_assert(R % 16 == 0, "whole 16-token V^T chunks");
 #pragma unroll 2
-    for (int j = 0; j < R * CH / 256; ++j) {
+    for (int j = 0; j < (R * CH + 255) / 256; ++j) {
       const int f = tid + 256 * j, row = f / CH, gsel = (f % CH) >> 2, w = (f & 3) * 8;
+      if ((R * CH) % 256 && f >= R * CH) break;
       const int gr = m0 + row, p = n0 + gsel * 64;
       int kind, head, r;
       classify(p, kind, head, r);
@@ -514,12 +515,28 @@ hipError_t launch(const bf16_t* A, int lda, const WOperand& W, int M, int N, int
   // slots (two per CU; measured: O-projection and down at M = 1024 4-6%
   // faster, a 288-tile grid 7% slower); otherwise 128x128 tiles (4 waves of
   // 64x64, two workgroups per CU)
-  // QKV: 256x192 tiles (8 waves of 64x96) when they fill whole rounds of one
-  // workgroup per CU
+  // 8-wave tiles at one workgroup per CU where they fill whole rounds: QKV
+  // 256x192 (waves of 64x96) or 192x384 (96x96), GELU 192x256 (96x64)
+  auto rounds_of = [&](int bm, int bn) -> long {
+    if (N % bn) return 0;
+    const long t = (long)((M + bm - 1) / bm) * (N / bn);
+    return t >= 256 && t % 256 == 0 ? t : 0;
+  };
   if constexpr (std::is_same<Epi, EpiQKV>::value) {
-    const long t192 = (long)((M + 255) / 256) * (N / 192);
-    if (N % 192 == 0 && t192 >= 256 && t192 % 256 == 0) {
-      hipLaunchKernelGGL((gemm_bf16_dma_kernel<256, 192, 64, 96, 8, WT, Epi>), dim3((unsigned)t192), dim3(512), 0, s,
+    if (const long t = rounds_of(256, 192)) {
+      hipLaunchKernelGGL((gemm_bf16_dma_kernel<256, 192, 64, 96, 8, WT, Epi>), dim3((unsigned)t), dim3(512), 0, s,
+                         A, lda, W, M, N, a_parts * K, K, epi);
+      return hipGetLastError();
+    }
+    if (const long t = rounds_of(192, 384)) {
+      hipLaunchKernelGGL((gemm_bf16_dma_kernel<192, 384, 96, 96, 8, WT, Epi>), dim3((unsigned)t), dim3(512), 0, s,
+                         A, lda, W, M, N, a_parts * K, K, epi);
+      return hipGetLastError();
+    }
+  }
+  if constexpr (std::is_same<Epi, EpiGelu>::value) {
+    if (const long t = rounds_of(192, 256)) {
+      hipLaunchKernelGGL((gemm_bf16_dma_kernel<192, 256, 96, 64, 8, WT, Epi>), dim3((unsigned)t), dim3(512), 0, s,
                          A, lda, W, M, N, a_parts * K, K, epi);
       return hipGetLastError();
     }
