@@ -166,6 +166,8 @@ def decode_bench(args):
     ctx = vb.Context(llm=vb.stack_cfg(s, "bf16", max_tokens=L_cap, max_batch=B, n_blocks=k))
     for l in range(k):
         ctx.vla_load_block_weights(vb.VLA_STACK_LLM, l, synth.llm_block_weights(wl, l))
+    if args.decode_precision == "split":
+        ctx.vla_set_precision(vb.VLA_STACK_LLM, vb.VLA_PREC_SPLIT)
     toks = synth.tokens(wl, frame=3, B=B, L=L + T)
     bnd = vb.Boundary(B, L, d, k, Hkv, dh)
     ctx.vla_run_prefix(1, np.ascontiguousarray(toks[:, :L]), B, L, k, bnd)
@@ -220,7 +222,8 @@ def decode_bench(args):
            "dtype": "bf16", "data": "synthetic",
            "tokens_per_s": round(B * 1000 / ms, 1),
            "config": {"workload": "sweep7b decoder blocks (d=4096, 32x128 MHA, SwiGLU 11008) [0,k), bf16 weights "
-                                  "N(0,0.02), KV cache from the prefix handoff", "k": k, "batch": B, "prefix_len": L},
+                                  "N(0,0.02), KV cache from the prefix handoff", "k": k, "batch": B, "prefix_len": L,
+                      "operands": args.decode_precision},
            "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                         "frac": round(achieved / PEAK_HBM_GBS, 4), "bytes_per_step": w_bytes + kv_bytes},
            "kernels": kern}
@@ -711,6 +714,8 @@ def main():
     ap.add_argument("--pipeline", action="store_true",
                     help="measure the partitioned model (GPU prefix + host suffix) instead of the GPU prefix")
     ap.add_argument("--pipeline-ks", default="16,24,28,31,32")
+    ap.add_argument("--decode-precision", choices=("bf16", "split"), default="bf16",
+                    help="activation operands of the prefill and the decode steps (split: hi + lo bf16 pairs)")
     ap.add_argument("--decode", action="store_true",
                     help="measure decode steps of blocks [0,k) over the prefix's KV cache instead")
     ap.add_argument("--decode-steps", type=int, default=32)

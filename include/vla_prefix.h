@@ -256,7 +256,9 @@ vla_status vla_decode_step(vla_ctx *ctx, uint64_t frame_id, const void *x, int B
  * device array of 4 MiB that the library holds on each GPU it runs on until
  * the process ends, instead of the context's workspace; the call allocates
  * nothing.  Larger steps fail with VLA_ERR_SHAPE before any launch (the
- * 7B-shaped stack fits up to position ~6400 at B = 4, ~30000 at B = 1).
+ * 7B-shaped stack fits up to position ~6400 at B = 4, ~30000 at B = 1;
+ * ~6270 and ~30460 with split operands, whose gated activation carries its
+ * remainder rows too).
  * Every call on one GPU shares that GPU's array, which keeps the last call's
  * contents (nothing in it needs to start at zero): calls from different
  * contexts or streams that overlap on one GPU race.  Within one context a
@@ -316,10 +318,10 @@ vla_status vla_profile_read(vla_ctx *ctx, vla_stack which, vla_kernel_class cls,
  *                  significand in place of 8, for twice the MFMA work of
  *                  those three products.  Weights, the attention path, the
  *                  KV cache and the boundary are unchanged.
- * Applies to prefix and block runs (vla_run_prefix, vla_run_blocks)
- * enqueued after the call.  Decode steps (vla_decode_step and its static
- * variant) keep one bf16 operand per product in either mode: a step adds one
- * token whose rounding does not accumulate over a long prefill.
+ * Applies to prefix and block runs (vla_run_prefix, vla_run_blocks) and to
+ * decode steps (vla_decode_step and its static variant) enqueued after the
+ * call; a decode step stages each sequence's hi and lo rows side by side and
+ * streams the weights once, so its cost stays that of the weight stream.
  * VLA_ERR_UNSUPPORTED for encoder stacks and fp32 stacks (the fp32 debug
  * path has no reduced precision).
  */

@@ -46,6 +46,8 @@ constexpr int ATT_KC = 128;        // keys per attention split
 
 __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+// the part of x that bf16(x) leaves out (rounded to bf16 by the caller)
+__device__ __forceinline__ float lo_part(float x) { return x - bf2f(f2bf(x)); }
 
 // acc + sum of the 8 products of bf16 pairs, two per v_dot2_f32_bf16: the
 // bf16 operands go in as they are (no conversion to fp32) and every product
@@ -108,31 +110,47 @@ struct StageNorm {
                             eps);
     __syncthreads();
   }
-  __device__ void fill(bf16_t* xs, const float* sc, int B, int K, int k0, int n, int tid) const {
-    for (int b = 0; b < B; ++b)
-      for (int i = tid; i < n; i += 256) xs[b * GV_KCH + i] = f2bf(h[(size_t)b * K + k0 + i] * sc[b] * g[k0 + i]);
+  // staged row bp = logical row bp / P; with P = 2 rows alternate between
+  // the bf16 value (hi) and its remainder bf16(x - hi) (lo)
+  __device__ void fill(bf16_t* xs, const float* sc, int Bp, int P, int K, int k0, int n, int tid) const {
+    for (int bp = 0; bp < Bp; ++bp) {
+      const int b = bp / P;
+      const bool lo = bp % P;
+      for (int i = tid; i < n; i += 256) {
+        const float x = h[(size_t)b * K + k0 + i] * sc[b] * g[k0 + i];
+        xs[bp * GV_KCH + i] = lo ? f2bf(lo_part(x)) : f2bf(x);
+      }
+    }
   }
-  // dst[0, K) = row b, normalised (K % 4 == 0)
-  __device__ void fill_row(bf16_t* dst, const float* sc, int b, int K, int tid) const {
+  // dst[0, K) = row b normalised, or its remainder (part 1) (K % 4 == 0)
+  __device__ void fill_row(bf16_t* dst, const float* sc, int b, int part, int K, int tid) const {
     const float s = sc[b];
     for (int i = tid * 4; i < K; i += 256 * 4) {
       const f32x4 x = *(const f32x4*)(h + (size_t)b * K + i), gg = *(const f32x4*)(g + i);
-      *(u32x2*)(dst + i) = u32x2{pack_bf2(x[0] * s * gg[0], x[1] * s * gg[1]), pack_bf2(x[2] * s * gg[2], x[3] * s * gg[3])};
+      f32x4 y = {x[0] * s * gg[0], x[1] * s * gg[1], x[2] * s * gg[2], x[3] * s * gg[3]};
+      if (part)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) y[e] = lo_part(y[e]);
+      *(u32x2*)(dst + i) = u32x2{pack_bf2(y[0], y[1]), pack_bf2(y[2], y[3])};
     }
   }
 };
 
-// x = a bf16 row already in global memory, a[B][K]
+// x = a bf16 row already in global memory: row b at a + b * ld, its
+// remainder row (split operands, part 1) lo elements further
 struct StageCopy {
   const bf16_t* a;
+  int ld, lo;
   __device__ void prepare(float*, int, int, int, float*) const {}
-  __device__ void fill(bf16_t* xs, const float*, int B, int K, int k0, int n, int tid) const {
-    for (int b = 0; b < B; ++b)
-      for (int i = tid * 8; i < n; i += 256 * 8)
-        *(u32x4*)(xs + b * GV_KCH + i) = *(const u32x4*)(a + (size_t)b * K + k0 + i);
+  __device__ void fill(bf16_t* xs, const float*, int Bp, int P, int K, int k0, int n, int tid) const {
+    for (int bp = 0; bp < Bp; ++bp) {
+      const bf16_t* src = a + (size_t)(bp / P) * ld + (bp % P) * lo + k0;
+      for (int i = tid * 8; i < n; i += 256 * 8) *(u32x4*)(xs + bp * GV_KCH + i) = *(const u32x4*)(src + i);
+    }
   }
-  __device__ void fill_row(bf16_t* dst, const float*, int b, int K, int tid) const {
-    for (int i = tid * 8; i < K; i += 256 * 8) *(u32x4*)(dst + i) = *(const u32x4*)(a + (size_t)b * K + i);
+  __device__ void fill_row(bf16_t* dst, const float*, int b, int part, int K, int tid) const {
+    const bf16_t* src = a + (size_t)b * ld + part * lo;
+    for (int i = tid * 8; i < K; i += 256 * 8) *(u32x4*)(dst + i) = *(const u32x4*)(src + i);
   }
 };
 
@@ -141,14 +159,18 @@ struct StageCopy {
 // a[b][f] = bf16(silu(gate) * up) from the raw gate/up product gu[B][2*fpad]
 // in the packed row order (each group of 64 rows: 32 gate rows, then their 32
 // up rows).  Features past d_ff have zero weight rows, so they come out zero.
+// Row b of a starts at a + b * ld; lo > 0 also writes bf16(y - bf16(y)) at
+// column lo + f (split operands for the down projection).
 __global__ __launch_bounds__(256) void swiglu_kernel(const float* __restrict__ gu, int fpad, int B,
-                                                     bf16_t* __restrict__ a) {
+                                                     bf16_t* __restrict__ a, int ld, int lo) {
   const int i = blockIdx.x * 256 + threadIdx.x;
   if (i >= B * fpad) return;
   const int b = i / fpad, f = i % fpad;
   const float* r = gu + (size_t)b * 2 * fpad + (f / 32) * 64 + f % 32;
   const float g = r[0];
-  a[i] = f2bf(g / (1.f + __expf(-g)) * r[32]);
+  const float y = g / (1.f + __expf(-g)) * r[32];
+  a[(size_t)b * ld + f] = f2bf(y);
+  if (lo) a[(size_t)b * ld + lo + f] = f2bf(lo_part(y));
 }
 
 // ---------------------------------------------------------------- epilogues
@@ -165,23 +187,28 @@ struct EpiAdd {  // h[b][n] += acc
   __device__ void operator()(int b, int n, float v) const { h[(size_t)b * ld + n] += v; }
 };
 
-// a[b][f] = bf16(silu(gate) * up), from the gate and up sums of feature f
+// a[b][f] = bf16(silu(gate) * up), from the gate and up sums of feature f;
+// lo > 0: also its remainder at a[b][lo + f]
 struct EpiGated {
   bf16_t* a;
-  int ld;
+  int ld, lo;
   __device__ void operator()(int b, int f, float g, float u) const {
-    a[(size_t)b * ld + f] = f2bf(g / (1.f + __expf(-g)) * u);
+    const float y = g / (1.f + __expf(-g)) * u;
+    a[(size_t)b * ld + f] = f2bf(y);
+    if (lo) a[(size_t)b * ld + lo + f] = f2bf(lo_part(y));
   }
 };
 
 // out[b][n] for n in [blockIdx.x*ROWS, +ROWS), b < B: the dot of row n of
-// the packed W [K/64][nblk][128][64] with the staged input row b.
-template <int ROWS, class Stage, class Epi>
+// the packed W [K/64][nblk][128][64] with the staged input row b.  Each
+// logical row is staged as P rows (P = 2: hi and lo of split operands, whose
+// products are summed), B * P <= MB.
+template <int ROWS, int MB, int P, class Stage, class Epi>
 __global__ __launch_bounds__(256) void gemv_chunk_kernel(Stage sg, const bf16_t* __restrict__ W, int nblk, int N, int K,
                                                    int B, Epi epi) {
   constexpr int GV_ROWS = ROWS, J = ROWS / 8;  // rows per workgroup, 8-row groups per lane
-  __shared__ __attribute__((aligned(16))) bf16_t xs[GV_MB * GV_KCH];
-  __shared__ float red[4 * GV_ROWS * GV_MB];
+  __shared__ __attribute__((aligned(16))) bf16_t xs[MB * GV_KCH];
+  __shared__ float red[4 * GV_ROWS * MB];
   __shared__ float sc[GV_MB];
   __shared__ float tmp[4 * GV_MB];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -189,11 +216,12 @@ __global__ __launch_bounds__(256) void gemv_chunk_kernel(Stage sg, const bf16_t*
   const int r8 = lane >> 3, c8 = lane & 7;
   // rows n0 + r8 + 8 j lie in the same 128-row block (ROWS | 128)
   const int blk = n0 / SLAB_N, ra = n0 % SLAB_N + r8;
-  float acc[J][GV_MB];
+  const int Bp = B * P;
+  float acc[J][MB];
 #pragma unroll
   for (int j = 0; j < J; ++j)
 #pragma unroll
-    for (int b = 0; b < GV_MB; ++b) acc[j][b] = 0.f;
+    for (int b = 0; b < MB; ++b) acc[j][b] = 0.f;
   // this wave's slabs of a chunk: wave, wave + 4, ...; a chunk's weight
   // loads (up to 16 per lane) are issued before the staging work they do not
   // depend on, so the HBM fetch overlaps it
@@ -216,15 +244,15 @@ __global__ __launch_bounds__(256) void gemv_chunk_kernel(Stage sg, const bf16_t*
   for (int k0 = 0; k0 < K; k0 += GV_KCH) {
     const int n = min(GV_KCH, K - k0), ns = n / 64;
     __syncthreads();  // the previous chunk's reads of xs are done
-    sg.fill(xs, sc, B, K, k0, n, tid);
+    sg.fill(xs, sc, Bp, P, K, k0, n, tid);
     __syncthreads();
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int sl = wave + 4 * u;
       if (sl < ns) {
 #pragma unroll
-        for (int b = 0; b < GV_MB; ++b)
-          if (b < B) {
+        for (int b = 0; b < MB; ++b)
+          if (b < Bp) {
             const u32x4 xv = *(const u32x4*)(xs + b * GV_KCH + sl * 64 + c8 * 8);
 #pragma unroll
             for (int j = 0; j < J; ++j) acc[j][b] = dot8(wv[u][j], xv, acc[j][b]);
@@ -237,7 +265,7 @@ __global__ __launch_bounds__(256) void gemv_chunk_kernel(Stage sg, const bf16_t*
 #pragma unroll
   for (int j = 0; j < J; ++j)
 #pragma unroll
-    for (int b = 0; b < GV_MB; ++b) {
+    for (int b = 0; b < MB; ++b) {
       float v = acc[j][b];
       v += __shfl_xor(v, 1);
       v += __shfl_xor(v, 2);
@@ -248,7 +276,7 @@ __global__ __launch_bounds__(256) void gemv_chunk_kernel(Stage sg, const bf16_t*
 #pragma unroll
     for (int j = 0; j < J; ++j)
 #pragma unroll
-      for (int b = 0; b < GV_MB; ++b) red[(wave * GV_ROWS + r8 + 8 * j) * GV_MB + b] = acc[j][b];
+      for (int b = 0; b < MB; ++b) red[(wave * GV_ROWS + r8 + 8 * j) * MB + b] = acc[j][b];
   __syncthreads();
   if (tid < GV_ROWS * GV_MB) {
     const int row = tid / GV_MB, b = tid % GV_MB;
@@ -256,7 +284,9 @@ __global__ __launch_bounds__(256) void gemv_chunk_kernel(Stage sg, const bf16_t*
     if (b < B && nn < N) {
       float v = 0.f;
 #pragma unroll
-      for (int w = 0; w < 4; ++w) v += red[(w * GV_ROWS + row) * GV_MB + b];
+      for (int w = 0; w < 4; ++w)
+#pragma unroll
+        for (int q = 0; q < P; ++q) v += red[(w * GV_ROWS + row) * MB + b * P + q];
       epi(b, nn, v);
     }
   }
@@ -275,7 +305,8 @@ __device__ __forceinline__ u32x4 buffer_load16(__amdgpu_buffer_rsrc_t r, unsigne
 // features [16 w, 16 w + 16): their 16 gate rows and 16 up rows, 32 rows apart
 // in the packed order (each 64-row group: 32 gate rows, then their 32 up
 // rows), and epi(b, f, gate, up) writes the gated activation.
-template <int ROWS, bool PAIR, class Stage, class Epi>
+// Each logical row is staged as P rows (hi, lo with P = 2), B * P <= MB.
+template <int ROWS, bool PAIR, int MB, int P, class Stage, class Epi>
 __global__ __launch_bounds__(256) void gemv_stream_kernel(Stage sg, const bf16_t* __restrict__ W, int nblk, int N,
                                                           int K, int B, int Kp, Epi epi) {
   static_assert(!PAIR || ROWS == 32, "a paired workgroup owns 16 gate and 16 up rows");
@@ -284,7 +315,7 @@ __global__ __launch_bounds__(256) void gemv_stream_kernel(Stage sg, const bf16_t
   constexpr int U = KC / 64 / 4;
   constexpr int SPC = KC / 64;                 // slabs per chunk
   extern __shared__ __attribute__((aligned(16))) bf16_t xs[];
-  __shared__ float red[4 * ROWS * GV_MB];
+  __shared__ float red[4 * ROWS * MB];
   __shared__ float sc[GV_MB];
   __shared__ float tmp[4 * GV_MB];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -320,16 +351,17 @@ __global__ __launch_bounds__(256) void gemv_stream_kernel(Stage sg, const bf16_t
   for (int d = 0; d < GS_D; ++d) issue(d, d);
   // the input rows (these barriers also give the first chunks time to land)
   sg.prepare(sc, B, K, tid, tmp);
-  for (int b = 0; b < B; ++b) {
-    sg.fill_row(xs + (size_t)b * Kp, sc, b, K, tid);
+  const int Bp = B * P;
+  for (int b = 0; b < Bp; ++b) {
+    sg.fill_row(xs + (size_t)b * Kp, sc, b / P, b % P, K, tid);
     for (int i = K + tid; i < Kp; i += 256) xs[(size_t)b * Kp + i] = 0;
   }
   __syncthreads();
-  float acc[J][GV_MB];
+  float acc[J][MB];
 #pragma unroll
   for (int j = 0; j < J; ++j)
 #pragma unroll
-    for (int b = 0; b < GV_MB; ++b) acc[j][b] = 0.f;
+    for (int b = 0; b < MB; ++b) acc[j][b] = 0.f;
   const int nch = Kp / KC;
   for (int c0 = 0; c0 < nch; c0 += GS_D) {
 #pragma unroll
@@ -339,8 +371,8 @@ __global__ __launch_bounds__(256) void gemv_stream_kernel(Stage sg, const bf16_t
       for (int u = 0; u < U; ++u) {
         const int sl = c * SPC + wave + 4 * u;
 #pragma unroll
-        for (int b = 0; b < GV_MB; ++b)
-          if (b < B) {
+        for (int b = 0; b < MB; ++b)
+          if (b < Bp) {
             const u32x4 xv = *(const u32x4*)(xs + (size_t)b * Kp + sl * 64 + c8 * 8);
 #pragma unroll
             for (int j = 0; j < J; ++j) acc[j][b] = dot8(wv[d][u][j], xv, acc[j][b]);
@@ -354,7 +386,7 @@ __global__ __launch_bounds__(256) void gemv_stream_kernel(Stage sg, const bf16_t
 #pragma unroll
   for (int j = 0; j < J; ++j)
 #pragma unroll
-    for (int b = 0; b < GV_MB; ++b) {
+    for (int b = 0; b < MB; ++b) {
       float v = acc[j][b];
       v += __shfl_xor(v, 1);
       v += __shfl_xor(v, 2);
@@ -365,7 +397,7 @@ __global__ __launch_bounds__(256) void gemv_stream_kernel(Stage sg, const bf16_t
 #pragma unroll
     for (int j = 0; j < J; ++j)
 #pragma unroll
-      for (int b = 0; b < GV_MB; ++b) red[(wave * ROWS + r8 + 8 * j) * GV_MB + b] = acc[j][b];
+      for (int b = 0; b < MB; ++b) red[(wave * ROWS + r8 + 8 * j) * MB + b] = acc[j][b];
   __syncthreads();
   if constexpr (PAIR) {
     if (tid < 16 * GV_MB) {
@@ -373,10 +405,12 @@ __global__ __launch_bounds__(256) void gemv_stream_kernel(Stage sg, const bf16_t
       if (b < B) {
         float g = 0.f, u = 0.f;
 #pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          g += red[(w * ROWS + fl) * GV_MB + b];
-          u += red[(w * ROWS + 16 + fl) * GV_MB + b];
-        }
+        for (int w = 0; w < 4; ++w)
+#pragma unroll
+          for (int q = 0; q < P; ++q) {
+            g += red[(w * ROWS + fl) * MB + b * P + q];
+            u += red[(w * ROWS + 16 + fl) * MB + b * P + q];
+          }
         epi(b, blockIdx.x * 16 + fl, g, u);
       }
     }
@@ -387,7 +421,9 @@ __global__ __launch_bounds__(256) void gemv_stream_kernel(Stage sg, const bf16_t
       if (b < B && nn < N) {
         float v = 0.f;
 #pragma unroll
-        for (int w = 0; w < 4; ++w) v += red[(w * ROWS + row) * GV_MB + b];
+        for (int w = 0; w < 4; ++w)
+#pragma unroll
+          for (int q = 0; q < P; ++q) v += red[(w * ROWS + row) * MB + b * P + q];
         epi(b, nn, v);
       }
     }
@@ -412,33 +448,34 @@ inline bool stream_offsets_ok(const WOperand& W, int Kp) {
   return (size_t)(Kp / 64 + 16) * W.nblk * SLAB_N * 64 * 2 < (1ull << 31);
 }
 
-template <class Stage, class Epi>
+// B logical rows, each staged as P rows (P = 2: split operands), B * P <= MB
+template <int MB, int P, class Stage, class Epi>
 hipError_t gemv_stream(const Stage& sg, const WOperand& W, int N, int K, int B, const Epi& epi, hipStream_t s) {
   const int Kp = stream_kp(K);
-  const size_t lds = (size_t)B * Kp * 2;
+  const size_t lds = (size_t)B * P * Kp * 2;
   if (!stream_offsets_ok(W, Kp)) return hipErrorInvalidValue;
   if ((N + 15) / 16 >= (lds > GS_LDS_SHARED ? 256 : 512)) {
-    hipError_t e = allow_lds(gemv_stream_kernel<16, false, Stage, Epi>, lds);
+    hipError_t e = allow_lds(gemv_stream_kernel<16, false, MB, P, Stage, Epi>, lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((gemv_stream_kernel<16, false, Stage, Epi>), dim3((N + 15) / 16), dim3(256), lds, s, sg, W.p,
-                       W.nblk, N, K, B, Kp, epi);
+    hipLaunchKernelGGL((gemv_stream_kernel<16, false, MB, P, Stage, Epi>), dim3((N + 15) / 16), dim3(256), lds, s, sg,
+                       W.p, W.nblk, N, K, B, Kp, epi);
   } else {
-    hipError_t e = allow_lds(gemv_stream_kernel<8, false, Stage, Epi>, lds);
+    hipError_t e = allow_lds(gemv_stream_kernel<8, false, MB, P, Stage, Epi>, lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((gemv_stream_kernel<8, false, Stage, Epi>), dim3((N + 7) / 8), dim3(256), lds, s, sg, W.p,
-                       W.nblk, N, K, B, Kp, epi);
+    hipLaunchKernelGGL((gemv_stream_kernel<8, false, MB, P, Stage, Epi>), dim3((N + 7) / 8), dim3(256), lds, s, sg,
+                       W.p, W.nblk, N, K, B, Kp, epi);
   }
   return hipGetLastError();
 }
 
-template <class Stage, class Epi>
+template <int MB, int P, class Stage, class Epi>
 hipError_t gemv_chunk(const Stage& sg, const WOperand& W, int N, int K, int B, const Epi& epi, hipStream_t s) {
   if ((N + 15) / 16 >= 512)
-    hipLaunchKernelGGL((gemv_chunk_kernel<16, Stage, Epi>), dim3((N + 15) / 16), dim3(256), 0, s, sg, W.p, W.nblk, N,
-                       K, B, epi);
+    hipLaunchKernelGGL((gemv_chunk_kernel<16, MB, P, Stage, Epi>), dim3((N + 15) / 16), dim3(256), 0, s, sg, W.p,
+                       W.nblk, N, K, B, epi);
   else
-    hipLaunchKernelGGL((gemv_chunk_kernel<8, Stage, Epi>), dim3((N + 7) / 8), dim3(256), 0, s, sg, W.p, W.nblk, N, K,
-                       B, epi);
+    hipLaunchKernelGGL((gemv_chunk_kernel<8, MB, P, Stage, Epi>), dim3((N + 7) / 8), dim3(256), 0, s, sg, W.p, W.nblk,
+                       N, K, B, epi);
   return hipGetLastError();
 }
 
@@ -446,10 +483,15 @@ inline bool gemv_args_ok(const WOperand& W, int N, int K, int B) {
   return B > 0 && B <= GV_MB && K % 64 == 0 && N > 0 && W.nblk * SLAB_N >= (N + 15) / 16 * 16;
 }
 
+// parts = 1: one bf16 row per sequence (up to 4 staged rows); parts = 2: hi
+// and lo rows (up to 8)
 template <class Stage, class Epi>
-hipError_t gemv(const Stage& sg, const WOperand& W, int N, int K, int B, const Epi& epi, hipStream_t s) {
-  if (!gemv_args_ok(W, N, K, B)) return hipErrorInvalidValue;
-  return use_stream(K, B) ? gemv_stream(sg, W, N, K, B, epi, s) : gemv_chunk(sg, W, N, K, B, epi, s);
+hipError_t gemv(const Stage& sg, const WOperand& W, int N, int K, int B, int parts, const Epi& epi, hipStream_t s) {
+  if (!gemv_args_ok(W, N, K, B) || parts < 1 || parts > 2) return hipErrorInvalidValue;
+  if (parts == 2)
+    return use_stream(K, 2 * B) ? gemv_stream<2 * GV_MB, 2>(sg, W, N, K, B, epi, s)
+                                : gemv_chunk<2 * GV_MB, 2>(sg, W, N, K, B, epi, s);
+  return use_stream(K, B) ? gemv_stream<GV_MB, 1>(sg, W, N, K, B, epi, s) : gemv_chunk<GV_MB, 1>(sg, W, N, K, B, epi, s);
 }
 
 // packed QKV row of true dimension d of a head (the packing keeps every
@@ -659,8 +701,8 @@ __global__ __launch_bounds__(DH) void combine_kernel(const float* __restrict__ p
 }  // namespace
 
 hipError_t decode_qkv(const float* h, const float* g, float eps, const WOperand& W, float* raw, int B, int N, int K,
-                      hipStream_t s) {
-  return gemv(StageNorm{h, g, eps}, W, N, K, B, EpiRaw{raw, N}, s);
+                      hipStream_t s, int parts) {
+  return gemv(StageNorm{h, g, eps}, W, N, K, B, parts, EpiRaw{raw, N}, s);
 }
 
 size_t decode_attention_scratch(int B, int H, int dh, int pos) {
@@ -691,32 +733,47 @@ hipError_t decode_attention(const float* qkv, int qkv_n, const float* rope_cos, 
 }
 
 hipError_t decode_oproj(const bf16_t* o, int K, const WOperand& W, float* h, int B, int N, hipStream_t s) {
-  return gemv(StageCopy{o}, W, N, K, B, EpiAdd{h, N}, s);
+  return gemv(StageCopy{o, K, 0}, W, N, K, B, 1, EpiAdd{h, N}, s);
 }
 
-hipError_t decode_up(const float* h, const float* g, float eps, const WOperand& W, int fpad, float* gu, bf16_t* a,
-                     int B, int K, hipStream_t s) {
+namespace {
+// the gate/up product with SwiGLU: B logical rows staged P times each; the
+// gated activation row b at a + b * P * fpad, its remainder (P = 2) fpad on
+template <int MB, int P>
+hipError_t decode_up_impl(const float* h, const float* g, float eps, const WOperand& W, int fpad, float* gu, bf16_t* a,
+                          int B, int K, hipStream_t s) {
   const int N = 2 * fpad;
-  if (!gemv_args_ok(W, N, K, B) || fpad % 64) return hipErrorInvalidValue;
-  if (use_stream(K, B)) {
+  const EpiGated epi{a, P * fpad, (P - 1) * fpad};
+  if (use_stream(K, B * P)) {
     // SwiGLU in the product's epilogue, 16 features per workgroup
     const int Kp = stream_kp(K);
     if (!stream_offsets_ok(W, Kp)) return hipErrorInvalidValue;
-    hipError_t e = allow_lds(gemv_stream_kernel<32, true, StageNorm, EpiGated>, (size_t)B * Kp * 2);
+    const size_t lds = (size_t)B * P * Kp * 2;
+    hipError_t e = allow_lds(gemv_stream_kernel<32, true, MB, P, StageNorm, EpiGated>, lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((gemv_stream_kernel<32, true, StageNorm, EpiGated>), dim3(fpad / 16), dim3(256),
-                       (size_t)B * Kp * 2, s, StageNorm{h, g, eps}, W.p, W.nblk, N, K, B, Kp, EpiGated{a, fpad});
+    hipLaunchKernelGGL((gemv_stream_kernel<32, true, MB, P, StageNorm, EpiGated>), dim3(fpad / 16), dim3(256), lds, s,
+                       StageNorm{h, g, eps}, W.p, W.nblk, N, K, B, Kp, epi);
     return hipGetLastError();
   }
-  hipError_t e = gemv_chunk(StageNorm{h, g, eps}, W, N, K, B, EpiRaw{gu, N}, s);
+  hipError_t e = gemv_chunk<MB, P>(StageNorm{h, g, eps}, W, N, K, B, EpiRaw{gu, N}, s);
   if (e != hipSuccess) return e;
   const int n = B * fpad;
-  hipLaunchKernelGGL(swiglu_kernel, dim3((n + 255) / 256), dim3(256), 0, s, gu, fpad, B, a);
+  hipLaunchKernelGGL(swiglu_kernel, dim3((n + 255) / 256), dim3(256), 0, s, gu, fpad, B, a, epi.ld, epi.lo);
   return hipGetLastError();
 }
+}  // namespace
 
-hipError_t decode_down(const bf16_t* a, int fpad, const WOperand& W, float* h, int B, int N, hipStream_t s) {
-  return gemv(StageCopy{a}, W, N, fpad, B, EpiAdd{h, N}, s);
+hipError_t decode_up(const float* h, const float* g, float eps, const WOperand& W, int fpad, float* gu, bf16_t* a,
+                     int B, int K, hipStream_t s, int parts) {
+  if (!gemv_args_ok(W, 2 * fpad, K, B) || fpad % 64 || parts < 1 || parts > 2) return hipErrorInvalidValue;
+  return parts == 2 ? decode_up_impl<2 * GV_MB, 2>(h, g, eps, W, fpad, gu, a, B, K, s)
+                    : decode_up_impl<GV_MB, 1>(h, g, eps, W, fpad, gu, a, B, K, s);
+}
+
+hipError_t decode_down(const bf16_t* a, int fpad, const WOperand& W, float* h, int B, int N, hipStream_t s,
+                       int parts) {
+  if (parts < 1 || parts > 2) return hipErrorInvalidValue;
+  return gemv(StageCopy{a, parts * fpad, (parts - 1) * fpad}, W, N, fpad, B, parts, EpiAdd{h, N}, s);
 }
 
 }  // namespace vla

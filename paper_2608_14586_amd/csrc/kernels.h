@@ -93,10 +93,13 @@ hipError_t attention_bf16(const bf16_t* q, const bf16_t* k, const bf16_t* vt, in
 
 // ------------------------------------------------------------ bf16 decode step
 // One new token for each of B <= 4 sequences (decode_bf16.hip).  W operands
-// are the packed resident weights; fp32 rows [B][...] throughout.
+// are the packed resident weights; fp32 rows [B][...] throughout.  parts = 2
+// carries the normalised rows (QKV, gate/up) and the gated activation (down)
+// as split operands, hi = bf16(v) and lo = bf16(v - hi), whose products sum
+// in fp32, as the prefill does under VLA_PREC_SPLIT.
 // QKV (and gate/up): raw[b][n] = (RMSNorm(h[b]) g) . W[n], packed row order.
 hipError_t decode_qkv(const float* h, const float* g, float eps, const WOperand& W, float* raw, int B, int N, int K,
-                      hipStream_t s);
+                      hipStream_t s, int parts = 1);
 // Attention of the token at position pos over cache rows [0, pos] of
 // kc/vc [B][Hkv][L_cap][dh]: RoPE on q and the new key, the new key and value
 // appended at pos, o[B][H*dh] (bf16).  Scratch: split-key partials, fp32,
@@ -108,12 +111,15 @@ hipError_t decode_attention(const float* qkv, int qkv_n, const float* rope_cos, 
 // h[b] += o[b] . W^T (the O projection, o [B][K] bf16)
 hipError_t decode_oproj(const bf16_t* o, int K, const WOperand& W, float* h, int B, int N, hipStream_t s);
 // a[b] = bf16(swiglu(RMSNorm(h[b]) g . W^T)) over the interleaved gate/up
-// rows (N = 2 fpad), the gated activation [B][fpad]; gu [B][2 fpad] fp32 is
-// scratch for inputs too wide to stage whole.
+// rows (N = 2 fpad), the gated activation [B][parts * fpad] (parts = 2: its
+// remainder in columns [fpad, 2 fpad)); gu [B][2 fpad] fp32 is scratch for
+// inputs too wide to stage whole.
 hipError_t decode_up(const float* h, const float* g, float eps, const WOperand& W, int fpad, float* gu, bf16_t* a,
-                     int B, int K, hipStream_t s);
-// h[b] += a[b] . W^T (the down projection over the padded width fpad)
-hipError_t decode_down(const bf16_t* a, int fpad, const WOperand& W, float* h, int B, int N, hipStream_t s);
+                     int B, int K, hipStream_t s, int parts = 1);
+// h[b] += a[b] . W^T (the down projection over the padded width fpad; a as
+// decode_up writes it)
+hipError_t decode_down(const bf16_t* a, int fpad, const WOperand& W, float* h, int B, int N, hipStream_t s,
+                       int parts = 1);
 
 // Fixed device scratch of the decode step that allocates nothing
 // (static_scratch.hip): its size, and its address on `device` (resolved once

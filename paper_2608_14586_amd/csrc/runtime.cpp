@@ -804,7 +804,7 @@ struct DecodeBufs {
   float* part = nullptr;    // split-key attention partials
   float* gu = nullptr;      // gate/up rows [B][2 f_pad] (inputs too wide to stage whole)
   bf16_t* obuf = nullptr;   // attention output [B][H*dh]
-  bf16_t* abuf = nullptr;   // gated activation [B][f_pad]
+  bf16_t* abuf = nullptr;   // gated activation [B][parts * f_pad] (split operands: hi, then lo)
   void* hid = nullptr;      // boundary staging [B][d] (f32 at most)
 };
 
@@ -820,7 +820,7 @@ size_t static_decode_layout(const Stack& s, int B, int pos, char* base, DecodeBu
   t.part = (float*)a.take(vla::decode_attention_scratch(B, s.c.n_heads, s.c.head_dim, pos));
   t.gu = (float*)a.take((size_t)B * 2 * s.f_pad * 4);
   t.obuf = (bf16_t*)a.take((size_t)B * s.hd * 2);
-  t.abuf = (bf16_t*)a.take((size_t)B * s.f_pad * 2);
+  t.abuf = (bf16_t*)a.take((size_t)B * s.parts() * s.f_pad * 2);
   t.hid = a.take((size_t)B * d * 4);
   if (b) *b = t;
   return align_up(a.off, ALIGN);
@@ -962,7 +962,8 @@ Status decode_step(vla_ctx* c, uint64_t frame_id, const void* x, int B, int pos,
     // scratch borrowed from the prefill workspace
     const size_t M = s.m_max;
     if ((size_t)B * s.qkv_n * 4 > M * s.hd * 2 || vla::decode_attention_scratch(B, H, dh, pos) > M * s.hd * 2 ||
-        (size_t)B * 2 * s.f_pad * 4 > M * s.f_pad * 2 || (size_t)B * s.hd > M * d || (size_t)B * s.f_pad > M * d)
+        (size_t)B * 2 * s.f_pad * 4 > M * s.f_pad * 2 || (size_t)B * s.hd > M * d ||
+        (size_t)B * s.parts() * s.f_pad > M * d)
       return fail(VLA_ERR_SHAPE, "workspace too small for a decode step at position %d (raise max_tokens)", pos);
     Workspace& ws = c->ws[VLA_STACK_LLM];
     buf.h = ws.h;
@@ -1014,17 +1015,18 @@ Status enqueue_decode(vla_ctx* c, Slot& sl, const void* x, int B, int pos, int k
   bf16_t* obuf = buf.obuf;
   bf16_t* abuf = buf.abuf;
   const size_t layer = (size_t)B * Hkv * L_cap * dh;
+  const int P = s.parts();  // split operands (hi + lo) under VLA_PREC_SPLIT
   for (int l = 0; l < k; ++l) {
     const Stack::Block& w = s.blocks[l];
     bf16_t* kc = (bf16_t*)kv_cache + (size_t)l * 2 * layer;
     bf16_t* vc = kc + layer;
-    PLAUNCH(c, VLA_STACK_LLM, VLA_K_QKV, vla::decode_qkv(h, w.n1g, cf.norm_eps, Stack::packed(w.w_qkv, s.qkv_n), raw, B, s.qkv_n, d, cs));
+    PLAUNCH(c, VLA_STACK_LLM, VLA_K_QKV, vla::decode_qkv(h, w.n1g, cf.norm_eps, Stack::packed(w.w_qkv, s.qkv_n), raw, B, s.qkv_n, d, cs, P));
     PLAUNCH(c, VLA_STACK_LLM, VLA_K_ATTN, vla::decode_attention(raw, s.qkv_n, cf.use_rope ? c->rope_cos : nullptr,
                                                              cf.use_rope ? c->rope_sin : nullptr, kc, vc, L_cap, pos, B,
                                                              H, Hkv, dh, part, obuf, cs));
     PLAUNCH(c, VLA_STACK_LLM, VLA_K_OPROJ, vla::decode_oproj(obuf, s.hd, Stack::packed(w.w_o, d), h, B, d, cs));
-    PLAUNCH(c, VLA_STACK_LLM, VLA_K_MLP_UP, vla::decode_up(h, w.n2g, cf.norm_eps, Stack::packed(w.w_up, 2 * s.f_pad), s.f_pad, gu, abuf, B, d, cs));
-    PLAUNCH(c, VLA_STACK_LLM, VLA_K_MLP_DOWN, vla::decode_down(abuf, s.f_pad, Stack::packed(w.w_down, d), h, B, d, cs));
+    PLAUNCH(c, VLA_STACK_LLM, VLA_K_MLP_UP, vla::decode_up(h, w.n2g, cf.norm_eps, Stack::packed(w.w_up, 2 * s.f_pad), s.f_pad, gu, abuf, B, d, cs, P));
+    PLAUNCH(c, VLA_STACK_LLM, VLA_K_MLP_DOWN, vla::decode_down(abuf, s.f_pad, Stack::packed(w.w_down, d), h, B, d, cs, P));
   }
   if (out->out_dtype == VLA_BF16)
     PLAUNCH(c, VLA_STACK_LLM, VLA_K_OTHER, vla::f32_to_bf16(h, (bf16_t*)buf.hid, n, cs));

@@ -16,7 +16,7 @@ from prefix_cases import f32_weights, log, rel_l2
 pytestmark = pytest.mark.gpu
 
 
-def _run(shape, B, L, k, steps, name, out_dtype="f32", nan_tail=False):
+def _run(shape, B, L, k, steps, name, out_dtype="f32", nan_tail=False, prec=None, prec_decode=None):
     import torch
     wl = Workload(name, "bf16", shape, None)
     W = [synth.llm_block_weights(wl, l, perturbed=True) for l in range(k)]
@@ -25,6 +25,8 @@ def _run(shape, B, L, k, steps, name, out_dtype="f32", nan_tail=False):
     ctx = vb.Context(llm=vb.stack_cfg(shape, "bf16", max_tokens=L_cap, max_batch=B, n_blocks=k))
     for l in range(k):
         ctx.vla_load_block_weights(vb.VLA_STACK_LLM, l, W[l])
+    if prec is not None:
+        ctx.vla_set_precision(vb.VLA_STACK_LLM, prec)
     toks = synth.normal_bf16(synth.seed_of(name, "tok"), (B, L + steps, d))
     bnd = vb.Boundary(B, L, d, k, Hkv, dh)
     ctx.vla_run_prefix(1, np.ascontiguousarray(toks[:, :L]), B, L, k, bnd)
@@ -34,6 +36,8 @@ def _run(shape, B, L, k, steps, name, out_dtype="f32", nan_tail=False):
         # rows past the prefix hold bf16 NaN (0x7FC0): the interface asks only for rows [0, pos)
         cache.view(torch.int16).fill_(0x7FC0)
     cache[:, :, :, :, :L] = bnd.kv.cuda()
+    if prec_decode is not None:
+        ctx.vla_set_precision(vb.VLA_STACK_LLM, prec_decode)
     outs = []
     for t in range(steps):
         ob = vb.Boundary(B, 1, d, 0, Hkv, dh, out_dtype=out_dtype, with_kv=False)
@@ -72,6 +76,35 @@ def test_decode_steps_match_oracle(name, shape, B, L, k):
             # the blocks' update of the residual, at the prefix's 1e-2 bar
             e = rel_l2(outs[t][b] - x[b, t], ref[b, t] - x[b, t])
             log("%s step %d seq %d: update rel L2 %.2e" % (name, t, b, e))
+            assert e < 1e-2, (name, t, b, e)
+
+
+@pytest.mark.parametrize("name,shape,B,L,k", [
+    ("decs_gqa", llama_like(2, 256, 4, 2, 64, 704), 2, 77, 2),
+    ("decs_short", llama_like(3, 128, 2, 2, 64, 320), 1, 1, 3),
+    # eight staged rows (four sequences, hi and lo) in the streaming GEMV
+    ("decs_stream4", llama_like(2, 1024, 8, 2, 128, 2816), 4, 100, 2),
+    ("decs_stream3", llama_like(1, 1024, 16, 4, 64, 2816), 3, 257, 1),
+    # d_ff = 11008: the down product's hi and lo rows of four sequences exceed
+    # the streaming kernel's LDS and take the chunked GEMV
+    ("decs_chunk", llama_like(1, 512, 8, 2, 64, 11008), 4, 60, 1),
+])
+def test_split_decode_steps_match_oracle(name, shape, B, L, k):
+    # VLA_PREC_SPLIT also carries the decode step's normalised rows and gated
+    # activation as hi + lo bf16 pairs; the prefill before it runs split too
+    steps = 2
+    wl, W, toks, outs, _, _ = _run(shape, B, L, k, steps, name, prec=vb.VLA_PREC_SPLIT)
+    # the same split prefill, then bf16 decode steps
+    _, _, _, outs_bf16, _, _ = _run(shape, B, L, k, steps, name, prec=vb.VLA_PREC_SPLIT,
+                                    prec_decode=vb.VLA_PREC_BF16)
+    x, ref = _oracle_rows(wl, W, toks, L, steps, k)
+    for t in range(steps):
+        # the mode reaches the step: its products differ from the bf16 ones
+        assert not np.array_equal(outs[t], outs_bf16[t]), (name, t)
+        for b in range(B):
+            e = rel_l2(outs[t][b] - x[b, t], ref[b, t] - x[b, t])
+            e16 = rel_l2(outs_bf16[t][b] - x[b, t], ref[b, t] - x[b, t])
+            log("%s step %d seq %d: update rel L2 %.2e split, %.2e bf16" % (name, t, b, e, e16))
             assert e < 1e-2, (name, t, b, e)
 
 
@@ -167,6 +200,42 @@ def test_decode_full_size_against_oracle():
     log("7B-shaped decode at position %d: update rel L2 vs the oracle %.2e, vs the GPU prefill %.2e, "
         "appended K/V %.2e" % (L, e, e_pf, e_kv))
     assert e < 1e-2 and e_pf < 1e-2 and e_kv < 1e-2
+
+
+def test_split_decode_7b_k16_against_oracle():
+    # 7B-shaped blocks [0, 16) at the bench length, where bf16 operands leave
+    # the boundary beyond 1e-2 of the fp32 model: prefill and decode step with
+    # split operands, the step at position L against row L of the oracle's
+    # prefill over L + 1 tokens
+    import torch
+    wl = synth.CONFIGS["sweep7b"]
+    s = wl.llm
+    L, k, B = 2048, 16, 1
+    W = [synth.llm_block_weights(wl, l) for l in range(k)]
+    ctx = vb.Context(llm=vb.stack_cfg(s, "bf16", max_tokens=L + 8, max_batch=B, n_blocks=k))
+    for l in range(k):
+        ctx.vla_load_block_weights(vb.VLA_STACK_LLM, l, W[l])
+    toks = synth.tokens(wl, frame=9, B=B, L=L + 1)
+    x = synth.as_f32(toks[:, L])
+    got = {}
+    for mode in (vb.VLA_PREC_SPLIT, vb.VLA_PREC_BF16):
+        ctx.vla_set_precision(vb.VLA_STACK_LLM, mode)
+        pre = vb.Boundary(B, L, s.d_model, k, s.n_kv_heads, s.head_dim, out_dtype="f32")
+        ctx.vla_run_prefix(10 + mode, np.ascontiguousarray(toks[:, :L]), B, L, k, pre)
+        ctx.vla_wait_boundary(10 + mode, 120000)
+        cache = torch.zeros((k, 2, B, s.n_kv_heads, L + 8, s.head_dim), dtype=torch.bfloat16, device="cuda")
+        cache[:, :, :, :, :L] = pre.kv.cuda()
+        ob = vb.Boundary(B, 1, s.d_model, 0, s.n_kv_heads, s.head_dim, out_dtype="f32", with_kv=False)
+        ctx.vla_decode_step(20 + mode, np.ascontiguousarray(toks[:, L]), B, L, k, cache, L + 8, ob)
+        ctx.vla_wait_boundary(20 + mode, 120000)
+        got[mode] = ob.hidden.numpy().reshape(B, s.d_model).copy()
+        del cache
+    Wf = [f32_weights(w) for w in W]
+    ref, _ = oracle.run_prefix(synth.as_f32(toks), lambda l: Wf[l], s, k, keep_kv=False)
+    e = rel_l2(got[vb.VLA_PREC_SPLIT] - x, ref[:, L] - x)
+    e16 = rel_l2(got[vb.VLA_PREC_BF16] - x, ref[:, L] - x)
+    log("7B-shaped decode at position %d, k=%d: update rel L2 vs the oracle %.2e split, %.2e bf16" % (L, k, e, e16))
+    assert e < 1e-2
 
 
 def test_decode_across_the_boundary():

@@ -21,12 +21,16 @@ def _context(shape, B, L_cap, k, name):
     return ctx
 
 
-def test_static_step_matches_workspace_step():
+@pytest.mark.parametrize("prec", ["bf16", "split"])
+def test_static_step_matches_workspace_step(prec):
     import torch
     shape = llama_like(2, 1024, 8, 2, 128, 2816)
     k, L, L_cap = 2, 300, 320
     d, Hkv, dh = shape.d_model, shape.n_kv_heads, shape.head_dim
     ctx = _context(shape, 3, L_cap, k, "noalloc")
+    if prec == "split":
+        # split operands: the gated activation's remainder rows also live in the fixed array
+        ctx.vla_set_precision(vb.VLA_STACK_LLM, vb.VLA_PREC_SPLIT)
     toks = synth.normal_bf16(synth.seed_of("noalloc", "tok"), (3, L + 1, d))
     bnd = vb.Boundary(3, L, d, k, Hkv, dh)
     ctx.vla_run_prefix(1, np.ascontiguousarray(toks[:, :L]), 3, L, k, bnd)
