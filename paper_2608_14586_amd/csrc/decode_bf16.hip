@@ -33,7 +33,12 @@
 //    device-scope counter, needs an L2 write-back per workgroup on this
 //    multi-XCD part and measured 3x slower than the extra launch.)
 // Rounding points follow the prefill: normed activations, q and K/V after
-// RoPE, the attention output and the gated activation are bf16.
+// RoPE, the attention output and the gated activation are bf16.  With split
+// operands each sequence's normed row and gated activation are staged twice,
+// as bf16(v) and bf16(v - bf16(v)), and the two dot products of a weight row
+// are added in fp32 (the weights still stream once).  The kernels take the
+// number of staged rows per sequence, P, and the largest row count, MB, as
+// template arguments.
 
 #include "kernels.h"
 
