@@ -714,6 +714,8 @@ def main():
     ap.add_argument("--pipeline", action="store_true",
                     help="measure the partitioned model (GPU prefix + host suffix) instead of the GPU prefix")
     ap.add_argument("--pipeline-ks", default="16,24,28,31,32")
+    ap.add_argument("--encoder-stream", action="store_true",
+                    help="run the encoder on a stream of its own, overlapping the previous frame's prefix")
     ap.add_argument("--decode-precision", choices=("bf16", "split"), default="bf16",
                     help="activation operands of the prefill and the decode steps (split: hi + lo bf16 pairs)")
     ap.add_argument("--decode", action="store_true",
@@ -790,7 +792,10 @@ def main():
     # (its arena plus whatever the runtime adds for its streams and events)
     torch.cuda.synchronize()
     free0 = torch.cuda.mem_get_info()[0]
-    ctx = vb.Context(llm=llm_cfg, enc=enc_cfg)
+    # --encoder-stream: the encoder of frame f+1 runs on a stream of its own,
+    # beside the prefix of frame f (the default keeps one compute stream)
+    ctx = vb.Context(llm=llm_cfg, enc=enc_cfg,
+                     encoder_stream=torch.cuda.Stream() if args.encoder_stream else None)
     torch.cuda.synchronize()
     mem_delta = free0 - torch.cuda.mem_get_info()[0]
     log("arena %.2f GiB, hipMemGetInfo delta %.2f GiB" % (ctx.arena_bytes / 2 ** 30, mem_delta / 2 ** 30))
