@@ -78,6 +78,32 @@ def test_vit_l_full():
     c.close()
 
 
+def test_wide_tiles_with_ragged_rows():
+    """The 8-wave tiles that fill whole rounds also take row counts that are
+    not multiples of their height: 7B-shaped blocks at L=2000 (QKV in 256x192
+    tiles, gate/up in 256x256, the last row tile 208 rows tall) and ViT-L
+    blocks over 6 x 1000 patches (QKV in 192x384, fc1 in 192x256 tiles, the
+    last 48 rows tall, tiles straddling images).  Two blocks each against the
+    oracle, boundary and every KV layer within 1e-2."""
+    c = LlmCase("llm7b", 2000, 2, perturbed=True)
+    tok = c.tokens(frame=3)
+    bnd = c.run(tok, frame=0)
+    ref, kv = c.oracle(tok)
+    e_h = rel_l2(to_f32(bnd.hidden), ref)
+    e_kv = [rel_l2(to_f32(bnd.kv[l]), kv[l]) for l in range(2)]
+    log("  llm7b L=2000 k=2: boundary %.2e, kv max %.2e" % (e_h, max(e_kv)))
+    assert e_h <= 1e-2 and max(e_kv) <= 1e-2
+    c.close()
+    e = EncCase("vit_l", 6, 1000, n_blocks=2, perturbed=True)
+    p = e.patches(frame=3)
+    got = to_f32(e.run(p))
+    ref = e.oracle(p)
+    err = rel_l2(got, ref)
+    log("  vit_l 6x1000, 2 blocks: %.2e" % err)
+    assert err <= 1e-2
+    e.close()
+
+
 def _per_block(c, blocks, tok):
     """Chain the GPU block by block through bf16 boundaries; each block is
     compared with the oracle's block on the very same bf16 input."""
