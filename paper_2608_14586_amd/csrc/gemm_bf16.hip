@@ -76,13 +76,6 @@ __device__ __forceinline__ float gelu_as(float z) {
   return z * (z >= 0.f ? 1.f - h : h);
 }
 
-// largest divisor of n that is at most 16
-constexpr int batch_of(int n) {
-  int b = n < 16 ? n : 16;
-  while (n % b) --b;
-  return b;
-}
-
 // silu(g) = g / (1 + e^-g), the division by the hardware reciprocal (1 ulp),
 // as in the GELU: an IEEE divide costs ten VALU instructions per element of
 // an epilogue that no MFMA work overlaps.  Large negative g: e^-g overflows
@@ -90,7 +83,7 @@ constexpr int batch_of(int n) {
 __device__ __forceinline__ float silu(float g) { return g * __builtin_amdgcn_rcpf(1.f + __expf(-g)); }
 
 struct EpiStoreF32 {
-  static constexpr bool kViaLds = false, kBig = true;
+  static constexpr bool kViaLds = false, kBig = true, kPre = false;
   float* C;
   int ldc, M, N;
   template <int TM, int TN>
@@ -112,13 +105,15 @@ struct EpiStoreF32 {
   __device__ void drain(const float*, int, int, int) const {}
 };
 
-// C (bf16) = acc + bias, or gelu(acc + bias) when GELU.
+// C (bf16) = acc + bias, or gelu(acc + bias) when GELU (the bias is added to
+// the accumulators before the tile is parked).
 template <bool GELU>
 struct EpiBF16 {
-  static constexpr bool kViaLds = true, kBig = true;
+  static constexpr bool kViaLds = true, kBig = true, kPre = false;
   bf16_t* C;
   const float* bias;
   int ldc, M, N;
+  __device__ __forceinline__ const float* park_bias() const { return bias; }
   __device__ __forceinline__ float op(float z) const { return GELU ? gelu_as(z) : z; }
   template <int TM, int TN>
   __device__ void operator()(const Acc<TM, TN>&, int, int, int) const {}  // LDS path only
@@ -130,20 +125,11 @@ struct EpiBF16 {
     // a thread's columns are the same in every chunk it drains
     const int c8 = (tid % CH) * 8, gc = n0 + c8;
     if (gc >= N) return;
-    f32x4 b0 = {0.f, 0.f, 0.f, 0.f}, b1 = b0;
-    if (bias) {
-      b0 = ld4(bias + gc);
-      b1 = ld4(bias + gc + 4);
-    }
 #pragma unroll 4
     for (int j = 0; j < R * CH / 256; ++j) {
       const int row = (tid + 256 * j) / CH, gr = m0 + row;
       if (gr >= M) continue;
       f32x4 x0 = ld4(T + row * NC + c8), x1 = ld4(T + row * NC + c8 + 4);
-      if (bias) {
-        x0 += b0;
-        x1 += b1;
-      }
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         x0[e] = op(x0[e]);
@@ -156,38 +142,48 @@ struct EpiBF16 {
 using EpiStoreBF16 = EpiBF16<false>;
 using EpiGelu = EpiBF16<true>;
 
-// H (fp32 residual) += acc + bias.
+// H (fp32 residual) += acc + bias (the bias added to the accumulators before
+// the tile is parked).  The residual tile is read into registers during the
+// last slab's MFMAs (prefetch), so its load latency is off the epilogue's
+// path.
 struct EpiResidual {
-  static constexpr bool kViaLds = true, kBig = false;
+  static constexpr bool kViaLds = true, kBig = false, kPre = true;
   float* H;
   const float* bias;
   int ldh, M, N;
+  __device__ __forceinline__ const float* park_bias() const { return bias; }
+  template <int R, int NC>
+  struct Pre {
+    f32x4 v[R * (NC / 4) / 256];
+  };
   template <int TM, int TN>
   __device__ void operator()(const Acc<TM, TN>&, int, int, int) const {}  // LDS path only
   template <int R, int NC>
-  __device__ void drain(const float* T, int m0, int n0, int tid) const {
-    // R rows x NC/4 float4, in batches of 16 per thread with every residual
-    // load of a batch issued before its first add
-    constexpr int CH = NC / 4, NJ = R * CH / 256, NB = batch_of(NJ);
-    static_assert((R * CH) % 256 == 0 && NJ % NB == 0, "tile must split evenly over the workgroup");
+  __device__ void prefetch(Pre<R, NC>& pre, int m0, int n0, int tid) const {
+    // one buffer resource over the R rows from m0 (rows past M read as zero)
+    // and one lane offset; the rows step by a scalar offset, so nothing but
+    // the loaded values stays live across the last slab
+    constexpr int CH = NC / 4, NJ = R * CH / 256, RS = 256 / CH;
+    static_assert((R * CH) % 256 == 0 && 256 % CH == 0, "tile must split evenly over the workgroup");
+    const int rows = min(max(M - m0, 0), R);
+    const __amdgpu_buffer_rsrc_t rh = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(H + (size_t)min(m0, M) * ldh), (short)0, rows * ldh * 4, 0x00020000);
+    const int gc = n0 + (tid % CH) * 4;
+    const int voff = ((tid / CH) * ldh + gc) * 4;
 #pragma unroll
-    for (int j0 = 0; j0 < NJ; j0 += NB) {
-      f32x4 hv[NB];
+    for (int j = 0; j < NJ; ++j)
+      pre.v[j] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rh, voff, j * RS * ldh * 4, 0));
+  }
+  template <int R, int NC>
+  __device__ void drain(const float* T, int m0, int n0, int tid, const Pre<R, NC>& pre) const {
+    constexpr int CH = NC / 4, NJ = R * CH / 256;
+    const int gc = n0 + (tid % CH) * 4;
+    if (gc >= N) return;
 #pragma unroll
-      for (int j = 0; j < NB; ++j) {
-        const int f = tid + 256 * (j0 + j), row = f / CH, c4 = (f % CH) * 4;
-        const int gr = m0 + row, gc = n0 + c4;
-        hv[j] = (gr < M && gc < N) ? ld4(H + (size_t)gr * ldh + gc) : f32x4{0.f, 0.f, 0.f, 0.f};
-      }
-#pragma unroll
-      for (int j = 0; j < NB; ++j) {
-        const int f = tid + 256 * (j0 + j), row = f / CH, c4 = (f % CH) * 4;
-        const int gr = m0 + row, gc = n0 + c4;
-        if (gr >= M || gc >= N) continue;
-        f32x4 x = ld4(T + row * NC + c4);
-        if (bias) x += ld4(bias + gc);
-        *(f32x4*)(H + (size_t)gr * ldh + gc) = hv[j] + x;
-      }
+    for (int j = 0; j < NJ; ++j) {
+      const int row = (tid + 256 * j) / CH, gr = m0 + row;
+      if (gr >= M) continue;
+      *(f32x4*)(H + (size_t)gr * ldh + gc) = pre.v[j] + ld4(T + row * NC + (tid % CH) * 4);
     }
   }
 };
@@ -197,7 +193,8 @@ struct EpiResidual {
 // bf16(y - bf16(y)) at column lo + c, so that hi + lo carries y to 16
 // significant bits into the down projection.
 struct EpiSwiGLU {
-  static constexpr bool kViaLds = true, kBig = true;
+  static constexpr bool kViaLds = true, kBig = true, kPre = false;
+  __device__ __forceinline__ const float* park_bias() const { return nullptr; }
   bf16_t* out;
   int ldo, M, N, lo;
   template <int TM, int TN>
@@ -233,9 +230,10 @@ struct EpiSwiGLU {
 // holds 32 first-half dims and their 32 second-half partners, see QkvArgs),
 // scatter to q / K / V rows and to V^T.
 struct EpiQKV {
-  static constexpr bool kViaLds = true, kBig = false;
+  static constexpr bool kViaLds = true, kBig = false, kPre = false;
   QkvArgs q;
   int M;
+  __device__ __forceinline__ const float* park_bias() const { return q.bias; }
   // column group p (multiple of 64) -> kind (0 q, 1 k, 2 v, 3 none), head, dim offset
   __device__ __forceinline__ void classify(int p, int& kind, int& head, int& r) const {
     const int dh = q.dh;
@@ -269,12 +267,6 @@ struct EpiQKV {
       const int d1 = c * 32 + w, d2 = dh / 2 + c * 32 + w;
       const float* tr = T + row * NC + gsel * 64 + w;
       f32x4 x10 = ld4(tr), x11 = ld4(tr + 4), x20 = ld4(tr + 32), x21 = ld4(tr + 36);
-      if (q.bias) {
-        x10 += ld4(q.bias + p + w);
-        x11 += ld4(q.bias + p + w + 4);
-        x20 += ld4(q.bias + p + 32 + w);
-        x21 += ld4(q.bias + p + 36 + w);
-      }
       const int b = gr / L, pos = gr - b * L;
       if (kind < 2 && q.rope_cos) {
         const float* cp = q.rope_cos + (size_t)pos * (dh / 2) + d1;
@@ -306,10 +298,9 @@ struct EpiQKV {
         const int gr0 = m0 + t16;
         if (gr0 >= M) continue;
         const int d = (col < 32) ? c * 32 + col : dh / 2 + c * 32 + (col - 32);
-        const float bcol = q.bias ? q.bias[p + col] : 0.f;
         float v[16];
 #pragma unroll
-        for (int e = 0; e < 16; ++e) v[e] = T[(t16 + e) * NC + gsel * 64 + col] + bcol;
+        for (int e = 0; e < 16; ++e) v[e] = T[(t16 + e) * NC + gsel * 64 + col];
         const int b0 = gr0 / L, pos0 = gr0 - b0 * L;
         bf16_t* row = q.vt + (((size_t)b0 * q.Hkv + head) * dh + d) * q.ldvt;
         if (gr0 + 15 < M && pos0 + 15 < L && (pos0 & 15) == 0 && (q.ldvt & 15) == 0) {
@@ -340,6 +331,16 @@ struct EpiQKV {
 // ((row >> 1) & 7): each 16-lane phase of a fragment read covers all banks.
 // Buffer resources clamp ragged M / N tiles: rows past the end read as zero.
 // MFMA fragments are double buffered across the four k16 steps of a slab.
+
+// the epilogue's prefetched registers, or nothing
+template <class Epi, int R, int NC, bool = Epi::kPre>
+struct PreOf {
+  struct type {};
+};
+template <class Epi, int R, int NC>
+struct PreOf<Epi, R, NC, true> {
+  using type = typename Epi::template Pre<R, NC>;
+};
 
 __device__ __forceinline__ void buffer_load_lds16(__amdgpu_buffer_rsrc_t r, void* lds, unsigned voff) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, voff, 0, 0, 0);
@@ -432,14 +433,17 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __
     for (int tn = 0; tn < TN; ++tn) fb[slot][tn] = *(const bf16x8*)(base + b_row0 + tn * 32 * ROWB + off);
   };
 
+  constexpr int GROUPS = NW / 4, RG = BM / 2 / GROUPS;
+  const int grp = tid >> 8, t = tid & 255;
+  typename PreOf<Epi, RG, BN>::type pre[2];
+
   const int nk = K / BK;
   issue(0, 0);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   frags(0, 0, 0);
-  for (int kt = 0; kt < nk; ++kt) {
-    // the other buffer was last read before the previous slab's barrier
-    if (kt + 1 < nk) issue((kt + 1) * BK, (kt + 1) & 1);
+  // the MFMAs of slab kt (fragments of its first k16 step already loaded)
+  auto slab = [&](int kt) {
 #pragma unroll
     for (int ks = 0; ks < BK / 16; ++ks) {
       const int cur = ks & 1;
@@ -454,14 +458,45 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __
           acc.v[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cur][tm], fb[cur][tn], acc.v[tm][tn], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
-    if (kt + 1 < nk) {
-      // the next slab's loads; this wave's fragment reads are consumed
-      __builtin_amdgcn_s_waitcnt(0x0F70);
-      __syncthreads();
-      frags(kt + 1, 0, 0);
+  };
+  for (int kt = 0; kt + 1 < nk; ++kt) {
+    // the other buffer was last read before the previous slab's barrier
+    issue((kt + 1) * BK, (kt + 1) & 1);
+    slab(kt);
+    // the next slab's loads; this wave's fragment reads are consumed
+    __builtin_amdgcn_s_waitcnt(0x0F70);
+    __syncthreads();
+    frags(kt + 1, 0, 0);
+  }
+  // the last slab, peeled so that loads issued behind it are straight-line
+  // code the compiler's wait counting can follow
+  if constexpr (Epi::kPre) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) epi.template prefetch<RG, BN>(pre[h], m0 + h * (BM / 2) + grp * RG, n0, t);
+  }
+  // the bias of this lane's accumulator columns, added before the tile is parked
+  float pb[TN];
+  const float* bias = nullptr;
+  if constexpr (Epi::kViaLds) {
+    bias = epi.park_bias();
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) {
+      const int col = n0 + wn * WN + tn * 32 + (lane & 31);
+      pb[tn] = (bias && col < N) ? bias[col] : 0.f;
     }
   }
+  slab(nk - 1);
   __builtin_amdgcn_s_waitcnt(0);
+  if constexpr (Epi::kViaLds) {
+    if (bias) {
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc.v[tm][tn][r] += pb[tn];
+    }
+  }
 
   if constexpr (Epi::kViaLds) {
     // Park one wave row (BM/2 x BN fp32) at a time in the idle slab buffers;
@@ -469,9 +504,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __
     constexpr int WR = BM / WM, HR = WR / 2;  // wave rows, parked per half
     static_assert(WR % 2 == 0, "an even number of wave rows");
     static_assert((BM / 2) * BN * 4 <= sizeof(smem), "half tile must fit the slab buffers");
-    constexpr int GROUPS = NW / 4, RG = BM / 2 / GROUPS;
     float* T = (float*)smem;
-    const int grp = tid >> 8, t = tid & 255;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       __syncthreads();
@@ -486,7 +519,10 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __
               T[(r0 + tm * 32 + acc_row(r, lane)) * BN + wn * WN + tn * 32 + (lane & 31)] = acc.v[tm][tn][r];
       }
       __syncthreads();
-      epi.template drain<RG, BN>(T + grp * RG * BN, m0 + h * (BM / 2) + grp * RG, n0, t);
+      if constexpr (Epi::kPre)
+        epi.template drain<RG, BN>(T + grp * RG * BN, m0 + h * (BM / 2) + grp * RG, n0, t, pre[h]);
+      else
+        epi.template drain<RG, BN>(T + grp * RG * BN, m0 + h * (BM / 2) + grp * RG, n0, t);
     }
   } else {
     epi(acc, m0 + wm * WM, n0 + wn * WN, lane);
@@ -575,7 +611,8 @@ hipError_t gemm_bf16_store_f32(const bf16_t* A, int lda, const bf16_t* W, int ld
 
 hipError_t gemm_bf16_residual(const bf16_t* A, int lda, const WOperand& W, float* H, int ldh, const float* bias, int M,
                               int N, int K, hipStream_t s, int a_parts) {
-  if (N % 4 || ldh % 4) return hipErrorInvalidValue;
+  // the residual prefetch addresses a half tile's rows with 32-bit byte offsets
+  if (N % 4 || ldh % 4 || (size_t)256 * ldh * 4 >= (1u << 31)) return hipErrorInvalidValue;
   return launch<true>(A, lda, W, M, N, K, EpiResidual{H, bias, ldh, M, N}, s, a_parts);
 }
 
