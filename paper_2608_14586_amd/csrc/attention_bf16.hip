@@ -79,7 +79,9 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const bf16_t* __restrict
   __shared__ __attribute__((aligned(1024))) char sm1[STAGE];
   __shared__ __attribute__((aligned(1024))) char sm2[NS > 2 ? STAGE : 16];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // the wave index is uniform: from a scalar register, the DMA destinations
+  // (M0) are scalar arithmetic and take no VGPRs
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int half = lane >> 5, li = lane & 31;
   const int nqb = (L + BQ - 1) / BQ;
   const int id = blockIdx.x;
