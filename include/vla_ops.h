@@ -31,6 +31,33 @@ vla_status vla_op_gemm_bf16(const void *A, const void *W, float *C, int M, int N
 vla_status vla_op_attention_bf16(const void *q, const void *k, const void *vt, int ldvt, void *o, int B, int H,
                                  int Hkv, int L, int dh, int causal, void *stream);
 
+/* The fused-epilogue products below take their weights packed slab-major,
+ * the layout the resident block weights use: W[N][K] (bf16 rows) cut into
+ * slabs of 128 rows x 64 k, each one contiguous block,
+ *   element (n, k) at ((k / 64 * nblk + n / 128) * 128 + n % 128) * 64 + k % 64,
+ * nblk = N rounded up to a multiple of 256, divided by 128 (pad rows zero).
+ * vla_op_packed_weight_elems gives the element count (0 for a shape the
+ * products reject: N <= 0, K <= 0, K % 64 != 0);
+ * vla_op_pack_weight_bf16 packs HOST row-major W into HOST memory Wp of
+ * that many elements (no GPU work). */
+size_t vla_op_packed_weight_elems(int N, int K);
+vla_status vla_op_pack_weight_bf16(const void *W, void *Wp, int N, int K);
+
+/* H[M][N] (fp32, in place) += A[M][K] (bf16) * W^T + bias[N] (fp32, NULL =
+ * none), Wp packed as above: the residual products of the blocks (output
+ * projection, down / fc2).  The residual tile is read behind the last K slab
+ * and the bias joins the accumulators before the epilogue.  N % 4 == 0,
+ * K % 64 == 0. */
+vla_status vla_op_gemm_residual_bf16(const void *A, const void *Wp, float *H, const float *bias, int M, int N, int K,
+                                     void *stream);
+
+/* out[M][N] (bf16) = f(A[M][K] * W^T + bias[N]), Wp packed as above, bias
+ * fp32 or NULL, f = the exact GELU z * Phi(z) (erfc by Abramowitz & Stegun
+ * 7.1.26, |error| <= 1.5e-7) when `gelu`, else the identity: the ViT fc1
+ * product and the plain bias product.  N % 8 == 0, K % 64 == 0. */
+vla_status vla_op_gemm_bias_bf16(const void *A, const void *Wp, void *out, const float *bias, int M, int N, int K,
+                                 int gelu, void *stream);
+
 /* y[M][d] (bf16) = RMSNorm(x[M][d] fp32; gain g[d] fp32, eps) -- or
  * LayerNorm with shift b[d] when b != NULL.  d % 4 == 0, d <= 8192. */
 vla_status vla_op_norm_bf16(const float *x, const float *g, const float *b, float eps, void *y, int M, int d,

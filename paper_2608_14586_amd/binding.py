@@ -106,6 +106,9 @@ def lib():
             "vla_op_attention_bf16": [c_void_p, c_void_p, c_void_p, c_int, c_void_p, c_int, c_int, c_int, c_int,
                                       c_int, c_int, c_void_p],
             "vla_op_norm_bf16": [c_void_p, c_void_p, c_void_p, c_float, c_void_p, c_int, c_int, c_void_p],
+            "vla_op_pack_weight_bf16": [c_void_p, c_void_p, c_int, c_int],
+            "vla_op_gemm_residual_bf16": [c_void_p, c_void_p, c_void_p, c_void_p, c_int, c_int, c_int, c_void_p],
+            "vla_op_gemm_bias_bf16": [c_void_p, c_void_p, c_void_p, c_void_p, c_int, c_int, c_int, c_int, c_void_p],
             "vla_suffix_create": [P(vla_stack_cfg), c_int, c_int, c_int, P(c_void_p)],
             "vla_suffix_load_block_weights": [c_void_p, c_int, P(vla_block_weights)],
             "vla_suffix_run": [c_void_p, c_void_p, c_int, c_int, c_int, c_void_p],
@@ -127,6 +130,8 @@ def lib():
             fn = getattr(L, name)
             fn.argtypes = args
             fn.restype = c_int
+        L.vla_op_packed_weight_elems.argtypes = [c_int, c_int]
+        L.vla_op_packed_weight_elems.restype = c_size_t
         L.vla_status_string.argtypes = [c_int]
         L.vla_status_string.restype = c_char_p
         L.vla_last_error.argtypes = [c_void_p]
@@ -354,6 +359,26 @@ def vla_op_attention_bf16(q, k, vt, ldvt, o, B, H, Hkv, L, dh, causal, stream=No
 
 def vla_op_norm_bf16(x, g, b, eps, y, M, d, stream=None):
     _check(lib().vla_op_norm_bf16(_ptr(x), _ptr(g), _ptr(b), eps, _ptr(y), M, d, stream))
+
+
+def vla_op_packed_weight_elems(N, K):
+    return lib().vla_op_packed_weight_elems(N, K)
+
+
+def vla_op_pack_weight_bf16(W, N, K):
+    """Host row-major bf16 rows W[N][K] (uint16 array) -> the packed slab-major
+    host array the fused-epilogue products take."""
+    out = np.zeros(vla_op_packed_weight_elems(N, K), dtype=np.uint16)
+    _check(lib().vla_op_pack_weight_bf16(_ptr(np.ascontiguousarray(W)), _ptr(out), N, K))
+    return out
+
+
+def vla_op_gemm_residual_bf16(A, Wp, H, bias, M, N, K, stream=None):
+    _check(lib().vla_op_gemm_residual_bf16(_ptr(A), _ptr(Wp), _ptr(H), _ptr(bias), M, N, K, stream))
+
+
+def vla_op_gemm_bias_bf16(A, Wp, out, bias, M, N, K, gelu, stream=None):
+    _check(lib().vla_op_gemm_bias_bf16(_ptr(A), _ptr(Wp), _ptr(out), _ptr(bias), M, N, K, int(gelu), stream))
 
 
 def vla_status_string(code: int) -> str:

@@ -21,6 +21,16 @@ namespace vla {
 // the weights, rather than 128-byte pieces of rows 2*K bytes apart.
 constexpr int SLAB_N = 128;
 inline int slab_blocks(int N) { return (N + 2 * SLAB_N - 1) / (2 * SLAB_N) * 2; }
+// Host-side packing of row-major bf16 rows W[N][K] into that layout
+// (dst: slab_blocks(N) * SLAB_N * K elements, pad rows zero).  K % 64 == 0.
+inline void pack_slabs(const uint16_t* W, uint16_t* dst, int N, int K) {
+  const int nblk = slab_blocks(N);
+  for (size_t i = 0; i < (size_t)nblk * SLAB_N * K; ++i) dst[i] = 0;
+  for (int kt = 0; kt < K / 64; ++kt)
+    for (int n = 0; n < N; ++n)
+      for (int j = 0; j < 64; ++j)
+        dst[(((size_t)kt * nblk + n / SLAB_N) * SLAB_N + n % SLAB_N) * 64 + j] = W[(size_t)n * K + (size_t)kt * 64 + j];
+}
 
 // A weight operand: packed (nblk > 0, ld unused) or row-major with leading
 // dimension ld (nblk == 0).

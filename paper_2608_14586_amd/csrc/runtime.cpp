@@ -416,12 +416,8 @@ Status copy_h2d(void* dst, const void* src, size_t bytes) {
 // stacks (the layout the GEMMs read, kernels.h), as-is for fp32 stacks.
 Status put_matrix(bool bf16, void* dst, const void* rm, int N, int K) {
   if (!bf16) return copy_h2d(dst, rm, (size_t)N * K * 4);
-  const int nblk = vla::slab_blocks(N), SN = vla::SLAB_N;
-  std::vector<uint16_t> t((size_t)nblk * SN * K, 0);
-  const uint16_t* src = (const uint16_t*)rm;
-  for (int kt = 0; kt < K / 64; ++kt)
-    for (int n = 0; n < N; ++n)
-      memcpy(&t[(((size_t)kt * nblk + n / SN) * SN + n % SN) * 64], src + (size_t)n * K + (size_t)kt * 64, 128);
+  std::vector<uint16_t> t((size_t)vla::slab_blocks(N) * vla::SLAB_N * K);
+  vla::pack_slabs((const uint16_t*)rm, t.data(), N, K);
   return copy_h2d(dst, t.data(), t.size() * 2);
 }
 

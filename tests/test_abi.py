@@ -156,3 +156,26 @@ def test_vision_needs_an_encoder_and_f32_relaxes_widths():
     with pytest.raises(vb.VlaError) as e:
         vb.vla_query_vision_sizes(None, v)
     assert e.value.name == "VLA_ERR_INVALID_ARG"
+
+
+def test_pack_weight_layout():
+    """The host packer puts element (n, k) of row-major W at the slab-major
+    position the header documents, pads rows to whole 256-row pairs with zeros
+    and rejects K % 64 != 0; no GPU work."""
+    import numpy as np
+    N, K = 300, 192
+    rng = np.random.default_rng(7)
+    W = rng.integers(1, 65535, size=(N, K), dtype=np.uint16)
+    nblk = (N + 255) // 256 * 2
+    assert vb.vla_op_packed_weight_elems(N, K) == nblk * 128 * K
+    assert vb.vla_op_packed_weight_elems(N, 100) == 0
+    P = vb.vla_op_pack_weight_bf16(W, N, K)
+    n, k = np.meshgrid(np.arange(N), np.arange(K), indexing="ij")
+    pos = ((k // 64 * nblk + n // 128) * 128 + n % 128) * 64 + k % 64
+    assert np.array_equal(P[pos], W)
+    mask = np.ones(P.size, dtype=bool)
+    mask[pos.ravel()] = False
+    assert not P[mask].any()
+    with pytest.raises(vb.VlaError) as e:
+        vb.vla_op_pack_weight_bf16(np.zeros((4, 128), np.uint16), 4, 100)
+    assert e.value.name == "VLA_ERR_UNSUPPORTED"

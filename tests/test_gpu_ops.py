@@ -32,6 +32,77 @@ def test_gemm_bf16(M, N, K):
     assert err < 1e-5, err
 
 
+def _packed(W, N, K):
+    from paper_2608_14586_amd import binding as vb
+    return _dev_bf16(vb.vla_op_pack_weight_bf16(W, N, K))
+
+
+# Tile choices these shapes reach: 128x128 over 384 tiles (ViT proj / fc2),
+# one round of 128x128 (decoder O-projection / down at L=2048), 64x128 (half
+# a round of 128x128), ragged rows and columns, single rows.
+@pytest.mark.parametrize("M,N,K,bias", [(6144, 1024, 128, True), (2048, 4096, 192, False), (1024, 4096, 128, False),
+                                        (6104, 1000, 192, True), (77, 96, 64, True), (1, 4, 64, True),
+                                        (130, 8, 128, False)])
+def test_gemm_residual_bf16(M, N, K, bias):
+    """H += A W^T + b through the fused residual epilogue (the residual tile
+    read behind the last K slab, the bias added before the park): element-wise
+    against float64, to the fp32 accumulation error."""
+    import torch
+    from paper_2608_14586_amd import binding as vb
+    A = synth.normal_bf16(synth.seed_of("resA", M, N, K), (M, K))
+    W = synth.normal_bf16(synth.seed_of("resW", M, N, K), (N, K))
+    H0 = synth.normal_f32(synth.seed_of("resH", M, N, K), (M, N))
+    b = synth.normal_f32(synth.seed_of("resb", M, N, K), (N,)) if bias else None
+    H = torch.from_numpy(H0.copy()).cuda()
+    vb.vla_op_gemm_residual_bf16(_dev_bf16(A), _packed(W, N, K), H, None if b is None else torch.from_numpy(b).cuda(),
+                                 M, N, K)
+    torch.cuda.synchronize()
+    prod = synth.as_f32(A).astype(np.float64) @ synth.as_f32(W).astype(np.float64).T
+    ref = H0.astype(np.float64) + prod + (0.0 if b is None else b.astype(np.float64))
+    got = H.cpu().numpy().astype(np.float64)
+    # fp32 accumulation of K <= 192 exact bf16 products (at most K roundings,
+    # K 2^-24 <= 2^-16 of the sum of |products|) and three fp32 additions; a
+    # lost or doubled bias or residual is off by O(1)
+    mag = np.abs(synth.as_f32(A)).astype(np.float64) @ np.abs(synth.as_f32(W)).astype(np.float64).T
+    bound = 2.0 ** -16 * mag + 2.0 ** -22 * np.abs(ref) + 1e-30
+    err = np.abs(got - ref)
+    worst = np.unravel_index(np.argmax(err / bound), err.shape)
+    assert (err <= bound).all(), (worst, err[worst], bound[worst])
+
+
+# 192x256 tiles with 8 waves in whole rounds (ViT fc1), the same over ragged
+# rows, 256x256 tiles (two rounds and more), 64x128 tiles, single rows.
+@pytest.mark.parametrize("M,N,K,bias,gelu", [(6144, 4096, 128, True, True), (6000, 4096, 64, True, True),
+                                             (2048, 16384, 64, True, False), (300, 1000, 128, True, True),
+                                             (77, 96, 64, False, False), (1, 8, 64, False, True)])
+def test_gemm_bias_gelu_bf16(M, N, K, bias, gelu):
+    """out = f(A W^T + b) in bf16 through the fused bias / GELU epilogues (the
+    bias added before the park): element-wise against float64 with the exact
+    GELU, to one bf16 rounding plus the fp32 accumulation and erfc errors."""
+    import torch
+    from paper_2608_14586_amd import binding as vb
+    A = synth.normal_bf16(synth.seed_of("geluA", M, N, K), (M, K))
+    W = synth.normal_bf16(synth.seed_of("geluW", M, N, K), (N, K), std=0.1)
+    b = synth.normal_f32(synth.seed_of("gelub", M, N, K), (N,)) if bias else None
+    out = torch.empty((M, N), dtype=torch.int16, device="cuda")
+    vb.vla_op_gemm_bias_bf16(_dev_bf16(A), _packed(W, N, K), out, None if b is None else torch.from_numpy(b).cuda(),
+                             M, N, K, gelu)
+    torch.cuda.synchronize()
+    z = synth.as_f32(A).astype(np.float64) @ synth.as_f32(W).astype(np.float64).T
+    if b is not None:
+        z = z + b.astype(np.float64)
+    ref = oracle.gelu_erf(z) if gelu else z
+    got = synth.as_f32(out.cpu().numpy().view(np.uint16)).astype(np.float64)
+    mag = np.abs(synth.as_f32(A)).astype(np.float64) @ np.abs(synth.as_f32(W)).astype(np.float64).T + np.abs(z)
+    # half a bf16 ulp of the result (2^-9, with a factor 2), the fp32
+    # accumulation of K <= 128 products through GELU's slope (<= 1.13), and
+    # the erfc approximation (|error| <= 1.5e-7 on Phi, times |z|)
+    bound = 2.0 ** -8 * np.abs(ref) + 2.0 ** -16 * mag + (2e-7 * np.abs(z) if gelu else 0.0) + 1e-30
+    err = np.abs(got - ref)
+    worst = np.unravel_index(np.argmax(err / bound), err.shape)
+    assert (err <= bound).all(), (worst, got[worst], ref[worst], bound[worst])
+
+
 @pytest.mark.parametrize("B,H,Hkv,L,dh,causal", [
     (1, 4, 4, 128, 128, True), (1, 4, 4, 200, 128, True), (2, 6, 2, 77, 64, True), (1, 14, 2, 300, 64, True),
     (3, 4, 4, 130, 64, False), (1, 2, 2, 1024, 64, False), (1, 2, 1, 513, 128, False),
