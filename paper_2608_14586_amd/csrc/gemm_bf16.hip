@@ -40,13 +40,15 @@ __device__ __forceinline__ int acc_row(int r, int lane) { return (r >> 2) * 8 + 
 //  * Direct: every lane writes its accumulators straight to memory (4-byte
 //    stores); used by the fp32-out operator.
 //  * Through LDS: once the K loop is done the slab buffers are free, so the
-//    waves park the fp32 tile in LDS row-major, one wave row (half the tile's
-//    rows) at a time, and 256-thread groups then walk it in 16-byte chunks:
-//    coalesced residual read-modify-writes, 16-byte bf16 stores, and the
-//    rotary embedding plus the q / K / V / V^T scatter done row-contiguously
-//    per head.
-// drain() is the second half of the LDS path: T is the tile [128][128] fp32,
-// (m0, n0) its origin, tid the thread index in the 256-thread workgroup.
+//    waves add the bias to their accumulators and park the fp32 tile in LDS
+//    row-major, half of the wave rows (half the tile's rows) at a time, and
+//    256-thread groups then walk it in 16-byte chunks: coalesced residual
+//    read-modify-writes (the residual tile read into registers behind the
+//    last K slab), 16-byte bf16 stores, and the rotary embedding plus the
+//    q / K / V / V^T scatter done row-contiguously per head.
+// drain<R, NC>() is the second half of the LDS path: T is an R x NC fp32
+// piece of the parked tile (row stride NC), (m0, n0) its origin, tid the
+// thread index in its 256-thread group.
 
 __device__ __forceinline__ u32x4 pack8(const f32x4& a, const f32x4& b) {
   return u32x4{pack_bf2(a[0], a[1]), pack_bf2(a[2], a[3]), pack_bf2(b[0], b[1]), pack_bf2(b[2], b[3])};
