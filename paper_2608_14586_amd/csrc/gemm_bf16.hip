@@ -39,6 +39,8 @@ __device__ __forceinline__ int acc_row(int r, int lane) { return (r >> 2) * 8 + 
 // Two epilogue paths.
 //  * Direct: every lane writes its accumulators straight to memory (4-byte
 //    stores); used by the fp32-out operator.
+//  * SwiGLU forms its activation in the accumulators (a wave's columns are
+//    whole (gate, up) groups) and parks only the activation, in one phase.
 //  * Through LDS: once the K loop is done the slab buffers are free, so the
 //    waves add the bias to their accumulators and park the fp32 tile in LDS
 //    row-major, half of the wave rows (half the tile's rows) at a time, and
@@ -85,7 +87,7 @@ __device__ __forceinline__ float gelu_as(float z) {
 __device__ __forceinline__ float silu(float g) { return g * __builtin_amdgcn_rcpf(1.f + __expf(-g)); }
 
 struct EpiStoreF32 {
-  static constexpr bool kViaLds = false, kBig = true, kPre = false;
+  static constexpr bool kViaLds = false, kBig = true, kPre = false, kActInRegs = false;
   float* C;
   int ldc, M, N;
   template <int TM, int TN>
@@ -111,7 +113,7 @@ struct EpiStoreF32 {
 // the accumulators before the tile is parked).
 template <bool GELU>
 struct EpiBF16 {
-  static constexpr bool kViaLds = true, kBig = true, kPre = false;
+  static constexpr bool kViaLds = true, kBig = true, kPre = false, kActInRegs = false;
   bf16_t* C;
   const float* bias;
   int ldc, M, N;
@@ -149,7 +151,7 @@ using EpiGelu = EpiBF16<true>;
 // last slab's MFMAs (prefetch), so its load latency is off the epilogue's
 // path.
 struct EpiResidual {
-  static constexpr bool kViaLds = true, kBig = false, kPre = true;
+  static constexpr bool kViaLds = true, kBig = false, kPre = true, kActInRegs = false;
   float* H;
   const float* bias;
   int ldh, M, N;
@@ -195,7 +197,10 @@ struct EpiResidual {
 // bf16(y - bf16(y)) at column lo + c, so that hi + lo carries y to 16
 // significant bits into the down projection.
 struct EpiSwiGLU {
-  static constexpr bool kViaLds = true, kBig = true, kPre = false;
+  // the activation is formed in the accumulators: a wave's 64 columns are
+  // one (gate, up) group, so a lane holds the gate and the up value of the
+  // same feature, and only the activation (half the columns) is parked
+  static constexpr bool kViaLds = true, kBig = true, kPre = false, kActInRegs = true;
   __device__ __forceinline__ const float* park_bias() const { return nullptr; }
   bf16_t* out;
   int ldo, M, N, lo;
@@ -226,13 +231,33 @@ struct EpiSwiGLU {
       if (lo) *(u32x4*)(dst + lo) = pack8(y0 - unpack_lo4(hi, 0), y1 - unpack_lo4(hi, 2));
     }
   }
+  // Y: R x NC fp32 activations (row stride NC) of the tile at (m0, feature
+  // n0 / 2); 256 threads, chunks of 8 features.
+  template <int R, int NC>
+  __device__ void drain_act(const float* Y, int m0, int n0, int tid) const {
+    constexpr int CH = NC / 8;
+    static_assert((R * CH) % 256 == 0 && 256 % CH == 0, "tile must split evenly over the workgroup");
+    // a thread's features are the same in every chunk it drains
+    const int c8 = (tid % CH) * 8, gc = (n0 >> 1) + c8;
+    if (2 * gc >= N) return;
+#pragma unroll 4
+    for (int j = 0; j < R * CH / 256; ++j) {
+      const int row = (tid + 256 * j) / CH, gr = m0 + row;
+      if (gr >= M) continue;
+      const f32x4 y0 = ld4(Y + row * NC + c8), y1 = ld4(Y + row * NC + c8 + 4);
+      bf16_t* dst = out + (size_t)gr * ldo + gc;
+      const u32x4 hi = pack8(y0, y1);
+      *(u32x4*)dst = hi;
+      if (lo) *(u32x4*)(dst + lo) = pack8(y0 - unpack_lo4(hi, 0), y1 - unpack_lo4(hi, 2));
+    }
+  }
 };
 
 // QKV projection: bias, rotary embedding of q and k (each 64-column group
 // holds 32 first-half dims and their 32 second-half partners, see QkvArgs),
 // scatter to q / K / V rows and to V^T.
 struct EpiQKV {
-  static constexpr bool kViaLds = true, kBig = false, kPre = false;
+  static constexpr bool kViaLds = true, kBig = false, kPre = false, kActInRegs = false;
   QkvArgs q;
   int M;
   __device__ __forceinline__ const float* park_bias() const { return q.bias; }
@@ -561,7 +586,25 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __
     }
   }
 
-  if constexpr (Epi::kViaLds) {
+  if constexpr (Epi::kActInRegs) {
+    // gate (tn even) and up (tn odd) of the same 32 features: park silu(g) u,
+    // BM x BN/2 fp32, in one phase
+    constexpr int YN = BN / 2, RY = BM / GROUPS;
+    static_assert(WN % 64 == 0, "a wave's columns must be whole (gate, up) groups");
+    static_assert(BM * YN * 4 <= sizeof(smem), "the activation tile must fit the slab buffers");
+    float* Y = (float*)smem;
+    __syncthreads();
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int tp = 0; tp < TN / 2; ++tp)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          Y[(wm * WM + tm * 32 + acc_row(r, lane)) * YN + wn * (WN / 2) + tp * 32 + (lane & 31)] =
+              silu(acc.v[tm][2 * tp][r]) * acc.v[tm][2 * tp + 1][r];
+    __syncthreads();
+    epi.template drain_act<RY, YN>(Y + grp * RY * YN, m0 + grp * RY, n0, t);
+  } else if constexpr (Epi::kViaLds) {
     // Park one wave row (BM/2 x BN fp32) at a time in the idle slab buffers;
     // 256-thread groups then drain BM/4 (8 waves) or BM/2 (4 waves) rows each.
     constexpr int WR = BM / WM, HR = WR / 2;  // wave rows, parked per half
