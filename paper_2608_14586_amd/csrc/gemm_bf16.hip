@@ -36,18 +36,19 @@ __device__ __forceinline__ int acc_row(int r, int lane) { return (r >> 2) * 8 + 
 
 // ------------------------------------------------------------------ epilogues
 //
-// Two epilogue paths.
+// Epilogue paths.
 //  * Direct: every lane writes its accumulators straight to memory (4-byte
 //    stores); used by the fp32-out operator.
 //  * SwiGLU forms its activation in the accumulators (a wave's columns are
 //    whole (gate, up) groups) and parks only the activation, in one phase.
+//  * The fp32 residual epilogue adds the residual in the accumulators and
+//    stores from them (EpiResidual).
 //  * Through LDS: once the K loop is done the slab buffers are free, so the
 //    waves add the bias to their accumulators and park the fp32 tile in LDS
 //    row-major, half of the wave rows (half the tile's rows) at a time, and
-//    256-thread groups then walk it in 16-byte chunks: coalesced residual
-//    read-modify-writes (the residual tile read into registers behind the
-//    last K slab), 16-byte bf16 stores, and the rotary embedding plus the
-//    q / K / V / V^T scatter done row-contiguously per head.
+//    256-thread groups then walk it in 16-byte chunks: 16-byte bf16 stores,
+//    and the rotary embedding plus the q / K / V / V^T scatter done
+//    row-contiguously per head.
 // drain<R, NC>() is the second half of the LDS path: T is an R x NC fp32
 // piece of the parked tile (row stride NC), (m0, n0) its origin, tid the
 // thread index in its 256-thread group.
@@ -87,7 +88,7 @@ __device__ __forceinline__ float gelu_as(float z) {
 __device__ __forceinline__ float silu(float g) { return g * __builtin_amdgcn_rcpf(1.f + __expf(-g)); }
 
 struct EpiStoreF32 {
-  static constexpr bool kViaLds = false, kBig = true, kPre = false, kActInRegs = false;
+  static constexpr bool kViaLds = false, kBig = true, kActInRegs = false, kDirect = false;
   float* C;
   int ldc, M, N;
   template <int TM, int TN>
@@ -105,15 +106,13 @@ struct EpiStoreF32 {
         }
       }
   }
-  template <int R, int NC>
-  __device__ void drain(const float*, int, int, int) const {}
 };
 
 // C (bf16) = acc + bias, or gelu(acc + bias) when GELU (the bias is added to
 // the accumulators before the tile is parked).
 template <bool GELU>
 struct EpiBF16 {
-  static constexpr bool kViaLds = true, kBig = true, kPre = false, kActInRegs = false;
+  static constexpr bool kViaLds = true, kBig = true, kActInRegs = false, kDirect = false;
   bf16_t* C;
   const float* bias;
   int ldc, M, N;
@@ -146,50 +145,62 @@ struct EpiBF16 {
 using EpiStoreBF16 = EpiBF16<false>;
 using EpiGelu = EpiBF16<true>;
 
-// H (fp32 residual) += acc + bias (the bias added to the accumulators before
-// the tile is parked).  The residual tile is read into registers during the
-// last slab's MFMAs (prefetch), so its load latency is off the epilogue's
-// path.
+// H (fp32 residual) += acc + bias, with no park: each lane loads the
+// residual of its accumulators behind the last K slab (the accumulator
+// layout: 32 columns per lane half-row), adds it (the bias is already in the
+// accumulators) and stores its values back.  4-byte accesses, whole 128-byte
+// rows per instruction; no LDS round trip and no barriers.
 struct EpiResidual {
-  static constexpr bool kViaLds = true, kBig = false, kPre = true, kActInRegs = false;
+  static constexpr bool kViaLds = true, kBig = false, kActInRegs = false, kDirect = true;
   float* H;
   const float* bias;
   int ldh, M, N;
   __device__ __forceinline__ const float* park_bias() const { return bias; }
-  template <int R, int NC>
-  struct Pre {
-    f32x4 v[R * (NC / 4) / 256];
-  };
-  template <int TM, int TN>
-  __device__ void operator()(const Acc<TM, TN>&, int, int, int) const {}  // LDS path only
-  template <int R, int NC>
-  __device__ void prefetch(Pre<R, NC>& pre, int m0, int n0, int tid) const {
-    // one buffer resource over the R rows from m0 (rows past M read as zero)
-    // and one lane offset; the rows step by a scalar offset, so nothing but
-    // the loaded values stays live across the last slab
-    constexpr int CH = NC / 4, NJ = R * CH / 256, RS = 256 / CH;
-    static_assert((R * CH) % 256 == 0 && 256 % CH == 0, "tile must split evenly over the workgroup");
-    const int rows = min(max(M - m0, 0), R);
-    const __amdgpu_buffer_rsrc_t rh = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(H + (size_t)min(m0, M) * ldh), (short)0, rows * ldh * 4, 0x00020000);
-    const int gc = n0 + (tid % CH) * 4;
-    const int voff = ((tid / CH) * ldh + gc) * 4;
-#pragma unroll
-    for (int j = 0; j < NJ; ++j)
-      pre.v[j] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rh, voff, j * RS * ldh * 4, 0));
+  // One buffer resource over the wave's rows from r0 (rows past M read as
+  // zero, stores to them are dropped), one lane offset; rows step by a scalar
+  // offset and 32-column blocks by the immediate offset.  The row count goes
+  // through readfirstlane: the clamp compiles to a vector med3, and a
+  // descriptor word in a VGPR would make every access a per-lane (waterfall)
+  // loop.
+  __device__ __forceinline__ __amdgpu_buffer_rsrc_t rows_from(int r0, int nrows) const {
+    const int rows = __builtin_amdgcn_readfirstlane(min(max(M - r0, 0), nrows));
+    return __builtin_amdgcn_make_buffer_rsrc((void*)(H + (size_t)min(r0, M) * ldh), (short)0, rows * ldh * 4,
+                                             0x00020000);
   }
-  template <int R, int NC>
-  __device__ void drain(const float* T, int m0, int n0, int tid, const Pre<R, NC>& pre) const {
-    constexpr int CH = NC / 4, NJ = R * CH / 256;
-    const int gc = n0 + (tid % CH) * 4;
-    if (gc >= N) return;
+  template <int TM, int TN>
+  __device__ void load_acc(f32x16 (&hv)[TM][TN], int r0, int c0, int lane) const {
+    const __amdgpu_buffer_rsrc_t rh = rows_from(r0, TM * 32);
+    const int voff = (((lane >> 5) * 4) * ldh + c0 + (lane & 31)) * 4;
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const int row = (tid + 256 * j) / CH, gr = m0 + row;
-      if (gr >= M) continue;
-      *(f32x4*)(H + (size_t)gr * ldh + gc) = pre.v[j] + ld4(T + row * NC + (tid % CH) * 4);
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          hv[tm][tn][r] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+              rh, voff + tn * 128, (tm * 32 + (r >> 2) * 8 + (r & 3)) * ldh * 4, 0));
+  }
+  template <int TM, int TN>
+  __device__ void store_acc(const f32x16 (&v)[TM][TN], int r0, int c0, int lane) const {
+    const __amdgpu_buffer_rsrc_t rh = rows_from(r0, TM * 32);
+    const int voff = (((lane >> 5) * 4) * ldh + c0 + (lane & 31)) * 4;
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) {
+      // columns past N would land in the next row: not stored
+      if (c0 + tn * 32 + (lane & 31) >= N) continue;
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          // through a scalar: clang's bit cast of a vector element reads element 0
+          const float x = v[tm][tn][r];
+          __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(x), rh, voff + tn * 128,
+                                                (tm * 32 + (r >> 2) * 8 + (r & 3)) * ldh * 4, 0);
+        }
     }
   }
+  template <int R, int NC>
+  __device__ void drain(const float*, int, int, int) const {}
 };
 
 // Pairs tiles (2p, 2p+1) = (gate, up) of the same 32 features: out[M][N/2].
@@ -200,7 +211,7 @@ struct EpiSwiGLU {
   // the activation is formed in the accumulators: a wave's 64 columns are
   // one (gate, up) group, so a lane holds the gate and the up value of the
   // same feature, and only the activation (half the columns) is parked
-  static constexpr bool kViaLds = true, kBig = true, kPre = false, kActInRegs = true;
+  static constexpr bool kViaLds = true, kBig = true, kActInRegs = true, kDirect = false;
   __device__ __forceinline__ const float* park_bias() const { return nullptr; }
   bf16_t* out;
   int ldo, M, N, lo;
@@ -257,7 +268,7 @@ struct EpiSwiGLU {
 // holds 32 first-half dims and their 32 second-half partners, see QkvArgs),
 // scatter to q / K / V rows and to V^T.
 struct EpiQKV {
-  static constexpr bool kViaLds = true, kBig = false, kPre = false, kActInRegs = false;
+  static constexpr bool kViaLds = true, kBig = false, kActInRegs = false, kDirect = false;
   QkvArgs q;
   int M;
   __device__ __forceinline__ const float* park_bias() const { return q.bias; }
@@ -373,16 +384,6 @@ struct EpiQKV {
 template <class Epi>
 constexpr bool scalar_wave = !std::is_same<Epi, EpiQKV>::value && !std::is_same<Epi, EpiGelu>::value;
 
-// the epilogue's prefetched registers, or nothing
-template <class Epi, int R, int NC, bool = Epi::kPre>
-struct PreOf {
-  struct type {};
-};
-template <class Epi, int R, int NC>
-struct PreOf<Epi, R, NC, true> {
-  using type = typename Epi::template Pre<R, NC>;
-};
-
 __device__ __forceinline__ void buffer_load_lds16(__amdgpu_buffer_rsrc_t r, void* lds, unsigned voff) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, voff, 0, 0, 0);
 }
@@ -492,8 +493,8 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __
   };
 
   constexpr int GROUPS = NW / 4, RG = BM / 2 / GROUPS;
-  const int grp = tid >> 8, t = tid & 255;
-  typename PreOf<Epi, RG, BN>::type pre[2];
+  // the 256-thread group (0 in a 4-wave workgroup)
+  const int grp = NW > 4 ? tid >> 8 : 0, t = tid & 255;
 
   const int nk = K / BK;
   // the MFMAs of slab kt (W slot ws; fragments of its first k16 step already loaded)
@@ -558,10 +559,9 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __
   }
   // the last slab, peeled so that loads issued behind it are straight-line
   // code the compiler's wait counting can follow
-  if constexpr (Epi::kPre) {
-#pragma unroll
-    for (int h = 0; h < 2; ++h) epi.template prefetch<RG, BN>(pre[h], m0 + h * (BM / 2) + grp * RG, n0, t);
-  }
+  // the direct epilogue's residual, read behind the last slab's MFMAs
+  f32x16 hv[Epi::kDirect ? TM : 1][Epi::kDirect ? TN : 1];
+  if constexpr (Epi::kDirect) epi.template load_acc<TM, TN>(hv, m0 + wm * WM, n0 + wn * WN, lane);
   // the bias of this lane's accumulator columns, added before the tile is parked
   float pb[TN];
   const float* bias = nullptr;
@@ -586,7 +586,16 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __
     }
   }
 
-  if constexpr (Epi::kActInRegs) {
+  if constexpr (Epi::kDirect) {
+    // residual added in the accumulators and stored from them: no park
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc.v[tm][tn][r] = hv[tm][tn][r] + acc.v[tm][tn][r];
+    epi.template store_acc<TM, TN>(acc.v, m0 + wm * WM, n0 + wn * WN, lane);
+  } else if constexpr (Epi::kActInRegs) {
     // gate (tn even) and up (tn odd) of the same 32 features: park silu(g) u,
     // BM x BN/2 fp32, in one phase
     constexpr int YN = BN / 2, RY = BM / GROUPS;
@@ -625,10 +634,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __
               T[(r0 + tm * 32 + acc_row(r, lane)) * BN + wn * WN + tn * 32 + (lane & 31)] = acc.v[tm][tn][r];
       }
       __syncthreads();
-      if constexpr (Epi::kPre)
-        epi.template drain<RG, BN>(T + grp * RG * BN, m0 + h * (BM / 2) + grp * RG, n0, t, pre[h]);
-      else
-        epi.template drain<RG, BN>(T + grp * RG * BN, m0 + h * (BM / 2) + grp * RG, n0, t);
+      epi.template drain<RG, BN>(T + grp * RG * BN, m0 + h * (BM / 2) + grp * RG, n0, t);
     }
   } else {
     epi(acc, m0 + wm * WM, n0 + wn * WN, lane);
@@ -720,7 +726,7 @@ hipError_t gemm_bf16_store_f32(const bf16_t* A, int lda, const bf16_t* W, int ld
 
 hipError_t gemm_bf16_residual(const bf16_t* A, int lda, const WOperand& W, float* H, int ldh, const float* bias, int M,
                               int N, int K, hipStream_t s, int a_parts) {
-  // the residual prefetch addresses a half tile's rows with 32-bit byte offsets
+  // the residual epilogue addresses a wave's rows with 32-bit byte offsets
   if (N % 4 || ldh % 4 || (size_t)256 * ldh * 4 >= (1u << 31)) return hipErrorInvalidValue;
   return launch<true>(A, lda, W, M, N, K, EpiResidual{H, bias, ldh, M, N}, s, a_parts);
 }
