@@ -45,9 +45,9 @@ vla_status vla_op_pack_weight_bf16(const void *W, void *Wp, int N, int K);
 
 /* H[M][N] (fp32, in place) += A[M][K] (bf16) * W^T + bias[N] (fp32, NULL =
  * none), Wp packed as above: the residual products of the blocks (output
- * projection, down / fc2).  The residual tile is read behind the last K slab
- * and the bias joins the accumulators before the epilogue.  N % 4 == 0,
- * K % 64 == 0. */
+ * projection, down / fc2).  Each lane reads the residual of its accumulators
+ * behind the last K slab; bias and residual are added in the accumulators
+ * and the sums stored from them.  N % 4 == 0, K % 64 == 0. */
 vla_status vla_op_gemm_residual_bf16(const void *A, const void *Wp, float *H, const float *bias, int M, int N, int K,
                                      void *stream);
 
