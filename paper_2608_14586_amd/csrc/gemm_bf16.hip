@@ -497,22 +497,30 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __
   const int grp = NW > 4 ? tid >> 8 : 0, t = tid & 255;
 
   const int nk = K / BK;
-  // the MFMAs of slab kt (W slot ws; fragments of its first k16 step already loaded)
-  auto slab = [&](int kt, int ws) {
+  // the MFMAs of one k16 step from fragment slot `cur`
+  auto step = [&](int cur) {
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      const int cur = ks & 1;
-      // the next step's fragment reads stay ahead of this step's MFMAs (left
-      // alone, the scheduler sinks each read onto its first use)
-      if (ks + 1 < BK / 16) frags(kt, ws, ks + 1, cur ^ 1);
-      __builtin_amdgcn_sched_barrier(0);
+    for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
-      for (int tm = 0; tm < TM; ++tm)
+      for (int tn = 0; tn < TN; ++tn)
+        acc.v[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cur][tm], fb[cur][tn], acc.v[tm][tn], 0, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  // the k16 steps of slab kt but its last (W slot ws; fragments of the first
+  // step already loaded), each reading the next step's fragments before its
+  // MFMAs (left alone, the scheduler sinks each read onto its first use)
+  constexpr int KS = BK / 16, LAST = (KS - 1) & 1;
+  auto head = [&](int kt, int ws) {
 #pragma unroll
-        for (int tn = 0; tn < TN; ++tn)
-          acc.v[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cur][tm], fb[cur][tn], acc.v[tm][tn], 0, 0, 0);
-      __builtin_amdgcn_sched_barrier(0);
+    for (int ks = 0; ks + 1 < KS; ++ks) {
+      frags(kt, ws, ks + 1, (ks & 1) ^ 1);
+      step(ks & 1);
     }
+  };
+  auto slab = [&](int kt, int ws) {
+    head(kt, ws);
+    step(LAST);
   };
   int wl = 0;  // W slot of the last slab
   if constexpr (WS == 2) {
@@ -532,7 +540,10 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __
     wl = (nk - 1) & 1;
   } else {
     // W slabs 0 and 1 ahead of A slab 0; past the last slab, W loads repeat
-    // the last one (in bounds, into a free slot, never read)
+    // the last one (in bounds, into a free slot, never read).  The last k16
+    // step of each slab runs after the slab barrier, from fragments read
+    // before it, and so covers the latency of the next slab's first
+    // fragment reads.
     issue_a(0, 0);
     issue_w(0, 0);
     issue_w(min(1, nk - 1) * BK, 1);
@@ -542,18 +553,20 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __
     frags(0, 0, 0, 0);
     int ws = 0;  // W slot of slab kt
     for (int kt = 0; kt + 1 < nk; ++kt) {
-      // A slot (kt+1)&1 was last read before the previous barrier, and so was
-      // W slot (kt+2)%3 (slab kt-1)
+      // A slot (kt+1)&1 and W slot (kt+2)%3 (slab kt-1) were last read
+      // before the previous barrier
       const int wn2 = ws == 0 ? 2 : ws - 1;
       issue_a((kt + 1) * BK, (kt + 1) & 1);
       issue_w(min(kt + 2, nk - 1) * BK, wn2);
-      slab(kt, ws);
-      // A(kt+1) and W(kt+1) landed; W(kt+2) may stay in flight across the barrier
+      head(kt, ws);
+      // A(kt+1) and W(kt+1) landed; W(kt+2) may stay in flight across the
+      // barrier; every wave's reads of slab kt are done
       __builtin_amdgcn_s_waitcnt((B_INST & 15) | ((B_INST >> 4) << 14) | 0x0070);
       __builtin_amdgcn_s_barrier();
       asm volatile("" ::: "memory");
       ws = ws == 2 ? 0 : ws + 1;
       frags(kt + 1, ws, 0, 0);
+      step(LAST);  // slab kt's last step
     }
     wl = ws;
   }
