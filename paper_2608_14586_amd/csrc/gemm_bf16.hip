@@ -678,9 +678,12 @@ hipError_t launch(const bf16_t* A, int lda, const WOperand& W, int M, int N, int
   // 64x64, two workgroups per CU)
   // 8-wave tiles at one workgroup per CU where they fill whole rounds: QKV
   // 256x192 (waves of 64x96) or 192x384 (96x96), GELU 192x256 (96x64).
-  // The 256x256 and 192x256 tiles keep three weight slabs in LDS (W two slabs
-  // ahead, 160 and 144 KB): A/B, us: gate/up 330.5 -> 328.4, ViT fc1 71.1 ->
-  // 69.4; the QKV 256x192 tiles measured slower that way (197.7 -> 198.7).
+  // The 256x256, 192x256 and 256x192 tiles keep three weight slabs in LDS (W
+  // two slabs ahead, 160, 144 and 136 KB), and so do the 128x128 residual
+  // tiles (80 KB, still two workgroups per CU).  A/B, us: gate/up 330.5 ->
+  // 328.4, ViT fc1 71.1 -> 69.4; with each slab's last k16 step after the
+  // barrier also QKV 196.6 -> 190.7, O-projection 79.8 -> 77.3, down 193.9 ->
+  // 184.9, ViT fc2 68.7 -> 64.9.
   auto rounds_of = [&](int bm, int bn) -> long {
     if (N % bn) return 0;
     const long t = (long)((M + bm - 1) / bm) * (N / bn);
@@ -688,7 +691,7 @@ hipError_t launch(const bf16_t* A, int lda, const WOperand& W, int M, int N, int
   };
   if constexpr (std::is_same<Epi, EpiQKV>::value) {
     if (const long t = rounds_of(256, 192)) {
-      hipLaunchKernelGGL((gemm_bf16_dma_kernel<256, 192, 64, 96, 8, WT, Epi>), dim3((unsigned)t), dim3(512), 0, s,
+      hipLaunchKernelGGL((gemm_bf16_dma_kernel<256, 192, 64, 96, 8, WT, Epi, 3>), dim3((unsigned)t), dim3(512), 0, s,
                          A, lda, W, M, N, a_parts * K, K, epi);
       return hipGetLastError();
     }
@@ -724,8 +727,12 @@ hipError_t launch(const bf16_t* A, int lda, const WOperand& W, int M, int N, int
   }
   if (!big) {
     int grid = ((M + 127) / 128) * ((N + 127) / 128);
-    hipLaunchKernelGGL((gemm_bf16_dma_kernel<128, 128, 64, 64, 4, WT, Epi>), dim3(grid), dim3(256), 0, s, A, lda, W,
-                       M, N, a_parts * K, K, epi);
+    if constexpr (std::is_same<Epi, EpiResidual>::value)
+      hipLaunchKernelGGL((gemm_bf16_dma_kernel<128, 128, 64, 64, 4, WT, Epi, 3>), dim3(grid), dim3(256), 0, s, A, lda,
+                         W, M, N, a_parts * K, K, epi);
+    else
+      hipLaunchKernelGGL((gemm_bf16_dma_kernel<128, 128, 64, 64, 4, WT, Epi>), dim3(grid), dim3(256), 0, s, A, lda, W,
+                         M, N, a_parts * K, K, epi);
   }
   return hipGetLastError();
 }
