@@ -300,7 +300,7 @@ struct EpiQKV {
       const int gr = m0 + row, p = n0 + gsel * 64;
       int kind, head, r;
       classify(p, kind, head, r);
-      if (gr >= M || kind == 3) continue;
+      if (gr >= M || kind == 3 || (kind == 2 && !q.v)) continue;
       const int c = r / 64;
       const int d1 = c * 32 + w, d2 = dh / 2 + c * 32 + w;
       const float* tr = T + row * NC + gsel * 64 + w;

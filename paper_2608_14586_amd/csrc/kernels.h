@@ -70,7 +70,7 @@ struct QkvArgs {
   const float* rope_sin;
   bf16_t* q;   // [B][H][L][dh]
   bf16_t* k;   // [B][Hkv][L][dh]
-  bf16_t* v;   // [B][Hkv][L][dh]
+  bf16_t* v;   // [B][Hkv][L][dh], NULL: V rows not written (V^T still is)
   bf16_t* vt;  // [B][Hkv][dh][ldvt] (V transposed, keys of each 16-group in the order
                // [0-3, 8-11, 4-7, 12-15], for the attention's PV product)
   int ldvt;

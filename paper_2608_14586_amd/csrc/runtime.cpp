@@ -338,7 +338,8 @@ void layout(vla_ctx* c, Bump& a) {
     w.q = a.take(M * s->hd * e);
     if (!s->llm()) {
       w.ek = a.take(M * s->kvd * e);
-      w.ev = a.take(M * s->kvd * e);
+      // the bf16 encoder's attention reads V^T only: no V rows
+      if (!s->bf16()) w.ev = a.take(M * s->kvd * e);
     }
     w.vt = a.take((size_t)s->c.max_batch * s->kvd * s->ldvt * e);
     w.o = a.take(M * s->hd * e);
@@ -735,7 +736,7 @@ Status enc_block(vla_ctx* c, const Stack::Block& w, int n_img, int L) {
   if (s.bf16()) {
     bf16_t* x = (bf16_t*)ws.x;
     PLAUNCH(c, VLA_STACK_ENC, VLA_K_NORM, vla::layernorm_bf16(ws.h, w.n1g, w.n1b, k.norm_eps, x, M, d, st));
-    vla::QkvArgs qa{w.b_qkv, nullptr, nullptr, (bf16_t*)ws.q, (bf16_t*)ws.ek, (bf16_t*)ws.ev, (bf16_t*)ws.vt,
+    vla::QkvArgs qa{w.b_qkv, nullptr, nullptr, (bf16_t*)ws.q, (bf16_t*)ws.ek, nullptr, (bf16_t*)ws.vt,
                     round_up(L, 64), L, k.n_heads, k.n_kv_heads, k.head_dim};
     PLAUNCH(c, VLA_STACK_ENC, VLA_K_QKV, vla::gemm_bf16_qkv(x, d, Stack::packed(w.w_qkv, s.qkv_n), qa, M, s.qkv_n, d, st));
     PLAUNCH(c, VLA_STACK_ENC, VLA_K_ATTN, vla::attention_bf16((const bf16_t*)ws.q, (const bf16_t*)ws.ek, (const bf16_t*)ws.vt, round_up(L, 64),
