@@ -375,15 +375,6 @@ struct EpiQKV {
 // slab the W issue repeats the last slab into a free slot, so that every
 // issue is unconditional.
 
-// Whether the kernel takes the wave index through a scalar register.  It then
-// keeps the LDS DMA destinations (M0) and the wave's fragment row offsets in
-// scalar arithmetic: fewer VGPRs and VALU instructions.  Measured per
-// epilogue on the bench shapes (A/B, us): SwiGLU 332.1 -> 327.7, residual
-// 80.6 -> 79.9 and 70.5 -> 69.6; the QKV and GELU products measured slower
-// (196.9 -> 199.1, 71.1 -> 71.9) and keep the vector form.
-template <class Epi>
-constexpr bool scalar_wave = !std::is_same<Epi, EpiQKV>::value && !std::is_same<Epi, EpiGelu>::value;
-
 __device__ __forceinline__ void buffer_load_lds16(__amdgpu_buffer_rsrc_t r, void* lds, unsigned voff) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, voff, 0, 0, 0);
 }
@@ -411,7 +402,12 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_dma_kernel(const bf16_t* __
   };
 
   const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = scalar_wave<Epi> ? __builtin_amdgcn_readfirstlane(tid >> 6) : tid >> 6;
+  // the wave index through a scalar register: the LDS DMA destinations (M0)
+  // and the wave's fragment row offsets stay scalar arithmetic (fewer VGPRs
+  // and VALU instructions).  A/B, us: SwiGLU 332.1 -> 327.7, residual 80.6
+  // -> 79.9; with three weight slots also QKV 200.4 -> 198.9 and GELU 72.2
+  // -> 70.7.
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;
 
   const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
