@@ -37,17 +37,18 @@ def _packed(W, N, K):
     return _dev_bf16(vb.vla_op_pack_weight_bf16(W, N, K))
 
 
-# Tile choices these shapes reach: one round of 96x128 (ViT proj / fc2, also
-# over ragged rows), one round of 128x128 (decoder O-projection / down at
-# L=2048), 64x128 (half a round of 128x128), 128x128 over ragged rows and
-# columns, single rows.
+# Tile choices these shapes reach: 128x128 over three quarters of a round
+# (ViT proj / fc2, also over ragged rows), one round of 128x128 (decoder
+# O-projection / down at L=2048), 64x128 (half a round of 128x128), 128x128
+# over ragged rows and columns, single rows.
 @pytest.mark.parametrize("M,N,K,bias", [(6144, 1024, 128, True), (6100, 1024, 64, True), (2048, 4096, 192, False),
                                         (1024, 4096, 128, False), (6104, 1000, 192, True), (77, 96, 64, True),
                                         (1, 4, 64, True), (130, 8, 128, False)])
 def test_gemm_residual_bf16(M, N, K, bias):
-    """H += A W^T + b through the fused residual epilogue (the residual tile
-    read behind the last K slab, the bias added before the park): element-wise
-    against float64, to the fp32 accumulation error."""
+    """H += A W^T + b through the fused residual epilogue (each lane's
+    residual read behind the last K slab, bias and residual added in the
+    accumulators): element-wise against float64, to the fp32 accumulation
+    error."""
     import torch
     from paper_2608_14586_amd import binding as vb
     A = synth.normal_bf16(synth.seed_of("resA", M, N, K), (M, K))
@@ -102,6 +103,82 @@ def test_gemm_bias_gelu_bf16(M, N, K, bias, gelu):
     err = np.abs(got - ref)
     worst = np.unravel_index(np.argmax(err / bound), err.shape)
     assert (err <= bound).all(), (worst, got[worst], ref[worst], bound[worst])
+
+
+def _sample_rows(M, tag, n=24):
+    """Tile edges plus seeded random rows of an M-row product."""
+    rng = np.random.default_rng(synth.seed_of("rows", M, *tag))
+    fixed = [0, 1, 127, 128, 191, 192, 255, 256, M // 2, M - 2, M - 1]
+    return np.unique(np.concatenate([[r for r in fixed if 0 <= r < M], rng.integers(0, M, n)]))
+
+
+# The products at their full K, in the launch configuration of the bench
+# frame: decoder down (K = 11008, 172 k-slabs) and O-projection (K = 4096) on
+# one round of three-slot 128x128 tiles, ViT fc2 (K = 4096) with its bias;
+# sampled rows against float64.
+@pytest.mark.parametrize("M,N,K,bias", [(2048, 4096, 11008, False), (2048, 4096, 4096, False),
+                                        (6144, 1024, 4096, True)])
+def test_gemm_residual_bf16_full_k(M, N, K, bias):
+    import torch
+    from paper_2608_14586_amd import binding as vb
+    tag = ("resfull", M, N, K)
+    A = synth.normal_bf16(synth.seed_of("A", *tag), (M, K))
+    W = synth.normal_bf16(synth.seed_of("W", *tag), (N, K), std=0.02)
+    H0 = synth.normal_f32(synth.seed_of("H", *tag), (M, N))
+    b = synth.normal_f32(synth.seed_of("b", *tag), (N,)) if bias else None
+    H = torch.from_numpy(H0.copy()).cuda()
+    vb.vla_op_gemm_residual_bf16(_dev_bf16(A), _packed(W, N, K), H, None if b is None else torch.from_numpy(b).cuda(),
+                                 M, N, K)
+    torch.cuda.synchronize()
+    rows = _sample_rows(M, tag)
+    a64 = synth.as_f32(A[rows]).astype(np.float64)
+    w64 = synth.as_f32(W).astype(np.float64)
+    prod = a64 @ w64.T
+    ref = H0[rows].astype(np.float64) + prod + (0.0 if b is None else b.astype(np.float64))
+    got = H.cpu().numpy()[rows].astype(np.float64)
+    # fp32 accumulation over K / 16 MFMA steps, each rounding the running sum
+    # once (K/16 2^-24 <= 2^-14 of the sum of |products|), with a factor 4; a
+    # dropped, doubled or misplaced k-slab is off by about sqrt(64) products,
+    # several times this bound
+    mag = np.abs(a64) @ np.abs(w64).T
+    bound = 2.0 ** -12 * mag + 2.0 ** -22 * np.abs(ref) + 1e-30
+    err = np.abs(got - ref)
+    worst = np.unravel_index(np.argmax(err / bound), err.shape)
+    assert (err <= bound).all(), (rows[worst[0]], worst[1], err[worst], bound[worst])
+    e = np.linalg.norm(got - ref) / np.linalg.norm(ref - H0[rows])
+    assert e < 1e-5, e
+
+
+# ViT fc1 + GELU at its full K (192x256 three-slot tiles, two whole rounds)
+# and the plain bias product over a two-round 256x256 grid; sampled rows.
+@pytest.mark.parametrize("M,N,K,gelu", [(6144, 4096, 1024, True), (2048, 16384, 4096, False)])
+def test_gemm_bias_gelu_bf16_full_k(M, N, K, gelu):
+    import torch
+    from paper_2608_14586_amd import binding as vb
+    tag = ("gelufull", M, N, K)
+    A = synth.normal_bf16(synth.seed_of("A", *tag), (M, K))
+    W = synth.normal_bf16(synth.seed_of("W", *tag), (N, K), std=0.05)
+    b = synth.normal_f32(synth.seed_of("b", *tag), (N,))
+    out = torch.empty((M, N), dtype=torch.int16, device="cuda")
+    vb.vla_op_gemm_bias_bf16(_dev_bf16(A), _packed(W, N, K), out, torch.from_numpy(b).cuda(), M, N, K, gelu)
+    torch.cuda.synchronize()
+    rows = _sample_rows(M, tag)
+    a64 = synth.as_f32(A[rows]).astype(np.float64)
+    w64 = synth.as_f32(W).astype(np.float64)
+    z = a64 @ w64.T + b.astype(np.float64)
+    ref = oracle.gelu_erf(z) if gelu else z
+    got = synth.as_f32(out.cpu().numpy()[rows].view(np.uint16)).astype(np.float64)
+    mag = np.abs(a64) @ np.abs(w64).T + np.abs(z)
+    # one bf16 rounding (2^-9, with a factor 2), the fp32 accumulation over
+    # K / 16 MFMA steps (2^-14 of mag, with a factor 4) through GELU's slope,
+    # and the erfc approximation
+    bound = 2.0 ** -8 * np.abs(ref) + 2.0 ** -12 * mag + (2e-7 * np.abs(z) if gelu else 0.0) + 1e-30
+    err = np.abs(got - ref)
+    worst = np.unravel_index(np.argmax(err / bound), err.shape)
+    assert (err <= bound).all(), (rows[worst[0]], worst[1], got[worst], ref[worst], bound[worst])
+    # over all sampled elements: the bf16 rounding alone (about 2^-9 / sqrt 3 rms)
+    e = np.linalg.norm(got - ref) / np.linalg.norm(ref)
+    assert e < 3e-3, e
 
 
 @pytest.mark.parametrize("B,H,Hkv,L,dh,causal", [
