@@ -224,8 +224,42 @@ def test_attention_bf16(B, H, Hkv, L, dh, causal):
         assert e < 1e-2, (b, e)
 
 
+def test_attention_bf16_vit_shape():
+    """The encoder's attention at the bench frame's shape (6 images x 16 heads
+    x 1024 patches, head dim 64, bidirectional), in its launch configuration;
+    sampled query rows of every image against the float64 oracle (a query's
+    output depends on its own row only), element-wise."""
+    import torch
+    from paper_2608_14586_amd import binding as vb
+    B, H, Hkv, L, dh = 6, 16, 16, 1024, 64
+    tag = ("vitattn", B, H, L, dh)
+    q = synth.normal_bf16(synth.seed_of("q", *tag), (B, H, L, dh))
+    k = synth.normal_bf16(synth.seed_of("k", *tag), (B, Hkv, L, dh))
+    v = synth.normal_bf16(synth.seed_of("v", *tag), (B, Hkv, L, dh))
+    ldvt = L
+    vt = np.zeros((B, Hkv, dh, ldvt), np.uint16)
+    cols = np.arange(L)
+    cols = (cols & ~12) | ((cols & 4) << 1) | ((cols & 8) >> 1)
+    vt[..., cols] = v.transpose(0, 1, 3, 2)
+    o = torch.empty((B, L, H * dh), dtype=torch.bfloat16, device="cuda")
+    vb.vla_op_attention_bf16(_dev_bf16(q), _dev_bf16(k), _dev_bf16(vt), ldvt, o, B, H, Hkv, L, dh, False)
+    torch.cuda.synchronize()
+    got = o.float().cpu().numpy()
+    for b in range(B):
+        rows = _sample_rows(L, tag + (b,), n=40)
+        q64, k64, v64 = (synth.as_f32(t[b]).transpose(1, 0, 2).astype(np.float64) for t in (q, k, v))
+        ref = oracle.attention(q64[rows], k64, v64, False).reshape(len(rows), H * dh)
+        mag = oracle.attention(q64[rows], k64, np.abs(v64), False).reshape(len(rows), H * dh)
+        err = np.abs(got[b][rows] - ref)
+        bound = 2.0 ** -7 * (np.abs(ref) + mag) + 1e-6
+        worst = np.unravel_index(np.argmax(err / bound), err.shape)
+        assert (err <= bound).all(), (b, rows[worst[0]], worst[1], err[worst], bound[worst])
+
+
 @pytest.mark.parametrize("M,d,ln", [(5, 256, False), (300, 896, False), (64, 4096, False), (70, 1024, True),
-                                    (9, 4096, True), (1, 4, False), (1, 4, True), (3, 36, True)])
+                                    (9, 4096, True), (1, 4, False), (1, 4, True), (3, 36, True),
+                                    # the bench frame's decoder RMSNorm and ViT LayerNorm
+                                    (2048, 4096, False), (6144, 1024, True)])
 def test_norms_bf16(M, d, ln):
     import torch
     from paper_2608_14586_amd import binding as vb
